@@ -1,0 +1,258 @@
+/*
+ * quads.h -- C ABI of libquads.so: the NVFP4 W4A4 MoE expert layer with
+ * Residual Activation Compensation (QUADS, arXiv 2607.15810, rollout side)
+ * as HIP kernels for AMD Instinct MI355X (gfx950).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every pointer named in a signature is a DEVICE pointer unless its
+ *    comment says "host".  The caller allocates and owns every buffer,
+ *    workspace included; the library allocates no device memory and keeps no
+ *    pointer after a call returns.
+ *  - Every call is asynchronous on `stream` (a hipStream_t passed as void*;
+ *    NULL is the default stream) and never synchronises with the host.
+ *  - Arguments are validated on the host before any launch; a failed check
+ *    returns a negative status and launches nothing.  QD_ERR_HIP means a
+ *    launch failed (the HIP error is not cleared).
+ *  - Device pointers must be 16-byte aligned; NVFP4 widths (`cols`, K) must
+ *    be multiples of 16.  Zero rows is a successful no-op.
+ *  - Results are deterministic: reductions use order-independent integer or
+ *    max arithmetic, permutations are computed by ranks, never by atomic slot
+ *    claims.  Calls running concurrently on different streams must not share
+ *    output or workspace buffers.
+ *
+ * NVFP4 tensor (Sec. 2.2 "FP4" paragraph of the paper): E2M1 element codes,
+ * one E4M3 scale per 16 consecutive elements along the contraction axis, and
+ * an FP32 tensor scale pair.
+ */
+#ifndef QUADS_H
+#define QUADS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__) || defined(__clang__)
+#pragma GCC visibility push(default)
+#endif
+
+typedef int qd_status;
+#define QD_OK               0
+#define QD_ERR_NULL        -1  /* a required pointer is NULL                */
+#define QD_ERR_SHAPE       -2  /* a size is negative, inconsistent or not a multiple of 16 */
+#define QD_ERR_ALIGN       -3  /* a device pointer is not 16-byte aligned   */
+#define QD_ERR_DTYPE       -4  /* unknown dtype / epilogue code             */
+#define QD_ERR_WORKSPACE   -5  /* workspace NULL or smaller than required   */
+#define QD_ERR_UNSUPPORTED -6  /* valid but unsupported combination         */
+#define QD_ERR_HIP         -7  /* a kernel launch failed                    */
+
+#define QD_DTYPE_BF16 0
+#define QD_DTYPE_F32  1
+
+#define QD_EPI_NONE   0   /* out[r][n] = bf16(alpha * acc)                    */
+#define QD_EPI_SWIGLU 1   /* out[r][j] = bf16(silu(g_j) * u_j), N = 2I         */
+
+/*
+ * An NVFP4 tensor: `groups` matrices of [rows][cols].  The struct itself is
+ * host memory; the three arrays are device memory owned by the caller.
+ *   codes  : uint8 [groups][rows][cols/2]; element 2i of a row in bits 3:0,
+ *            element 2i+1 in bits 7:4; a code is sign<<3 | E2M1 magnitude
+ *            index (magnitudes 0, .5, 1, 1.5, 2, 3, 4, 6).
+ *   scales : uint8 [groups][rows][cols/16]; E4M3FN bit patterns, sign 0.
+ *   gscale : float [groups][2] = {s_enc, s_dec}, the FP32 tensor scale pair.
+ * Element value: e2m1(code) * e4m3(scale) * s_dec.
+ */
+typedef struct {
+  uint8_t *codes;
+  uint8_t *scales;
+  float   *gscale;
+  int64_t  groups, rows, cols;
+} qd_nvfp4;
+
+const char *qd_status_string(qd_status s);
+int         qd_version(void);
+
+/* ---------------------------------------------------------------------
+ * nvfp4_quantize_act -- Q_A, the activation QDQ of Eq. (act-error-def)
+ * and Eq. (residual-def); format of Sec. 2.2.
+ *   x          : [rows][cols] bf16 (x_dtype QD_DTYPE_BF16) or f32.
+ *   amax_partials, n_partials : optional.  If non-NULL the tensor amax is the
+ *                maximum of these n_partials non-negative floats (a static
+ *                scale, or the per-block maxima another kernel produced);
+ *                if NULL it is max|x|, computed here.
+ *   out        : groups 1, rows, cols; written.
+ *   rac_scores : optional uint64 [cols].  If non-NULL the same pass also
+ *                computes the RAC channel scores of Eq. (channel-score)
+ *                (fixed point: sum over rows of trunc(fl32(r*r) * 2^F),
+ *                r = x_hat - x, F = 36 - 2e with amax = f*2^e) and
+ *                rac_ramax (float [1]) receives max|r|.  Requires
+ *                amax_partials == NULL and x_dtype bf16.  Both buffers are
+ *                zeroed by this call before use.
+ *   ws         : at least nvfp4_quantize_act_workspace(rows, cols) bytes.
+ * ------------------------------------------------------------------- */
+size_t    nvfp4_quantize_act_workspace(int64_t rows, int64_t cols);
+qd_status nvfp4_quantize_act(const void *x, int x_dtype, int64_t rows, int64_t cols,
+                             const float *amax_partials, int64_t n_partials,
+                             const qd_nvfp4 *out, uint64_t *rac_scores, float *rac_ramax,
+                             void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------
+ * nvfp4_quantize_weight -- Q_W of Eq. (weight-error-def), one tensor scale
+ * per group (expert matrix).  The same quantiser feeds the trainer-side
+ * fake-quant of Eq. (w4a16-qat-forward) through nvfp4_dequantize.
+ *   w   : bf16 [groups][rows][cols].
+ *   out : groups, rows, cols; written.
+ *   ws  : at least nvfp4_quantize_weight_workspace(groups, rows, cols) bytes.
+ * ------------------------------------------------------------------- */
+size_t    nvfp4_quantize_weight_workspace(int64_t groups, int64_t rows, int64_t cols);
+qd_status nvfp4_quantize_weight(const void *w, int64_t groups, int64_t rows, int64_t cols,
+                                const qd_nvfp4 *out, void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------
+ * nvfp4_dequantize -- QDQ output of Eq. (w4a16-qat-forward).
+ *   unscaled 0: out = fl32(fl32(e2m1 * e4m3) * s_dec), stored as out_dtype
+ *               (bf16 output rounds that float once, to nearest even);
+ *   unscaled 1: out = e2m1 * e4m3 exactly (s_dec left to the caller).
+ *   out : [groups][rows][cols] of out_dtype.
+ * ------------------------------------------------------------------- */
+qd_status nvfp4_dequantize(const qd_nvfp4 *in, int unscaled, void *out, int out_dtype,
+                           void *stream);
+
+/* ---------------------------------------------------------------------
+ * moe_route_permute -- top-k routing and the grouped-GEMM row order for
+ * the MoE layer (Sec. 3.3, the W13 site; Sec. 4.1 MoE model).
+ *   logits         : f32 [T][E], finite.
+ *   topk_ids       : int32 [T][k], experts by (logit desc, index asc).
+ *   topk_w         : f32 [T][k]; renorm 1: softmax over the k selected
+ *                    logits; renorm 0: full softmax probability.
+ *   expert_offsets : int32 [E+1], exclusive scan of per-expert row counts.
+ *   row_token      : int32 [T*k], token of each row; rows ordered by
+ *                    (expert asc, token asc).
+ *   inv_row        : int32 [T][k], row holding (t, topk_ids[t][s]).
+ *   1 <= k <= E <= 1024.
+ * ------------------------------------------------------------------- */
+size_t    moe_route_permute_workspace(int64_t T, int32_t E, int32_t k);
+qd_status moe_route_permute(const float *logits, int64_t T, int32_t E, int32_t k,
+                            int32_t renorm, int32_t *topk_ids, float *topk_w,
+                            int32_t *expert_offsets, int32_t *row_token, int32_t *inv_row,
+                            void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------
+ * rac_select_channels -- online channel selection and masked residual of
+ * Sec. 3.3: Eq. (channel-score), Eq. (channel-select), and the term
+ * M_S (.) Q_A(dX_q) of Eq. (residual-recon).
+ *   x, xq       : the bf16 activation [T][K] and its NVFP4 quantisation.
+ *   Ks          : number of channels to keep, 0 <= Ks <= K (k% = Ks / K).
+ *   scores      : uint64 [K]; ramax: float [1].  stats_ready 1: they hold
+ *                 the values nvfp4_quantize_act produced for (x, xq);
+ *                 stats_ready 0: this call computes them.
+ *   sel_idx     : int32 [Ks], the selected channels in ascending order
+ *                 (top Ks by score, ties to the lower index).
+ *   rq          : groups 1, T, K; written: the residual quantised over all
+ *                 channels with its own tensor scale, then codes outside S
+ *                 set to 0 and scales of blocks without a selected channel
+ *                 set to 0.
+ *   ws          : at least rac_select_channels_workspace(T, K) bytes.
+ *   K <= 65536.
+ * ------------------------------------------------------------------- */
+size_t    rac_select_channels_workspace(int64_t T, int64_t K);
+qd_status rac_select_channels(const void *x, const qd_nvfp4 *xq, int32_t Ks,
+                              uint64_t *scores, float *ramax, int32_t stats_ready,
+                              int32_t *sel_idx, const qd_nvfp4 *rq,
+                              void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------
+ * rac_residual_gemm -- the residual contraction of Eq. (residual-recon)
+ * pushed through the linear layer:
+ *   out[r][n] = s_dec_r * s_dec_w[e] * sum_{j in S} rhat[src(r)][j] * what[e][n][j]
+ * with rhat, what the unscaled NVFP4 values (exact), accumulated in f32.
+ *   rq, sel_idx, Ks : from rac_select_channels.
+ *   row_token       : int32 [rows] gather map (NULL: row r reads rq row r).
+ *   expert_offsets  : int32 [E+1] (NULL: one group, all rows).
+ *   w               : E groups of [N][K].
+ *   out             : f32 [rows][N].
+ * ------------------------------------------------------------------- */
+qd_status rac_residual_gemm(const qd_nvfp4 *rq, const int32_t *sel_idx, int32_t Ks,
+                            const int32_t *row_token, const int32_t *expert_offsets,
+                            int64_t rows, const qd_nvfp4 *w, float *out, void *stream);
+
+/* ---------------------------------------------------------------------
+ * moe_w4a4_grouped_gemm -- the W4A4 expert GEMM of Sec. 3.3 with the RAC
+ * residual fused (the main GEMM stays on NVFP4 codes, Sec. 3.3 "Targeted
+ * residual compensation"):
+ *   acc[r][n]  = sum_k a[src(r)][k] * w[e(r)][n][k]           (a, w NVFP4)
+ *   accr[r][n] = sum_{k in S} rq[src(r)][k] * w[e(r)][n][k]   (if rq)
+ *   v[r][n]    = s_dec_a*s_dec_w[e] * acc - s_dec_r*s_dec_w[e] * accr
+ * Products of decoded operands are exact; accumulation is f32.
+ *   a               : activations [*][K] (groups 1).
+ *   row_token       : int32 [rows] gather map (NULL: row r reads a row r).
+ *   expert_offsets  : int32 [E+1] row ranges per expert (NULL: E must be 1).
+ *   rows            : number of grouped rows (T*k for the MoE layer).
+ *   w               : E groups of [N][K].
+ *   rq, sel_idx, Ks : the masked residual (NULL / 0: plain W4A4).
+ *   epilogue        : QD_EPI_NONE: out bf16 [rows][N] = bf16(v);
+ *                     QD_EPI_SWIGLU: N = 2I, gate rows [0,I), up rows
+ *                     [I,2I); out bf16 [rows][I] = bf16(silu(g)*u).
+ *   amax_partials   : optional float [moe_w4a4_grouped_gemm_amax_count(...)]
+ *                     receiving per-workgroup maxima of |out| (as stored);
+ *                     their maximum is the tensor amax of out.
+ * ------------------------------------------------------------------- */
+int64_t   moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int32_t E, int32_t epilogue);
+qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
+                                const int32_t *expert_offsets, int32_t E, int64_t rows,
+                                const qd_nvfp4 *w, const qd_nvfp4 *rq,
+                                const int32_t *sel_idx, int32_t Ks, int32_t epilogue,
+                                void *out, float *amax_partials, void *stream);
+
+/* ---------------------------------------------------------------------
+ * moe_unpermute_combine -- weighted sum of the k expert outputs per token:
+ *   y[t][n] = bf16( sum_{s=0..k-1} topk_w[t][s] * z[inv_row[t][s]][n] ),
+ * accumulated in f32 in slot order.
+ *   z : bf16 [T*k][H]; y : bf16 [T][H].
+ * ------------------------------------------------------------------- */
+qd_status moe_unpermute_combine(const void *z, const int32_t *inv_row, const float *topk_w,
+                                int64_t T, int32_t k, int64_t H, void *y, void *stream);
+
+/* ---------------------------------------------------------------------
+ * qd_moe_layer_forward -- the whole rollout-side layer in one call: route,
+ * quantise X with fused RAC scores, select, W13 GEMM with fused residual
+ * and SwiGLU, quantise h, W2 GEMM, combine.  Equivalent to the seven calls
+ * above in that order.
+ *   x      : bf16 [T][H]; logits: f32 [T][E];
+ *   w13    : E groups of [2I][H]; w2: E groups of [H][I];
+ *   y      : bf16 [T][H];
+ *   ws     : at least qd_moe_layer_workspace(T, H, E, k, I) bytes; the
+ *            intermediates live there (see qd_moe_layer_views).
+ * ------------------------------------------------------------------- */
+size_t    qd_moe_layer_workspace(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I);
+qd_status qd_moe_layer_forward(const void *x, const float *logits, int64_t T, int64_t H,
+                               int32_t E, int32_t k, int64_t I, int32_t Ks, int32_t renorm,
+                               const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y,
+                               void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Byte offsets of the layer's intermediates inside its workspace (host
+ * output array `off`, QD_VIEW_COUNT entries), so a caller can inspect them
+ * after qd_moe_layer_forward.
+ */
+enum {
+  QD_VIEW_TOPK_IDS = 0, QD_VIEW_TOPK_W, QD_VIEW_OFFSETS, QD_VIEW_ROW_TOKEN, QD_VIEW_INV_ROW,
+  QD_VIEW_XQ_CODES, QD_VIEW_XQ_SCALES, QD_VIEW_XQ_GSCALE, QD_VIEW_SCORES, QD_VIEW_RAMAX,
+  QD_VIEW_SEL, QD_VIEW_RQ_CODES, QD_VIEW_RQ_SCALES, QD_VIEW_RQ_GSCALE, QD_VIEW_H,
+  QD_VIEW_H_AMAX, QD_VIEW_HQ_CODES, QD_VIEW_HQ_SCALES, QD_VIEW_HQ_GSCALE, QD_VIEW_Z,
+  QD_VIEW_COUNT
+};
+qd_status qd_moe_layer_views(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I,
+                             int64_t *off /* host, QD_VIEW_COUNT */);
+
+#if defined(__GNUC__) || defined(__clang__)
+#pragma GCC visibility pop
+#endif
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* QUADS_H */

@@ -1,0 +1,139 @@
+// The whole rollout-side MoE layer in one call (paper, Sec. 3.3): routing,
+// activation quantisation with fused RAC statistics, channel selection and
+// masked residual, W13 grouped GEMM with the fused residual and SwiGLU,
+// quantisation of h, W2 grouped GEMM, weighted combine.  Intermediates are
+// carved from the caller's workspace at the offsets qd_moe_layer_views gives.
+#include "common.h"
+
+namespace {
+
+struct Layout {
+  int64_t off[QD_VIEW_COUNT];
+  int64_t route_ws, q1_ws, sel_ws, q2_ws, total;
+};
+
+Layout make_layout(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I) {
+  Layout L{};
+  const int64_t R = T * k;
+  int64_t o = 0;
+  auto put = [&](int idx, int64_t bytes) {
+    L.off[idx] = o;
+    o += (int64_t)qdh::align_up((size_t)(bytes > 0 ? bytes : 1));
+  };
+  auto blob = [&](int64_t bytes) {
+    int64_t at = o;
+    o += (int64_t)qdh::align_up((size_t)(bytes > 0 ? bytes : 1));
+    return at;
+  };
+  put(QD_VIEW_TOPK_IDS, R * 4);
+  put(QD_VIEW_TOPK_W, R * 4);
+  put(QD_VIEW_OFFSETS, (int64_t)(E + 1) * 4);
+  put(QD_VIEW_ROW_TOKEN, R * 4);
+  put(QD_VIEW_INV_ROW, R * 4);
+  L.route_ws = blob((int64_t)moe_route_permute_workspace(T, E, k));
+  put(QD_VIEW_XQ_CODES, T * H / 2);
+  put(QD_VIEW_XQ_SCALES, T * H / 16);
+  put(QD_VIEW_XQ_GSCALE, 8);
+  L.q1_ws = blob((int64_t)nvfp4_quantize_act_workspace(T, H));
+  put(QD_VIEW_SCORES, H * 8);
+  put(QD_VIEW_RAMAX, 4);
+  put(QD_VIEW_SEL, H * 4);
+  L.sel_ws = blob((int64_t)rac_select_channels_workspace(T, H));
+  put(QD_VIEW_RQ_CODES, T * H / 2);
+  put(QD_VIEW_RQ_SCALES, T * H / 16);
+  put(QD_VIEW_RQ_GSCALE, 8);
+  put(QD_VIEW_H, R * I * 2);
+  put(QD_VIEW_H_AMAX, moe_w4a4_grouped_gemm_amax_count(R, 2 * I, E, QD_EPI_SWIGLU) * 4);
+  put(QD_VIEW_HQ_CODES, R * I / 2);
+  put(QD_VIEW_HQ_SCALES, R * I / 16);
+  put(QD_VIEW_HQ_GSCALE, 8);
+  L.q2_ws = blob((int64_t)nvfp4_quantize_act_workspace(R, I));
+  put(QD_VIEW_Z, R * H * 2);
+  L.total = o;
+  return L;
+}
+
+}  // namespace
+
+extern "C" size_t qd_moe_layer_workspace(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I) {
+  if (T < 0 || H <= 0 || E < 1 || k < 1 || I <= 0) return 0;
+  return (size_t)make_layout(T, H, E, k, I).total;
+}
+
+extern "C" qd_status qd_moe_layer_views(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I,
+                                        int64_t *off) {
+  if (!off) return QD_ERR_NULL;
+  if (T < 0 || H <= 0 || E < 1 || k < 1 || I <= 0) return QD_ERR_SHAPE;
+  Layout L = make_layout(T, H, E, k, I);
+  for (int i = 0; i < QD_VIEW_COUNT; ++i) off[i] = L.off[i];
+  return QD_OK;
+}
+
+extern "C" qd_status qd_moe_layer_forward(const void *x, const float *logits, int64_t T,
+                                          int64_t H, int32_t E, int32_t k, int64_t I,
+                                          int32_t Ks, int32_t renorm, const qd_nvfp4 *w13,
+                                          const qd_nvfp4 *w2, void *y, void *ws,
+                                          size_t ws_bytes, void *stream) {
+  if (!w13 || !w2) return QD_ERR_NULL;
+  if (T < 0 || H <= 0 || H % 32 || I <= 0 || I % 32 || E < 1 || k < 1 || k > E) return QD_ERR_SHAPE;
+  if (Ks < 0 || Ks > H) return QD_ERR_SHAPE;
+  qd_status st = qdh::check_nvfp4(w13, E, 2 * I, H);
+  if (st) return st;
+  st = qdh::check_nvfp4(w2, E, H, I);
+  if (st) return st;
+  if (T == 0) return QD_OK;
+  if (!x || !logits || !y) return QD_ERR_NULL;
+  if (!ws) return QD_ERR_WORKSPACE;
+  Layout L = make_layout(T, H, E, k, I);
+  if (ws_bytes < (size_t)L.total) return QD_ERR_WORKSPACE;
+  if (!qdh::aligned16(ws) || !qdh::aligned16(x) || !qdh::aligned16(y) || !qdh::aligned16(logits))
+    return QD_ERR_ALIGN;
+  if (qdh::fault_injected()) return QD_ERR_HIP;
+  char *b = static_cast<char *>(ws);
+  auto P = [&](int idx) { return b + L.off[idx]; };
+  const int64_t R = T * k;
+  int32_t *ids = (int32_t *)P(QD_VIEW_TOPK_IDS);
+  float *wts = (float *)P(QD_VIEW_TOPK_W);
+  int32_t *offs = (int32_t *)P(QD_VIEW_OFFSETS);
+  int32_t *row_token = (int32_t *)P(QD_VIEW_ROW_TOKEN);
+  int32_t *inv_row = (int32_t *)P(QD_VIEW_INV_ROW);
+
+  st = moe_route_permute(logits, T, E, k, renorm, ids, wts, offs, row_token, inv_row,
+                         b + L.route_ws, moe_route_permute_workspace(T, E, k), stream);
+  if (st) return st;
+
+  qd_nvfp4 xq{(uint8_t *)P(QD_VIEW_XQ_CODES), (uint8_t *)P(QD_VIEW_XQ_SCALES),
+              (float *)P(QD_VIEW_XQ_GSCALE), 1, T, H};
+  qd_nvfp4 rq{(uint8_t *)P(QD_VIEW_RQ_CODES), (uint8_t *)P(QD_VIEW_RQ_SCALES),
+              (float *)P(QD_VIEW_RQ_GSCALE), 1, T, H};
+  uint64_t *scores = (uint64_t *)P(QD_VIEW_SCORES);
+  float *ramax = (float *)P(QD_VIEW_RAMAX);
+  int32_t *sel = (int32_t *)P(QD_VIEW_SEL);
+  const bool rac = Ks > 0;
+  st = nvfp4_quantize_act(x, QD_DTYPE_BF16, T, H, nullptr, 0, &xq, rac ? scores : nullptr,
+                          rac ? ramax : nullptr, b + L.q1_ws,
+                          nvfp4_quantize_act_workspace(T, H), stream);
+  if (st) return st;
+  if (rac) {
+    st = rac_select_channels(x, &xq, Ks, scores, ramax, 1, sel, &rq, b + L.sel_ws,
+                             rac_select_channels_workspace(T, H), stream);
+    if (st) return st;
+  }
+  uint16_t *h = (uint16_t *)P(QD_VIEW_H);
+  float *hamax = (float *)P(QD_VIEW_H_AMAX);
+  st = moe_w4a4_grouped_gemm(&xq, row_token, offs, E, R, w13, rac ? &rq : nullptr,
+                             rac ? sel : nullptr, Ks, QD_EPI_SWIGLU, h, hamax, stream);
+  if (st) return st;
+  qd_nvfp4 hq{(uint8_t *)P(QD_VIEW_HQ_CODES), (uint8_t *)P(QD_VIEW_HQ_SCALES),
+              (float *)P(QD_VIEW_HQ_GSCALE), 1, R, I};
+  st = nvfp4_quantize_act(h, QD_DTYPE_BF16, R, I, hamax,
+                          moe_w4a4_grouped_gemm_amax_count(R, 2 * I, E, QD_EPI_SWIGLU), &hq,
+                          nullptr, nullptr, b + L.q2_ws, nvfp4_quantize_act_workspace(R, I),
+                          stream);
+  if (st) return st;
+  uint16_t *z = (uint16_t *)P(QD_VIEW_Z);
+  st = moe_w4a4_grouped_gemm(&hq, nullptr, offs, E, R, w2, nullptr, nullptr, 0, QD_EPI_NONE, z,
+                             nullptr, stream);
+  if (st) return st;
+  return moe_unpermute_combine(z, inv_row, wts, T, k, H, y, stream);
+}

@@ -1,0 +1,403 @@
+// Residual Activation Compensation (paper, Sec. 3.3):
+//   Eq. (channel-score)  s_j = ||dX_q[:, j]||_2 over the token batch,
+//   Eq. (channel-select) S = TopK(s_j), chosen online every forward,
+//   Eq. (residual-recon) X~ = Q_A(X) - M_S (.) Q_A(dX_q).
+//
+// Kernels:
+//   rac_amax_kernel / rac_scores_kernel  the score pass when the quantiser did
+//                        not fuse it (reads x and its NVFP4 codes, recomputes
+//                        r = x_hat - x, fixed-point u64 sums).
+//   rac_select_kernel    one workgroup: radix select of the K_s largest u64
+//                        scores (ties to the lower channel), ascending list and
+//                        a channel bitmap.
+//   rac_resq_kernel      residual quantised over all channels with its own
+//                        tensor scale (max|r|), then masked to S.
+//   rac_residual_gemm_kernel  the residual contraction over S alone (f32 out).
+#include "common.h"
+
+namespace {
+
+using namespace qd;
+
+constexpr int kMaxK = 65536;
+
+__device__ __forceinline__ void load_bf16x16(const uint16_t *p, float (&x)[16]) {
+  const uint4 *q = reinterpret_cast<const uint4 *>(p);
+  uint4 a = q[0], b = q[1];
+  uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    x[2 * j] = __uint_as_float(w[j] << 16);
+    x[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+  }
+}
+
+// residual r = fl(x_hat - x) of one 16-block from its codes and scale
+__device__ __forceinline__ void block_residual(const float (&x)[16], uint2 cw, uint32_t sb,
+                                               float s_dec, float (&r)[16]) {
+  const float sbf = e4m3_to_f32(sb);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    uint32_t c = ((i < 8 ? cw.x : cw.y) >> (4 * (i & 7))) & 15u;
+    r[i] = dequant_value(c, sbf, s_dec) - x[i];
+  }
+}
+
+__global__ __launch_bounds__(256) void rac_amax_kernel(const uint16_t *__restrict__ x,
+                                                       int64_t n16, float *__restrict__ part,
+                                                       uint64_t *__restrict__ scores, int64_t K,
+                                                       float *__restrict__ ramax) {
+  __shared__ float red[16];
+  float m = 0.0f;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < n16; b += stride) {
+    float v[16];
+    load_bf16x16(x + b * 16, v);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) m = fmaxf(m, fabsf(v[i]));
+  }
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < K; i += stride)
+    scores[i] = 0ull;
+  if (blockIdx.x == 0 && threadIdx.x == 0) ramax[0] = 0.0f;
+  m = block_max(m, red);
+  if (threadIdx.x == 0) part[blockIdx.x] = m;
+}
+
+// Same workgroup shape as the fused quantiser: 16 column blocks x 16 rows.
+__global__ __launch_bounds__(256) void rac_scores_kernel(
+    const uint16_t *__restrict__ x, const uint8_t *__restrict__ codes,
+    const uint8_t *__restrict__ scales, const float *__restrict__ gscale, int64_t T, int64_t K,
+    const float *__restrict__ part, int n_part, uint64_t *__restrict__ scores,
+    float *__restrict__ ramax) {
+  __shared__ float red[16];
+  __shared__ uint64_t acc_s[16][256];
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  float a = 0.0f;
+  for (int i = threadIdx.x; i < n_part; i += blockDim.x) a = fmaxf(a, part[i]);
+  const float amax = block_max(a, red);
+  int e;
+  frexpf(amax, &e);
+  const int F = 36 - 2 * e;
+  const float s_dec = gscale[1];
+  const int64_t nbc = K >> 4;
+  const int64_t cb = (int64_t)blockIdx.x * 16 + tx;
+  uint64_t acc[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0ull;
+  float rmax = 0.0f;
+  if (cb < nbc) {
+    for (int64_t t = (int64_t)blockIdx.y * 16 + ty; t < T; t += (int64_t)gridDim.y * 16) {
+      float v[16], r[16];
+      load_bf16x16(x + t * K + cb * 16, v);
+      uint2 cw = reinterpret_cast<const uint2 *>(codes + t * (K >> 1))[cb];
+      block_residual(v, cw, scales[t * nbc + cb], s_dec, r);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        rmax = fmaxf(rmax, fabsf(r[i]));
+        float sq = r[i] * r[i];
+        acc[i] += (uint64_t)ldexp((double)sq, F);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc_s[ty][tx * 16 + i] = acc[i];
+  __syncthreads();
+  uint64_t s = 0;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) s += acc_s[j][threadIdx.x];
+  const int64_t ch = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (ch < K && s != 0ull) atomicAdd((unsigned long long *)&scores[ch], (unsigned long long)s);
+  float m = block_max(rmax, red);
+  if (threadIdx.x == 0 && m > 0.0f)
+    atomicMax(reinterpret_cast<unsigned int *>(ramax), __float_as_uint(m));
+}
+
+// Block-wide exclusive scan of one int per thread (1024 threads).
+__device__ int block_exclusive_scan(int v, int *sh /* 1024 + 32 ints */, int &total) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  // inclusive scan inside the wave
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sh[1024 + wid] = x;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int w = 0; w < 16; ++w) {
+      int c = sh[1024 + w];
+      sh[1024 + w] = run;
+      run += c;
+    }
+    sh[1024 + 16] = run;
+  }
+  __syncthreads();
+  int res = x - v + sh[1024 + wid];
+  total = sh[1024 + 16];
+  __syncthreads();
+  return res;
+}
+
+// One workgroup of 1024 threads.  Radix select over 8-bit digits of the u64
+// keys finds the K_s-th largest score theta; channels above theta are taken,
+// then channels equal to theta in ascending index order until K_s.
+__global__ __launch_bounds__(1024) void rac_select_kernel(const uint64_t *__restrict__ scores,
+                                                          int K, int Ks,
+                                                          int32_t *__restrict__ sel_idx,
+                                                          uint32_t *__restrict__ bitmap) {
+  __shared__ int hist[256];
+  __shared__ int sh[1024 + 32];
+  __shared__ uint64_t s_prefix, s_mask;
+  __shared__ int s_remaining;
+  const int tid = threadIdx.x;
+  const int per = (K + 1023) / 1024;
+  const int j0 = tid * per, j1 = min(K, j0 + per);
+  for (int w = tid; w < (K + 31) / 32; w += 1024) bitmap[w] = 0u;
+  if (tid == 0) {
+    s_prefix = 0ull;
+    s_mask = 0ull;
+    s_remaining = Ks;
+  }
+  __syncthreads();
+  if (Ks > 0) {
+    for (int d = 7; d >= 0; --d) {
+      for (int i = tid; i < 256; i += 1024) hist[i] = 0;
+      __syncthreads();
+      const uint64_t pre = s_prefix, msk = s_mask;
+      for (int j = j0; j < j1; ++j) {
+        uint64_t v = scores[j];
+        if ((v & msk) == pre) atomicAdd(&hist[(int)((v >> (8 * d)) & 255ull)], 1);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        int rem = s_remaining, above = 0, dig = 0;
+        for (int v = 255; v >= 0; --v) {
+          if (above + hist[v] >= rem) {
+            dig = v;
+            break;
+          }
+          above += hist[v];
+        }
+        s_remaining = rem - above;
+        s_prefix = pre | ((uint64_t)dig << (8 * d));
+        s_mask = msk | (255ull << (8 * d));
+      }
+      __syncthreads();
+    }
+  }
+  const uint64_t theta = s_prefix;
+  const int take_eq = s_remaining;          // channels equal to theta to keep
+  // rank the channels equal to theta by index
+  int n_eq = 0;
+  if (Ks > 0)
+    for (int j = j0; j < j1; ++j) n_eq += (scores[j] == theta);
+  int tot;
+  int eq_before = block_exclusive_scan(n_eq, sh, tot);
+  // selection flags and their positions
+  int n_sel = 0;
+  {
+    int eq_seen = eq_before;
+    for (int j = j0; j < j1; ++j) {
+      uint64_t v = scores[j];
+      bool take = false;
+      if (Ks > 0) {
+        if (v > theta) take = true;
+        else if (v == theta) {
+          take = eq_seen < take_eq;
+          ++eq_seen;
+        }
+      }
+      n_sel += take;
+    }
+  }
+  int pos = block_exclusive_scan(n_sel, sh, tot);
+  {
+    int eq_seen = eq_before;
+    for (int j = j0; j < j1; ++j) {
+      uint64_t v = scores[j];
+      bool take = false;
+      if (Ks > 0) {
+        if (v > theta) take = true;
+        else if (v == theta) {
+          take = eq_seen < take_eq;
+          ++eq_seen;
+        }
+      }
+      if (take) {
+        sel_idx[pos++] = j;
+        atomicOr(&bitmap[j >> 5], 1u << (j & 31));
+      }
+    }
+  }
+}
+
+// Masked residual quantisation: one thread per 16-element block of [T][K].
+__global__ __launch_bounds__(256) void rac_resq_kernel(
+    const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
+    const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
+    const float *__restrict__ ramax, const uint32_t *__restrict__ bitmap,
+    uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales, float *__restrict__ rgs) {
+  const float amax_r = ramax[0];
+  float s_enc, s_dec;
+  tensor_scale(amax_r, s_enc, s_dec);
+  const bool zero_tensor = !(amax_r >= kZeroAmax);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    rgs[0] = s_enc;
+    rgs[1] = s_dec;
+  }
+  const float xs_dec = xgs[1];
+  const int64_t nbc = K >> 4;
+  const int64_t total = T * nbc;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < total; b += stride) {
+    const int64_t cb = b % nbc;
+    const uint32_t m16 = (bitmap[cb >> 1] >> (16 * (cb & 1))) & 0xFFFFu;
+    uint32_t lo = 0u, hi = 0u, sb = 0u;
+    if (m16) {
+      const int64_t t = b / nbc;
+      float v[16], r[16];
+      load_bf16x16(x + t * K + cb * 16, v);
+      uint2 cw = reinterpret_cast<const uint2 *>(xcodes)[b];
+      block_residual(v, cw, xscales[b], xs_dec, r);
+      sb = quantize_block(r, s_enc, zero_tensor, lo, hi);
+      uint32_t mlo = 0u, mhi = 0u;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if ((m16 >> i) & 1u) mlo |= 15u << (4 * i);
+        if ((m16 >> (i + 8)) & 1u) mhi |= 15u << (4 * i);
+      }
+      lo &= mlo;
+      hi &= mhi;
+    }
+    reinterpret_cast<uint2 *>(rcodes)[b] = make_uint2(lo, hi);
+    rscales[b] = (uint8_t)sb;
+  }
+}
+
+__device__ __forceinline__ float nvfp4_unscaled(const uint8_t *codes, const uint8_t *scales,
+                                                int64_t row, int64_t K, int64_t j) {
+  uint32_t byte = codes[row * (K >> 1) + (j >> 1)];
+  uint32_t c = (j & 1) ? (byte >> 4) : (byte & 15u);
+  float p = e2m1_value(c) * e4m3_to_f32(scales[row * (K >> 4) + (j >> 4)]);
+  return (c & 8u) ? -p : p;
+}
+
+// out[r][n] = s_dec_r * s_dec_w[e] * sum_{j in S} rhat[src][j] * what[e][n][j]
+__global__ __launch_bounds__(256) void rac_residual_gemm_kernel(
+    const uint8_t *__restrict__ rcodes, const uint8_t *__restrict__ rscales,
+    const float *__restrict__ rgs, const int32_t *__restrict__ sel, int Ks,
+    const int32_t *__restrict__ row_token, const int32_t *__restrict__ offsets, int E,
+    int64_t rows, const uint8_t *__restrict__ wcodes, const uint8_t *__restrict__ wscales,
+    const float *__restrict__ wgs, int64_t N, int64_t K, float *__restrict__ out) {
+  __shared__ int32_t s_sel[1024];
+  const int64_t r = blockIdx.x;
+  int e = 0;
+  if (offsets) {
+    while (e + 1 < E && r >= offsets[e + 1]) ++e;
+  }
+  const int64_t src = row_token ? row_token[r] : r;
+  const float alpha = rgs[1] * wgs[2 * e + 1];
+  const uint8_t *wc = wcodes + (int64_t)e * N * (K >> 1);
+  const uint8_t *ws = wscales + (int64_t)e * N * (K >> 4);
+  const int64_t n = (int64_t)blockIdx.y * blockDim.x + threadIdx.x;
+  float acc = 0.0f;
+  for (int base = 0; base < Ks; base += 1024) {
+    const int cnt = min(1024, Ks - base);
+    __syncthreads();
+    for (int i = threadIdx.x; i < cnt; i += blockDim.x) s_sel[i] = sel[base + i];
+    __syncthreads();
+    if (n < N)
+      for (int i = 0; i < cnt; ++i) {
+        const int j = s_sel[i];
+        acc += nvfp4_unscaled(rcodes, rscales, src, K, j) * nvfp4_unscaled(wc, ws, n, K, j);
+      }
+  }
+  if (n < N) out[r * N + n] = alpha * acc;
+}
+
+}  // namespace
+
+extern "C" size_t rac_select_channels_workspace(int64_t T, int64_t K) {
+  (void)T;
+  return qdh::align_up((size_t)((K + 31) / 32) * 4) + 256 * sizeof(float) + 256;
+}
+
+extern "C" qd_status rac_select_channels(const void *x, const qd_nvfp4 *xq, int32_t Ks,
+                                         uint64_t *scores, float *ramax, int32_t stats_ready,
+                                         int32_t *sel_idx, const qd_nvfp4 *rq, void *ws,
+                                         size_t ws_bytes, void *stream) {
+  if (!x || !xq || !scores || !ramax || !rq) return QD_ERR_NULL;
+  const int64_t T = xq->rows, K = xq->cols;
+  qd_status st = qdh::check_nvfp4(xq, 1, T, K);
+  if (st) return st;
+  st = qdh::check_nvfp4(rq, 1, T, K);
+  if (st) return st;
+  if (K > kMaxK || Ks < 0 || Ks > K) return QD_ERR_SHAPE;
+  if (Ks > 0 && !sel_idx) return QD_ERR_NULL;
+  if (!ws || ws_bytes < rac_select_channels_workspace(T, K)) return QD_ERR_WORKSPACE;
+  if (!qdh::aligned16(x) || !qdh::aligned16(scores) || !qdh::aligned16(ws) ||
+      (sel_idx && !qdh::aligned16(sel_idx)))
+    return QD_ERR_ALIGN;
+  if (qdh::fault_injected()) return QD_ERR_HIP;
+  hipStream_t s = qdh::S(stream);
+  uint32_t *bitmap = static_cast<uint32_t *>(ws);
+  float *part = reinterpret_cast<float *>(static_cast<char *>(ws) +
+                                          qdh::align_up((size_t)((K + 31) / 32) * 4));
+  const uint16_t *xb = static_cast<const uint16_t *>(x);
+  if (!stats_ready) {
+    const int64_t n16 = T * K / 16;
+    int g = (int)((n16 + 255) / 256);
+    if (g > 256) g = 256;
+    if (g < 1) g = 1;
+    hipLaunchKernelGGL(rac_amax_kernel, dim3(g), dim3(256), 0, s, xb, n16, part, scores, K, ramax);
+    if (T > 0) {
+      const int gx = (int)((K / 16 + 15) / 16);
+      int64_t gy = (T + 15) / 16;
+      int64_t lim = 256 / gx;
+      if (lim < 1) lim = 1;
+      if (gy > lim) gy = lim;
+      hipLaunchKernelGGL(rac_scores_kernel, dim3(gx, (unsigned)gy), dim3(256), 0, s, xb,
+                         xq->codes, xq->scales, xq->gscale, T, K, part, g, scores, ramax);
+    }
+  }
+  hipLaunchKernelGGL(rac_select_kernel, dim3(1), dim3(1024), 0, s, scores, (int)K, Ks, sel_idx,
+                     bitmap);
+  {
+    const int64_t total = T * (K / 16);
+    int64_t g = (total + 255) / 256;
+    if (g > 4096) g = 4096;
+    if (g < 1) g = 1;
+    hipLaunchKernelGGL(rac_resq_kernel, dim3((unsigned)g), dim3(256), 0, s, xb, xq->codes,
+                       xq->scales, xq->gscale, T, K, ramax, bitmap, rq->codes, rq->scales,
+                       rq->gscale);
+  }
+  return qdh::check_launch();
+}
+
+extern "C" qd_status rac_residual_gemm(const qd_nvfp4 *rq, const int32_t *sel_idx, int32_t Ks,
+                                       const int32_t *row_token, const int32_t *expert_offsets,
+                                       int64_t rows, const qd_nvfp4 *w, float *out,
+                                       void *stream) {
+  if (!rq || !w || !out) return QD_ERR_NULL;
+  if (Ks < 0 || Ks > rq->cols) return QD_ERR_SHAPE;
+  if (Ks > 0 && !sel_idx) return QD_ERR_NULL;
+  qd_status st = qdh::check_nvfp4(rq, 1, rq->rows, rq->cols);
+  if (st) return st;
+  st = qdh::check_nvfp4(w, w->groups, w->rows, rq->cols);
+  if (st) return st;
+  if (!expert_offsets && w->groups != 1) return QD_ERR_SHAPE;
+  if (!row_token && rows > rq->rows) return QD_ERR_SHAPE;
+  if (rows < 0) return QD_ERR_SHAPE;
+  if ((w->rows + 255) / 256 > 65535) return QD_ERR_UNSUPPORTED;
+  if (!qdh::aligned16(out)) return QD_ERR_ALIGN;
+  if (qdh::fault_injected()) return QD_ERR_HIP;
+  if (rows == 0 || w->rows == 0) return QD_OK;
+  hipStream_t s = qdh::S(stream);
+  const int64_t gy = (w->rows + 255) / 256;
+  hipLaunchKernelGGL(rac_residual_gemm_kernel, dim3((unsigned)rows, (unsigned)gy), dim3(256), 0, s,
+                     rq->codes, rq->scales, rq->gscale, sel_idx, Ks, row_token, expert_offsets,
+                     (int)w->groups, rows, w->codes, w->scales, w->gscale, w->rows, rq->cols, out);
+  return qdh::check_launch();
+}

@@ -1,0 +1,207 @@
+// Top-k expert routing and the canonical token -> row permutation of the
+// MoE layer (the paper's MoE rollout layer, Sec. 3.3 / Sec. 4.1; the router
+// itself is not specified there: top-k of the logits with ties to the lower
+// expert index, softmax weights over the selected logits).
+//
+// Two kernels, both over blocks of 256 tokens:
+//   route_topk_kernel   one wavefront per token: k rounds of a wave-wide
+//                       arg-max; per-block expert bitmasks in LDS give every
+//                       (token, slot) its rank among the block's tokens of the
+//                       same expert, and per-block expert counts.
+//   route_scatter_kernel scan of the counts -> expert offsets; row =
+//                       offset[e] + rows of e in earlier blocks + rank.
+// No atomic slot claims: the row order (expert asc, token asc) is a pure
+// function of the routing, so the permutation is bit-reproducible.
+#include "common.h"
+
+namespace {
+
+constexpr int kTokBlock = 256;
+constexpr int kMaxE = 1024;
+constexpr int kMaxK = 32;
+
+struct Cand {
+  float v;
+  int e;
+};
+// (value desc, index asc)
+__device__ __forceinline__ bool better(float v1, int e1, float v2, int e2) {
+  return v1 > v2 || (v1 == v2 && e1 < e2);
+}
+
+__global__ __launch_bounds__(256) void route_topk_kernel(
+    const float *__restrict__ logits, int64_t T, int E, int k, int renorm,
+    int32_t *__restrict__ ids, float *__restrict__ wts, int32_t *__restrict__ counts,
+    int32_t *__restrict__ ranks) {
+  __shared__ uint32_t mask[kMaxE][kTokBlock / 32];
+  __shared__ int32_t sel[kTokBlock][kMaxK];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int64_t t0 = (int64_t)blockIdx.x * kTokBlock;
+  for (int i = threadIdx.x; i < E * (kTokBlock / 32); i += blockDim.x)
+    (&mask[0][0])[i] = 0u;
+  __syncthreads();
+
+  const int per_lane = (E + 63) / 64;
+  for (int tl = wid; tl < kTokBlock; tl += 4) {
+    const int64_t t = t0 + tl;
+    if (t >= T) break;
+    float v[16];
+    for (int j = 0; j < 16; ++j) {
+      int e = lane + 64 * j;
+      v[j] = (j < per_lane && e < E) ? logits[t * E + e] : -INFINITY;
+    }
+    uint32_t used = 0u;
+    float top_v = 0.0f, denom = 0.0f, my_v = 0.0f;
+    int my_e = 0;
+    for (int s = 0; s < k; ++s) {
+      // best unused candidate of this lane
+      float bv = -INFINITY;
+      int be = 0x7fffffff;
+      for (int j = 0; j < per_lane; ++j) {
+        int e = lane + 64 * j;
+        if (e < E && !((used >> j) & 1u) && better(v[j], e, bv, be)) {
+          bv = v[j];
+          be = e;
+        }
+      }
+      // wave-wide arg-max; the order is total, so every lane ends with the winner
+      for (int o = 32; o > 0; o >>= 1) {
+        float ov = __shfl_xor(bv, o, 64);
+        int oe = __shfl_xor(be, o, 64);
+        if (better(ov, oe, bv, be)) {
+          bv = ov;
+          be = oe;
+        }
+      }
+      if ((be & 63) == lane) used |= 1u << (be >> 6);
+      if (s == 0) top_v = bv;
+      if (renorm) denom += expf(bv - top_v);        // slot order 0..k-1
+      if (lane == s) {
+        my_v = bv;
+        my_e = be;
+      }
+    }
+    if (!renorm) {           // full softmax denominator over all E experts
+      float part = 0.0f;
+      for (int j = 0; j < per_lane; ++j) {
+        int e = lane + 64 * j;
+        if (e < E) part += expf(v[j] - top_v);
+      }
+      for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
+      denom = part;
+    }
+    if (lane < k) {
+      ids[t * k + lane] = my_e;
+      wts[t * k + lane] = expf(my_v - top_v) / denom;
+      sel[tl][lane] = my_e;
+      atomicOr(&mask[my_e][tl >> 5], 1u << (tl & 31));
+    }
+  }
+  __syncthreads();
+  // per-block counts
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    int c = 0;
+#pragma unroll
+    for (int w = 0; w < kTokBlock / 32; ++w) c += __popc(mask[e][w]);
+    counts[(int64_t)blockIdx.x * E + e] = c;
+  }
+  // rank of (token, slot) among the block's tokens routed to the same expert
+  {
+    const int tl = threadIdx.x;
+    const int64_t t = t0 + tl;
+    if (t < T) {
+      for (int s = 0; s < k; ++s) {
+        const int e = sel[tl][s];
+        int r = 0;
+        for (int w = 0; w < (tl >> 5); ++w) r += __popc(mask[e][w]);
+        r += __popc(mask[e][tl >> 5] & ((1u << (tl & 31)) - 1u));
+        ranks[t * k + s] = r;
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void route_scatter_kernel(
+    int64_t T, int E, int k, int nblk, const int32_t *__restrict__ ids,
+    const int32_t *__restrict__ counts, const int32_t *__restrict__ ranks,
+    int32_t *__restrict__ offsets, int32_t *__restrict__ row_token,
+    int32_t *__restrict__ inv_row) {
+  __shared__ int32_t base[kMaxE];
+  __shared__ int32_t total[kMaxE];
+  const int b = blockIdx.x;
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    int tot = 0, pre = 0;
+    for (int bb = 0; bb < nblk; ++bb) {
+      int c = counts[(int64_t)bb * E + e];
+      tot += c;
+      if (bb < b) pre += c;
+    }
+    total[e] = tot;
+    base[e] = pre;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {            // exclusive scan over experts (E <= 1024)
+    int run = 0;
+    for (int e = 0; e < E; ++e) {
+      int c = total[e];
+      total[e] = run;
+      run += c;
+    }
+    if (b == 0) offsets[E] = run;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    if (b == 0) offsets[e] = total[e];
+    base[e] += total[e];
+  }
+  __syncthreads();
+  const int64_t t = (int64_t)b * kTokBlock + threadIdx.x;
+  if (t < T) {
+    for (int s = 0; s < k; ++s) {
+      const int e = ids[t * k + s];
+      const int row = base[e] + ranks[t * k + s];
+      row_token[row] = (int32_t)t;
+      inv_row[t * k + s] = row;
+    }
+  }
+}
+
+}  // namespace
+
+extern "C" size_t moe_route_permute_workspace(int64_t T, int32_t E, int32_t k) {
+  const int64_t nblk = (T + kTokBlock - 1) / kTokBlock;
+  return qdh::align_up((size_t)(nblk > 0 ? nblk : 1) * (E > 0 ? E : 1) * 4) +
+         qdh::align_up((size_t)(T > 0 ? T : 1) * (k > 0 ? k : 1) * 4);
+}
+
+extern "C" qd_status moe_route_permute(const float *logits, int64_t T, int32_t E, int32_t k,
+                                       int32_t renorm, int32_t *topk_ids, float *topk_w,
+                                       int32_t *expert_offsets, int32_t *row_token,
+                                       int32_t *inv_row, void *ws, size_t ws_bytes,
+                                       void *stream) {
+  if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E || k > kMaxK) return QD_ERR_SHAPE;
+  if (!expert_offsets) return QD_ERR_NULL;
+  if (T > 0 && (!logits || !topk_ids || !topk_w || !row_token || !inv_row)) return QD_ERR_NULL;
+  if (T * (int64_t)k > 0x7fffffffLL) return QD_ERR_SHAPE;
+  if (!ws || ws_bytes < moe_route_permute_workspace(T, E, k)) return QD_ERR_WORKSPACE;
+  if (!qdh::aligned16(logits) || !qdh::aligned16(topk_ids) || !qdh::aligned16(topk_w) ||
+      !qdh::aligned16(expert_offsets) || !qdh::aligned16(row_token) ||
+      !qdh::aligned16(inv_row) || !qdh::aligned16(ws))
+    return QD_ERR_ALIGN;   // (NULL is aligned)
+  if (qdh::fault_injected()) return QD_ERR_HIP;
+  hipStream_t s = qdh::S(stream);
+  if (T == 0) {
+    // offsets of an empty batch are all zero
+    qdi::launch_fill_i32(expert_offsets, E + 1, 0, s);
+    return qdh::check_launch();
+  }
+  const int nblk = (int)((T + kTokBlock - 1) / kTokBlock);
+  int32_t *counts = static_cast<int32_t *>(ws);
+  int32_t *ranks = reinterpret_cast<int32_t *>(static_cast<char *>(ws) +
+                                               qdh::align_up((size_t)nblk * E * 4));
+  hipLaunchKernelGGL(route_topk_kernel, dim3(nblk), dim3(256), 0, s, logits, T, E, k, renorm,
+                     topk_ids, topk_w, counts, ranks);
+  hipLaunchKernelGGL(route_scatter_kernel, dim3(nblk), dim3(256), 0, s, T, E, k, nblk,
+                     topk_ids, counts, ranks, expert_offsets, row_token, inv_row);
+  return qdh::check_launch();
+}

@@ -1,0 +1,246 @@
+"""The library's calls on torch tensors.
+
+torch provides device memory and the current HIP stream; each function
+allocates its outputs (and workspace) as torch tensors and hands raw device
+pointers to libquads.so.  Nothing here computes any part of the layer.
+"""
+
+from dataclasses import dataclass
+
+import torch
+
+from . import quads as Q
+
+
+def _stream():
+    return ctypes_void(torch.cuda.current_stream().cuda_stream)
+
+
+def ctypes_void(v):
+    return int(v) if v is not None else None
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _require_cuda(*ts):
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("libquads operates on GPU tensors")
+
+
+def _ws(nbytes, device):
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+@dataclass
+class NVFP4Tensor:
+    """codes uint8 [G][R][C/2], scales uint8 [G][R][C/16], gscale f32 [G][2]."""
+    codes: torch.Tensor
+    scales: torch.Tensor
+    gscale: torch.Tensor
+    groups: int
+    rows: int
+    cols: int
+
+    @staticmethod
+    def empty(groups, rows, cols, device):
+        return NVFP4Tensor(
+            torch.empty((groups, rows, cols // 2), dtype=torch.uint8, device=device),
+            torch.empty((groups, rows, cols // 16), dtype=torch.uint8, device=device),
+            torch.empty((groups, 2), dtype=torch.float32, device=device),
+            groups, rows, cols)
+
+    def struct(self):
+        return Q.NVFP4(self.codes.data_ptr(), self.scales.data_ptr(), self.gscale.data_ptr(),
+                       self.groups, self.rows, self.cols)
+
+    def ref(self):
+        import ctypes
+        s = self.struct()
+        self._keep = s
+        return ctypes.byref(s)
+
+
+def _nv(t):
+    if t is None:
+        return None
+    import ctypes
+    s = t.struct()
+    return ctypes.pointer(s)
+
+
+def quantize_act(x, amax_partials=None, rac=False):
+    """Q_A of x ([rows][cols] bf16 or f32).  With rac=True also returns the
+    fused RAC channel scores (uint64 as int64 tensor) and max|r| (float [1])."""
+    _require_cuda(x)
+    x = x.contiguous()
+    rows, cols = x.shape
+    dt = Q.QD_DTYPE_BF16 if x.dtype == torch.bfloat16 else Q.QD_DTYPE_F32
+    out = NVFP4Tensor.empty(1, rows, cols, x.device)
+    ws = _ws(Q.lib().nvfp4_quantize_act_workspace(rows, cols), x.device)
+    scores = ramax = None
+    if rac:
+        scores = torch.empty(cols, dtype=torch.int64, device=x.device)
+        ramax = torch.empty(1, dtype=torch.float32, device=x.device)
+    n_part = 0 if amax_partials is None else amax_partials.numel()
+    Q.call("nvfp4_quantize_act", x.data_ptr(), dt, rows, cols, _ptr(amax_partials), n_part,
+           _nv(out), _ptr(scores), _ptr(ramax), ws.data_ptr(), ws.numel(), _stream())
+    return out, scores, ramax
+
+
+def quantize_weight(w):
+    """Q_W of a bf16 bank [groups][rows][cols], one tensor scale per group."""
+    _require_cuda(w)
+    w = w.contiguous()
+    if w.dim() == 2:
+        w = w.unsqueeze(0)
+    G, R, C = w.shape
+    out = NVFP4Tensor.empty(G, R, C, w.device)
+    ws = _ws(Q.lib().nvfp4_quantize_weight_workspace(G, R, C), w.device)
+    Q.call("nvfp4_quantize_weight", w.data_ptr(), G, R, C, _nv(out), ws.data_ptr(), ws.numel(),
+           _stream())
+    return out
+
+
+def dequantize(t, unscaled=False, dtype=torch.float32):
+    out = torch.empty((t.groups, t.rows, t.cols), dtype=dtype, device=t.codes.device)
+    dt = Q.QD_DTYPE_BF16 if dtype == torch.bfloat16 else Q.QD_DTYPE_F32
+    Q.call("nvfp4_dequantize", _nv(t), int(unscaled), out.data_ptr(), dt, _stream())
+    return out
+
+
+def route_permute(logits, k, renorm=True):
+    _require_cuda(logits)
+    logits = logits.contiguous().float()
+    T, E = logits.shape
+    dev = logits.device
+    ids = torch.empty((T, k), dtype=torch.int32, device=dev)
+    w = torch.empty((T, k), dtype=torch.float32, device=dev)
+    offs = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    row_token = torch.empty(max(T * k, 1), dtype=torch.int32, device=dev)
+    inv_row = torch.empty((T, k), dtype=torch.int32, device=dev)
+    ws = _ws(Q.lib().moe_route_permute_workspace(T, E, k), dev)
+    Q.call("moe_route_permute", logits.data_ptr(), T, E, k, int(renorm), ids.data_ptr(),
+           w.data_ptr(), offs.data_ptr(), row_token.data_ptr(), inv_row.data_ptr(),
+           ws.data_ptr(), ws.numel(), _stream())
+    return ids, w, offs, row_token[:T * k], inv_row
+
+
+def select_channels(x, xq, Ks, scores=None, ramax=None):
+    """RAC selection + masked residual.  scores/ramax from quantize_act(rac=True)
+    are used as given; otherwise they are computed here."""
+    _require_cuda(x)
+    T, K = x.shape
+    dev = x.device
+    ready = scores is not None
+    if not ready:
+        scores = torch.empty(K, dtype=torch.int64, device=dev)
+        ramax = torch.empty(1, dtype=torch.float32, device=dev)
+    sel = torch.empty(max(Ks, 1), dtype=torch.int32, device=dev)
+    rq = NVFP4Tensor.empty(1, T, K, dev)
+    ws = _ws(Q.lib().rac_select_channels_workspace(T, K), dev)
+    Q.call("rac_select_channels", x.data_ptr(), _nv(xq), Ks, scores.data_ptr(), ramax.data_ptr(),
+           int(ready), sel.data_ptr(), _nv(rq), ws.data_ptr(), ws.numel(), _stream())
+    return sel[:Ks], rq, scores, ramax
+
+
+def residual_gemm(rq, sel, w, rows, row_token=None, offsets=None):
+    dev = rq.codes.device
+    out = torch.empty((rows, w.rows), dtype=torch.float32, device=dev)
+    Q.call("rac_residual_gemm", _nv(rq), _ptr(sel), int(sel.numel()), _ptr(row_token),
+           _ptr(offsets), rows, _nv(w), out.data_ptr(), _stream())
+    return out
+
+
+def grouped_gemm(a, w, rows, row_token=None, offsets=None, rq=None, sel=None,
+                 epilogue=Q.QD_EPI_NONE, want_amax=False):
+    dev = a.codes.device
+    E = w.groups
+    N = w.rows
+    ncol = N // 2 if epilogue == Q.QD_EPI_SWIGLU else N
+    out = torch.empty((rows, ncol), dtype=torch.bfloat16, device=dev)
+    amax = None
+    if want_amax:
+        cnt = Q.lib().moe_w4a4_grouped_gemm_amax_count(rows, N, E, epilogue)
+        amax = torch.empty(max(cnt, 1), dtype=torch.float32, device=dev)
+    Ks = 0 if sel is None else int(sel.numel())
+    Q.call("moe_w4a4_grouped_gemm", _nv(a), _ptr(row_token), _ptr(offsets), E, rows, _nv(w),
+           _nv(rq) if Ks else None, _ptr(sel) if Ks else None, Ks, epilogue, out.data_ptr(),
+           _ptr(amax), _stream())
+    return out, amax
+
+
+def unpermute_combine(z, inv_row, w):
+    T, k = inv_row.shape
+    H = z.shape[1]
+    y = torch.empty((T, H), dtype=torch.bfloat16, device=z.device)
+    Q.call("moe_unpermute_combine", z.data_ptr(), inv_row.data_ptr(), w.data_ptr(), T, k, H,
+           y.data_ptr(), _stream())
+    return y
+
+
+class MoELayer:
+    """The whole layer through qd_moe_layer_forward, with a reusable
+    workspace; `views()` exposes the intermediates of the last call."""
+
+    def __init__(self, w13, w2, T, k, Ks, renorm=True):
+        self.w13, self.w2 = w13, w2
+        self.E = w13.groups
+        self.I = w13.rows // 2
+        self.H = w13.cols
+        self.T, self.k, self.Ks, self.renorm = T, k, Ks, renorm
+        dev = w13.codes.device
+        n = Q.lib().qd_moe_layer_workspace(T, self.H, self.E, k, self.I)
+        self.ws = _ws(n, dev)
+        import ctypes
+        off = (ctypes.c_int64 * len(Q.VIEW_NAMES))()
+        Q.call("qd_moe_layer_views", T, self.H, self.E, k, self.I, off)
+        self.off = list(off)
+        self._s13 = w13.struct()
+        self._s2 = w2.struct()
+
+    def __call__(self, x, logits, y=None):
+        import ctypes
+        if y is None:
+            y = torch.empty((self.T, self.H), dtype=torch.bfloat16, device=x.device)
+        Q.call("qd_moe_layer_forward", x.data_ptr(), logits.data_ptr(), self.T, self.H, self.E,
+               self.k, self.I, self.Ks, int(self.renorm), ctypes.byref(self._s13),
+               ctypes.byref(self._s2), y.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
+               _stream())
+        return y
+
+    def view(self, name, dtype, shape):
+        i = Q.VIEW_NAMES.index(name)
+        nbytes = 1
+        for s in shape:
+            nbytes *= s
+        nbytes *= torch.tensor([], dtype=dtype).element_size()
+        start = self.off[i]
+        return self.ws[start:start + nbytes].view(dtype).view(*shape)
+
+    def views(self):
+        T, H, E, k, I = self.T, self.H, self.E, self.k, self.I
+        R = T * k
+        u8, i32, f32 = torch.uint8, torch.int32, torch.float32
+        return dict(
+            ids=self.view("topk_ids", i32, (T, k)), w=self.view("topk_w", f32, (T, k)),
+            offsets=self.view("offsets", i32, (E + 1,)),
+            row_token=self.view("row_token", i32, (R,)),
+            inv_row=self.view("inv_row", i32, (T, k)),
+            xq_codes=self.view("xq_codes", u8, (T, H // 2)),
+            xq_scales=self.view("xq_scales", u8, (T, H // 16)),
+            xq_gscale=self.view("xq_gscale", f32, (2,)),
+            scores=self.view("scores", torch.int64, (H,)),
+            ramax=self.view("ramax", f32, (1,)),
+            sel=self.view("sel", i32, (self.Ks,)),
+            rq_codes=self.view("rq_codes", u8, (T, H // 2)),
+            rq_scales=self.view("rq_scales", u8, (T, H // 16)),
+            rq_gscale=self.view("rq_gscale", f32, (2,)),
+            h=self.view("h", torch.bfloat16, (R, I)),
+            hq_codes=self.view("hq_codes", u8, (R, I // 2)),
+            hq_scales=self.view("hq_scales", u8, (R, I // 16)),
+            hq_gscale=self.view("hq_gscale", f32, (2,)),
+            z=self.view("z", torch.bfloat16, (R, H)),
+        )

@@ -1,0 +1,73 @@
+"""Shared helpers for the GPU parity tests: conversions from device tensors
+to the oracle's numpy representation and the GEMM tolerance check."""
+
+import numpy as np
+import torch
+
+from oracle import formats, quant
+
+
+def np_bf16(t):
+    """bf16 torch tensor -> float32 numpy (exact)."""
+    return t.detach().float().cpu().numpy()
+
+
+def nv_host(t):
+    """NVFP4Tensor -> dict of numpy arrays (packed codes, scales, gscale)."""
+    return dict(packed=t.codes.cpu().numpy(), scales=t.scales.cpu().numpy(),
+                gscale=t.gscale.cpu().numpy())
+
+
+def oracle_nv(q):
+    """oracle quantize() result -> (packed, scales, gscale) shaped like the GPU."""
+    return q["packed"], q["scales"], np.array([q["s_enc"], q["s_dec"]], np.float32)
+
+
+def assert_nvfp4_equal(gpu, ref, name=""):
+    """Bit-exact comparison of one NVFP4 group: codes, scales, tensor scales."""
+    g = nv_host(gpu) if not isinstance(gpu, dict) else gpu
+    rp, rs, rg = oracle_nv(ref)
+    gp = g["packed"].reshape(rp.shape)
+    gs = g["scales"].reshape(rs.shape)
+    bad_c = np.count_nonzero(gp != rp)
+    bad_s = np.count_nonzero(gs != rs)
+    assert bad_s == 0, f"{name}: {bad_s} block scales differ (first at {np.argwhere(gs != rs)[:3]})"
+    assert bad_c == 0, f"{name}: {bad_c} code bytes differ (first at {np.argwhere(gp != rp)[:3]})"
+    gg = g["gscale"].reshape(-1)[:2]
+    assert gg.view(np.uint32).tolist() == rg.view(np.uint32).tolist(), f"{name}: gscale {gg} vs {rg}"
+
+
+def unpack_gpu(t, group=0):
+    """GPU NVFP4Tensor group -> oracle-style dict with unpacked codes."""
+    codes = quant.unpack(t.codes[group].cpu().numpy())
+    gs = t.gscale[group].cpu().numpy()
+    return dict(codes=codes, scales=t.scales[group].cpu().numpy(), s_enc=gs[0], s_dec=gs[1])
+
+
+def check_close_bf16(gpu, ref64, mag64, name, rel_l2=1e-3, floor=2.0 ** -20):
+    """GEMM-output tolerance.
+
+    gpu: bf16 values (float array); ref64: the oracle's float64 values;
+    mag64: sum of |products| behind each value.  Passes if the relative L2
+    error against the bf16-rounded reference is <= rel_l2 and every element
+    is within 2 bf16 ulp of it plus floor * mag (the float32 accumulation
+    error of a near-cancelling sum, which no bf16 ulp bound can cover).
+    """
+    gpu = np.asarray(gpu, np.float64)
+    refb = formats.bf16_round_f64(ref64)
+    diff = np.abs(gpu - refb)
+    nrm = np.linalg.norm(refb)
+    rel = np.linalg.norm(gpu - refb) / (nrm if nrm > 0 else 1.0)
+    assert rel <= rel_l2, f"{name}: rel-L2 {rel:.3e} > {rel_l2}"
+    bound = 2 * formats.ulp_bf16(refb) + floor * np.asarray(mag64, np.float64)
+    bad = diff > bound
+    if bad.any():
+        i = np.argwhere(bad)[0]
+        raise AssertionError(
+            f"{name}: {bad.sum()} of {bad.size} elements outside tolerance; first {tuple(i)}: "
+            f"gpu {gpu[tuple(i)]!r} ref {ref64[tuple(i)]!r} bound {bound[tuple(i)]!r}")
+    return rel
+
+
+def bf16_tensor(a, device="cuda"):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16).to(device)

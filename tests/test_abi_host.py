@@ -1,0 +1,167 @@
+"""Host-only checks of the C ABI (no GPU needed): the library loads, exports
+every function include/quads.h declares, and rejects invalid arguments with
+the documented status codes before touching the GPU."""
+
+import ctypes
+import os
+import re
+import subprocess
+import sys
+
+import pytest
+
+from paper_2607_15810_amd import quads as Q
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "quads.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w]*\s*\*?\s*([a-z_][a-z0-9_]*)\s*\(", src,
+                       flags=re.M)
+    return sorted(set(n for n in names if n not in ("if", "defined")))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(Q.LIB_PATH):
+        pytest.fail("libquads.so is not built (python -m paper_2607_15810_amd.build)")
+    return Q.lib()
+
+
+def test_header_declares_the_seven_calls():
+    names = declared_functions()
+    for n in ["nvfp4_quantize_act", "nvfp4_quantize_weight", "moe_route_permute",
+              "moe_w4a4_grouped_gemm", "rac_select_channels", "rac_residual_gemm",
+              "moe_unpermute_combine"]:
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", Q.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    exported = set(l.split()[-1] for l in out.splitlines() if " T " in l)
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, missing
+    for n in declared_functions():
+        assert n in Q.SIGNATURES, f"binding lacks {n}"
+    # nothing else leaks out of the library
+    assert exported == set(declared_functions())
+
+
+def test_status_strings(lib):
+    assert Q.status_string(0) == "ok"
+    for st in range(-7, 0):
+        assert Q.status_string(st) not in ("ok", "unknown status")
+    assert lib.qd_version() >= 1
+
+
+def _nv(groups, rows, cols, ptr=16):
+    return Q.NVFP4(ptr, ptr, ptr, groups, rows, cols)
+
+
+FAKE = 1 << 20            # an aligned, never-dereferenced address
+
+
+def test_quantize_act_validation(lib):
+    nv = _nv(1, 4, 32, FAKE)
+    ws = lib.nvfp4_quantize_act_workspace(4, 32)
+    r = lambda *a: Q.raw("nvfp4_quantize_act", *a)
+    assert r(FAKE, 0, 4, 30, None, 0, ctypes.byref(_nv(1, 4, 30, FAKE)), None, None, FAKE, ws,
+             None) == Q.QD_ERR_SHAPE
+    assert r(FAKE, 7, 4, 32, None, 0, ctypes.byref(nv), None, None, FAKE, ws, None) == Q.QD_ERR_DTYPE
+    assert r(None, 0, 4, 32, None, 0, ctypes.byref(nv), None, None, FAKE, ws, None) == Q.QD_ERR_NULL
+    assert r(FAKE + 2, 0, 4, 32, None, 0, ctypes.byref(nv), None, None, FAKE, ws,
+             None) == Q.QD_ERR_ALIGN
+    assert r(FAKE, 0, 4, 32, None, 0, ctypes.byref(nv), None, None, FAKE, ws - 1,
+             None) == Q.QD_ERR_WORKSPACE
+    assert r(FAKE, 0, 4, 32, None, 0, ctypes.byref(_nv(1, 5, 32, FAKE)), None, None, FAKE, ws,
+             None) == Q.QD_ERR_SHAPE
+    # RAC statistics need an internally computed amax and bf16 input
+    assert r(FAKE, 0, 4, 32, FAKE, 1, ctypes.byref(nv), FAKE, FAKE, FAKE, ws,
+             None) == Q.QD_ERR_UNSUPPORTED
+    assert r(FAKE, 1, 4, 32, None, 0, ctypes.byref(nv), FAKE, FAKE, FAKE, ws,
+             None) == Q.QD_ERR_UNSUPPORTED
+    # zero rows: a no-op that touches nothing
+    assert r(None, 0, 0, 32, None, 0, ctypes.byref(_nv(1, 0, 32, 0)), None, None, FAKE, ws,
+             None) == Q.QD_OK
+
+
+def test_route_validation(lib):
+    ws = lib.moe_route_permute_workspace(8, 16, 4)
+    r = lambda *a: Q.raw("moe_route_permute", *a)
+    args = [FAKE] * 6
+    assert r(FAKE, 8, 16, 0, 1, *args[:5], FAKE, ws, None) == Q.QD_ERR_SHAPE     # k = 0
+    assert r(FAKE, 8, 16, 17, 1, *args[:5], FAKE, ws, None) == Q.QD_ERR_SHAPE    # k > E
+    assert r(FAKE, 8, 2000, 4, 1, *args[:5], FAKE, ws, None) == Q.QD_ERR_SHAPE   # E > 1024
+    assert r(None, 8, 16, 4, 1, *args[:5], FAKE, ws, None) == Q.QD_ERR_NULL
+    assert r(FAKE, 8, 16, 4, 1, *args[:5], FAKE, 8, None) == Q.QD_ERR_WORKSPACE
+
+
+def test_gemm_validation(lib):
+    a = _nv(1, 16, 256, FAKE)
+    w = _nv(4, 128, 256, FAKE)
+    r = lambda *x: Q.raw("moe_w4a4_grouped_gemm", *x)
+    assert r(ctypes.byref(a), None, FAKE, 4, 16, ctypes.byref(w), None, None, 0, 5, FAKE,
+             None, None) == Q.QD_ERR_DTYPE
+    assert r(ctypes.byref(a), None, None, 4, 16, ctypes.byref(w), None, None, 0, 0, FAKE,
+             None, None) == Q.QD_ERR_SHAPE          # E > 1 needs offsets
+    w_badk = _nv(4, 128, 128, FAKE)
+    assert r(ctypes.byref(a), None, FAKE, 4, 16, ctypes.byref(w_badk), None, None, 0, 0, FAKE,
+             None, None) == Q.QD_ERR_SHAPE
+    w_odd = _nv(4, 40, 256, FAKE)                  # SwiGLU needs N % 32 == 0
+    assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w_odd), None, None, 0, 1, FAKE,
+             None, None) == Q.QD_ERR_SHAPE
+    rq = _nv(1, 16, 256, FAKE)
+    assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w), ctypes.byref(rq), None, 4, 0,
+             FAKE, None, None) == Q.QD_ERR_NULL     # residual without channel list
+    assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w), None, None, 0, 0, FAKE + 8,
+             None, None) == Q.QD_ERR_ALIGN
+    assert lib.moe_w4a4_grouped_gemm_amax_count(64, 256, 4, 1) > 0
+
+
+def test_select_and_combine_validation(lib):
+    xq = _nv(1, 8, 64, FAKE)
+    rq = _nv(1, 8, 64, FAKE)
+    ws = lib.rac_select_channels_workspace(8, 64)
+    r = lambda *x: Q.raw("rac_select_channels", *x)
+    assert r(FAKE, ctypes.byref(xq), 65, FAKE, FAKE, 1, FAKE, ctypes.byref(rq), FAKE, ws,
+             None) == Q.QD_ERR_SHAPE                 # K_s > K
+    assert r(FAKE, ctypes.byref(xq), 4, FAKE, FAKE, 1, None, ctypes.byref(rq), FAKE, ws,
+             None) == Q.QD_ERR_NULL
+    assert r(FAKE, ctypes.byref(xq), 4, FAKE, FAKE, 1, FAKE, ctypes.byref(rq), FAKE, 0,
+             None) == Q.QD_ERR_WORKSPACE
+    c = lambda *x: Q.raw("moe_unpermute_combine", *x)
+    assert c(FAKE, FAKE, FAKE, 4, 2, 12, FAKE, None) == Q.QD_ERR_SHAPE     # H % 8
+    assert c(None, None, None, 0, 2, 16, None, None) == Q.QD_OK           # empty batch
+
+
+def test_layer_workspace_and_views(lib):
+    n = lib.qd_moe_layer_workspace(256, 2048, 128, 8, 768)
+    assert n > 256 * 8 * 2048 * 2             # holds z
+    off = (ctypes.c_int64 * len(Q.VIEW_NAMES))()
+    assert Q.raw("qd_moe_layer_views", 256, 2048, 128, 8, 768, off) == Q.QD_OK
+    o = list(off)
+    assert o == sorted(o) and len(set(o)) == len(o)
+    assert all(v % 256 == 0 for v in o) and o[-1] < n
+
+
+def test_injected_launch_failure():
+    """QD_FAULT_INJECT=launch makes every launching call return QD_ERR_HIP
+    after argument checks (run in a subprocess so the env is isolated)."""
+    code = (
+        "import ctypes\n"
+        "from paper_2607_15810_amd import quads as Q\n"
+        "L = Q.lib()\n"
+        "F = 1 << 20\n"
+        "nv = Q.NVFP4(F, F, F, 1, 4, 32)\n"
+        "ws = L.nvfp4_quantize_act_workspace(4, 32)\n"
+        "st = Q.raw('nvfp4_quantize_act', F, 0, 4, 32, None, 0, ctypes.byref(nv), None, None, F, ws, None)\n"
+        "print(st)\n")
+    env = dict(os.environ, QD_FAULT_INJECT="launch")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env,
+                         cwd=ROOT, timeout=120)
+    assert out.returncode == 0, out.stderr
+    assert int(out.stdout.strip().splitlines()[-1]) == Q.QD_ERR_HIP

@@ -1,0 +1,263 @@
+"""GPU parity: every step of the HIP path against the CPU oracle.
+
+Codes, scales, tensor scales, routing ids, the permutation and the channel
+selection must match bit for bit; contraction outputs must pass the
+tolerance of helpers.check_close_bf16 (rel-L2 <= 1e-3 and 2 bf16 ulp per
+element plus a 2^-20 * sum|products| floor).  Later stages are
+teacher-forced with the GPU's own intermediates (the oracle recomputes stage
+i from the GPU's stage i-1 output), and the whole layer is also compared
+free-running.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import layer as OL, quant as OQ, rac as OR, route as ORt
+from paper_2607_15810_amd import ops, synth
+from paper_2607_15810_amd import quads as Q
+
+from helpers import (assert_nvfp4_equal, bf16_tensor, check_close_bf16, np_bf16, unpack_gpu)
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    Q.lib()          # the HIP library must load; there is no fallback
+    yield
+
+
+def _bank_oracle(gpu_bank):
+    """Oracle-style bank dict from a GPU NVFP4 bank (after bit-exact checks)."""
+    codes = np.stack([OQ.unpack(c) for c in gpu_bank.codes.cpu().numpy()])
+    return dict(codes=codes, scales=gpu_bank.scales.cpu().numpy(),
+                gscale=gpu_bank.gscale.cpu().numpy())
+
+
+def _check_weight_quant(w_bf16, gpu_bank, experts):
+    w = w_bf16.float().numpy()
+    for e in experts:
+        ref = OQ.quantize(w[e])
+        assert_nvfp4_equal(dict(packed=gpu_bank.codes[e].cpu().numpy(),
+                                scales=gpu_bank.scales[e].cpu().numpy(),
+                                gscale=gpu_bank.gscale[e].cpu().numpy()), ref, f"W[{e}]")
+
+
+SMALL = [
+    # name, T, H, E, k, I, Ks, kwargs
+    ("normal", 64, 256, 8, 2, 128, 8, {}),
+    ("ktail", 100, 512, 16, 4, 96, 24, {}),
+    ("zipf_t3_edges", 48, 256, 16, 4, 64, 16,
+     dict(acts="student_t3", routing="zipf", edge_cases=True, outlier_frac=0.0)),
+    ("k1_ragged", 33, 128, 4, 1, 64, 5, {}),
+    ("k_eq_E", 20, 128, 4, 4, 32, 128, {}),
+    ("ks0", 40, 256, 8, 2, 64, 0, {}),
+    ("ks1", 40, 256, 8, 2, 64, 1, {}),
+]
+
+
+def _run_small(case):
+    name, T, H, E, k, I, Ks, kw = case
+    inp = synth.small_moe(name, T, H, E, k, I, Ks, seed=hash(name) % 1000, **kw)
+    return inp
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_layer_stagewise_small(case):
+    name, T, H, E, k, I, Ks, _ = case
+    inp = _run_small(case)
+    x = inp.x.to(DEV)
+    logits = inp.logits.to(DEV)
+    if name == "k1_ragged":
+        logits[:, 2] = -1e4         # expert 2 receives no token
+    # A0: weights
+    w13 = ops.quantize_weight(inp.w13.to(DEV))
+    w2 = ops.quantize_weight(inp.w2.to(DEV))
+    _check_weight_quant(inp.w13, w13, range(E))
+    _check_weight_quant(inp.w2, w2, range(E))
+    W13, W2 = _bank_oracle(w13), _bank_oracle(w2)
+    # A1-A2
+    ids, wts, offs, row_token, inv_row = ops.route_permute(logits, k)
+    lg = logits.cpu().numpy()
+    ref_ids = ORt.topk(lg, k)
+    assert np.array_equal(ids.cpu().numpy(), ref_ids)
+    perm = ORt.permute(ref_ids, E)
+    assert np.array_equal(offs.cpu().numpy(), perm["offsets"])
+    assert np.array_equal(row_token.cpu().numpy(), perm["row_token"])
+    assert np.array_equal(inv_row.cpu().numpy(), perm["inv_row"])
+    ref_w = ORt.weights(lg, ref_ids, True)
+    np.testing.assert_allclose(wts.cpu().numpy(), ref_w, rtol=2e-6, atol=1e-7)
+    if name == "k1_ragged":
+        assert perm["counts"][2] == 0
+    # A3-A5
+    xf = np_bf16(inp.x)
+    xq, scores, ramax = ops.quantize_act(x, rac=True)
+    act = OR.rac_activation(xf, Ks)
+    assert_nvfp4_equal(xq, act["xq"], "xq")
+    assert np.array_equal(scores.cpu().numpy().view(np.uint64), act["scores"])
+    assert ramax.item() == np.max(np.abs(act["r"]))
+    sel, rq, _, _ = ops.select_channels(x, xq, Ks, scores, ramax)
+    assert np.array_equal(sel.cpu().numpy(), act["sel"])
+    assert_nvfp4_equal(rq, act["rq"], "rq")
+    # the unfused score pass gives the same statistics
+    sel2, rq2, sc2, ra2 = ops.select_channels(x, xq, Ks)
+    assert np.array_equal(sc2.cpu().numpy(), scores.cpu().numpy())
+    assert ra2.item() == ramax.item()
+    assert np.array_equal(sel2.cpu().numpy(), sel.cpu().numpy())
+    # A6 without the epilogue: [g; u] against the float64 contraction
+    R = T * k
+    gu, _ = ops.grouped_gemm(xq, w13, R, row_token, offs, rq if Ks else None,
+                             sel if Ks else None, Q.QD_EPI_NONE)
+    ref_gu, mag_gu = OL.w13_stage(act["xq"], act["rq"] if Ks else None, perm["row_token"],
+                                  perm["offsets"], W13)
+    check_close_bf16(np_bf16(gu), ref_gu, mag_gu, "W13 [g;u]")
+    # A6 with SwiGLU, teacher-forced on the oracle's g,u (values within tolerance)
+    h, hamax = ops.grouped_gemm(xq, w13, R, row_token, offs, rq if Ks else None,
+                                sel if Ks else None, Q.QD_EPI_SWIGLU, want_amax=True)
+    hf = np_bf16(h)
+    ref_h = OL.silu(ref_gu[:, :I]) * ref_gu[:, I:]
+    mag_h = (np.abs(OL.silu(ref_gu[:, :I])) * mag_gu[:, I:] +
+             1.1 * np.abs(ref_gu[:, I:]) * mag_gu[:, :I])
+    check_close_bf16(hf, ref_h, mag_h, "h (SwiGLU)")
+    assert hamax.max().item() == np.max(np.abs(hf))
+    # A7: quantise the GPU's h (bit-exact given h)
+    hq, _, _ = ops.quantize_act(h, amax_partials=hamax)
+    ref_hq = OQ.quantize(hf)
+    assert_nvfp4_equal(hq, ref_hq, "hq")
+    # A8 teacher-forced on the GPU's hq (equal to the oracle's)
+    z, _ = ops.grouped_gemm(hq, w2, R, None, offs)
+    ref_z, mag_z = OL.w2_stage(ref_hq, perm["offsets"], W2)
+    check_close_bf16(np_bf16(z), ref_z, mag_z, "z")
+    # A9 teacher-forced on the GPU's z and weights
+    y = ops.unpermute_combine(z, inv_row, wts)
+    ref_y, mag_y = OL.combine(np_bf16(z), perm["inv_row"], wts.cpu().numpy())
+    check_close_bf16(np_bf16(y), ref_y, mag_y, "y")
+    # whole layer in one call: identical to the op-by-op sequence
+    lay = ops.MoELayer(w13, w2, T, k, Ks)
+    y2 = lay(x, logits)
+    torch.cuda.synchronize()
+    assert torch.equal(y2.view(torch.int16), y.view(torch.int16))
+    v = lay.views()
+    assert torch.equal(v["h"].view(torch.int16), h.view(torch.int16))
+    # free-running: the oracle's own layer end to end
+    full = OL.moe_layer(xf, lg, W13, W2, k, Ks)
+    yb = full["yb"]
+    rel = np.linalg.norm(np_bf16(y) - yb) / max(np.linalg.norm(yb), 1e-30)
+    assert rel <= 1e-3, f"free-running rel-L2 {rel:.3e}"
+
+
+def test_dense_gemm_with_rac():
+    """16 tokens x K=256 x N=128, 4 outlier channels x30, RAC on 8 channels."""
+    inp = synth.generate("dense_t16_k256_n128")
+    wl = inp.wl
+    x = inp.x.to(DEV)
+    w = ops.quantize_weight(inp.w13.to(DEV))
+    _check_weight_quant(inp.w13, w, [0])
+    xq, scores, ramax = ops.quantize_act(x, rac=True)
+    act = OR.rac_activation(np_bf16(inp.x), wl.Ks)
+    assert_nvfp4_equal(xq, act["xq"], "xq")
+    sel, rq, _, _ = ops.select_channels(x, xq, wl.Ks, scores, ramax)
+    assert np.array_equal(sel.cpu().numpy(), act["sel"])
+    assert_nvfp4_equal(rq, act["rq"], "rq")
+    out, _ = ops.grouped_gemm(xq, w, wl.T, rq=rq, sel=sel)
+    W = _bank_oracle(w)
+    ref, mag = OL.w13_stage(act["xq"], act["rq"], None, np.array([0, wl.T]), W)
+    check_close_bf16(np_bf16(out), ref, mag, "dense")
+    # the standalone residual contraction (f32 output) and linearity
+    res = ops.residual_gemm(rq, sel, w, wl.T)
+    rh = OQ.dequantize_f64(act["rq"]["codes"], act["rq"]["scales"], act["rq"]["s_dec"])
+    ref_r, mag_r = OL.grouped_gemm(rh, None, np.array([0, wl.T]), W)
+    err = np.abs(res.cpu().numpy() - ref_r)
+    assert np.all(err <= 2.0 ** -20 * mag_r + 1e-30)
+    plain, _ = ops.grouped_gemm(xq, w, wl.T)
+    ref_p, mag_p = OL.w13_stage(act["xq"], None, None, np.array([0, wl.T]), W)
+    check_close_bf16(np_bf16(plain), ref_p, mag_p, "dense plain")
+    # the RAC output moves toward the unquantised product (expected, reported)
+    xf64 = np_bf16(inp.x).astype(np.float64)
+    wf = inp.w13[0].float().numpy().astype(np.float64)
+    exact = xf64 @ wf.T
+    e_rac = np.linalg.norm(np_bf16(out) - exact)
+    e_plain = np.linalg.norm(np_bf16(plain) - exact)
+    assert e_rac < e_plain
+
+
+def test_dequantize_modes():
+    rng = np.random.default_rng(5)
+    w = bf16_tensor(rng.standard_normal((3, 32, 64)) * 0.05)
+    q = ops.quantize_weight(w)
+    ref = OQ.fake_quant_weight(w.float().cpu().numpy())
+    refu = OQ.fake_quant_weight(w.float().cpu().numpy(), unscaled=True)
+    d = ops.dequantize(q).cpu().numpy()
+    du = ops.dequantize(q, unscaled=True).cpu().numpy()
+    assert np.array_equal(d.view(np.uint32), ref.view(np.uint32))
+    assert np.array_equal(du.view(np.uint32), refu.view(np.uint32))
+    db = ops.dequantize(q, dtype=torch.bfloat16)
+    refb = torch.from_numpy(ref).to(torch.bfloat16)
+    assert torch.equal(db.cpu().view(torch.int16), refb.view(torch.int16))
+
+
+def test_quantize_f32_input_and_static_scale():
+    rng = np.random.default_rng(6)
+    x = (rng.standard_normal((37, 96)) * 3).astype(np.float32)
+    xt = torch.from_numpy(x).to(DEV)
+    q, _, _ = ops.quantize_act(xt)
+    assert_nvfp4_equal(q, OQ.quantize(x), "f32 input")
+    amax = torch.tensor([10.0, 250.0, 3.0], device=DEV)
+    q2, _, _ = ops.quantize_act(xt, amax_partials=amax)
+    assert_nvfp4_equal(q2, OQ.quantize(x, amax=np.float32(250.0)), "static scale")
+    big = torch.rand(1000, device=DEV) * 7.0      # more partials than one pass holds
+    q3, _, _ = ops.quantize_act(xt, amax_partials=big)
+    assert_nvfp4_equal(q3, OQ.quantize(x, amax=np.float32(big.max().item())), "many partials")
+
+
+def test_quantize_edge_values():
+    """The oracle's hand-checked special cases on the GPU: ties, zeros,
+    subnormal and underflowing block scales, tiny and zero tensors."""
+    import test_oracle_quant as TQ
+    row = TQ._worked_row()
+    x = np.concatenate([row, -row, row * 0.5], axis=0)
+    xt = bf16_tensor(x)
+    q, _, _ = ops.quantize_act(xt)
+    assert_nvfp4_equal(q, OQ.quantize(np_bf16(xt)), "worked rows")
+    z = torch.zeros((4, 32), dtype=torch.bfloat16, device=DEV)
+    z[1, :16] = -0.0
+    qz, _, _ = ops.quantize_act(z)
+    assert_nvfp4_equal(qz, OQ.quantize(np_bf16(z)), "zero tensor")
+    tiny = torch.full((2, 16), 2.0 ** -110, dtype=torch.float32, device=DEV)
+    qt, _, _ = ops.quantize_act(tiny)
+    assert_nvfp4_equal(qt, OQ.quantize(tiny.cpu().numpy()), "tiny tensor")
+
+
+def test_determinism():
+    inp = synth.small_moe("det", 96, 256, 8, 2, 64, 12, seed=7)
+    w13 = ops.quantize_weight(inp.w13.to(DEV))
+    w2 = ops.quantize_weight(inp.w2.to(DEV))
+    lay = ops.MoELayer(w13, w2, 96, 2, 12)
+    x, lg = inp.x.to(DEV), inp.logits.to(DEV)
+    y1 = lay(x, lg).clone()
+    v1 = {k: t.clone() for k, t in lay.views().items()}
+    y2 = lay(x, lg)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+    for k, t in lay.views().items():
+        a, b = v1[k], t
+        if a.dtype == torch.bfloat16:
+            a, b = a.view(torch.int16), b.view(torch.int16)
+        assert torch.equal(a, b), k
+
+
+def test_empty_batch():
+    inp = synth.small_moe("empty", 4, 128, 4, 2, 32, 4, seed=8)
+    w13 = ops.quantize_weight(inp.w13.to(DEV))
+    w2 = ops.quantize_weight(inp.w2.to(DEV))
+    lay = ops.MoELayer(w13, w2, 0, 2, 4)
+    x = torch.empty((0, 128), dtype=torch.bfloat16, device=DEV)
+    lg = torch.empty((0, 4), dtype=torch.float32, device=DEV)
+    y = lay(x, lg)
+    torch.cuda.synchronize()
+    assert y.shape == (0, 128)
