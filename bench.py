@@ -1,0 +1,266 @@
+"""Benchmark: the NVFP4 W4A4 + RAC MoE layer forward on one MI355X.
+
+One step = the whole hot path (route, quantise X with RAC statistics,
+channel selection and masked residual, W13 grouped GEMM with fused residual
+and SwiGLU, quantise h, W2 grouped GEMM, combine) over one batch of the
+workload, with inputs already resident in HBM.  Weight banks and inputs are
+rotated over several copies so the weights never stay in the 256 MB MALL
+between steps.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
+
+`roofline` describes the dominant kernel (the W13 grouped GEMM): its
+algorithmic bytes (decode) or FLOPs (prefill) per launch over its average
+duration, timed with HIP events recorded on the layer's stream at the stage
+boundaries.  `cpu_baseline` times the CPU oracle on a bounded sample.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer tokens/s + effective TFLOP/s (% of MFMA peak) or GB/s (% HBM), 1 GPU"
+PEAK_HBM_GBS = 8000.0
+PEAK_F16_TFLOPS = 2500.0     # dense f16/bf16 MFMA (the operand type of exact NVFP4 here)
+PEAK_FP8_TFLOPS = 5000.0
+PEAK_FP4_TFLOPS = 10100.0
+NVFP4_BYTES_PER_ELEM = 0.5625   # 4-bit code + one E4M3 byte per 16 elements
+
+DECODE = {"moe_decode_t256_h2048", "moe_zipf_decode_t64_h4096", "dense_t16_k256_n128"}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="moe_decode_t256_h2048")
+    ap.add_argument("--copies", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-experts", type=int, default=0,
+                    help="experts in the oracle sample (0: automatic)")
+    return ap.parse_args()
+
+
+def algorithmic(wl, counts):
+    """Algorithmic bytes and FLOPs of one step and of the W13 launch.
+
+    Bytes: NVFP4 weights of the touched experts, X in and y out (bf16), the
+    router logits (f32); intermediates (codes, residual, h, z) are the
+    implementation's own traffic and are not counted.  FLOPs: 2*R*(H*2I +
+    I*H) for the expert GEMMs plus 2*R*Ks*2I for the residual.
+    """
+    T, H, I, k, Ks = wl.T, wl.H, wl.I, wl.k, wl.Ks
+    R = T * k
+    touched = int(np.count_nonzero(counts))
+    w13_bytes = touched * 2 * I * H * NVFP4_BYTES_PER_ELEM
+    w2_bytes = touched * H * I * NVFP4_BYTES_PER_ELEM
+    step_bytes = w13_bytes + w2_bytes + T * H * 2 * 2 + T * wl.E * 4
+    w13_flops = 2.0 * R * 2 * I * H + 2.0 * R * Ks * 2 * I
+    step_flops = w13_flops + 2.0 * R * I * H
+    # the W13 launch reads its weights, the NVFP4 activations and residual,
+    # and writes h (bf16)
+    w13_launch_bytes = w13_bytes + 2 * T * H * NVFP4_BYTES_PER_ELEM + R * I * 2
+    return dict(touched=touched, step_bytes=step_bytes, step_flops=step_flops,
+                w13_bytes=w13_launch_bytes, w13_flops=w13_flops)
+
+
+def cpu_baseline(inp, n_sample_experts):
+    """The oracle's free-running forward, timed on the host cores.
+
+    Bounded sample: routing and the RAC activation path run on the whole
+    batch; the expert GEMMs run for the rows of `n_sample_experts` of the
+    most loaded experts and their time is scaled by touched/sampled.  The
+    oracle quantises the sampled experts' weights itself (not timed: weights
+    are quantised once per weight sync, not per forward).
+    """
+    import torch
+    from oracle import layer as OL, quant as OQ, rac as OR, route as ORt
+    from oracle.formats import bf16_round_f64
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    wl = inp.wl
+    x = inp.x.float().numpy()
+    lg = inp.logits.numpy()
+    t0 = time.perf_counter()
+    ids = ORt.topk_fast(lg, wl.k)
+    wts = ORt.weights(lg, ids, True)
+    perm = ORt.permute(ids, wl.E)
+    act = OR.rac_activation(x, wl.Ks)
+    t_act = time.perf_counter() - t0
+    counts = perm["counts"]
+    order = np.sort(np.argsort(-counts, kind="stable")[:n_sample_experts])
+    E = wl.E
+    W13 = dict(codes=np.zeros((E, 2 * wl.I, wl.H), np.uint8),
+               scales=np.zeros((E, 2 * wl.I, wl.H // 16), np.uint8), gscale=np.ones((E, 2), np.float32))
+    W2 = dict(codes=np.zeros((E, wl.H, wl.I), np.uint8),
+              scales=np.zeros((E, wl.H, wl.I // 16), np.uint8), gscale=np.ones((E, 2), np.float32))
+    for e in order:
+        for bank, src in ((W13, inp.w13), (W2, inp.w2)):
+            q = OQ.quantize(src[int(e)].float().numpy())
+            bank["codes"][e], bank["scales"][e] = q["codes"], q["scales"]
+            bank["gscale"][e] = (q["s_enc"], q["s_dec"])
+    rows = np.concatenate([np.arange(perm["offsets"][e], perm["offsets"][e + 1]) for e in order])
+    t1 = time.perf_counter()
+    gu, _ = OL.w13_stage(act["xq"], act["rq"], perm["row_token"], perm["offsets"], W13, rows=rows)
+    h = OL.swiglu(gu, wl.I)
+    hq = OQ.quantize(h.astype(np.float32))
+    # the sampled rows as a contiguous block with their own offsets
+    sub_off = np.zeros(E + 1, np.int64)
+    for e in order:
+        sub_off[e + 1] = counts[e]
+    sub_off = np.cumsum(sub_off)
+    z, _ = OL.w2_stage(hq, sub_off, W2)
+    zb = bf16_round_f64(z)
+    t_exp = time.perf_counter() - t1
+    t2 = time.perf_counter()
+    _y, _ = OL.combine(np.zeros((wl.T * wl.k, wl.H)), perm["inv_row"], wts)
+    t_comb = time.perf_counter() - t2
+    touched = int(np.count_nonzero(counts))
+    est = t_act + t_exp * touched / max(1, len(order)) + t_comb
+    return dict(value=wl.T / est, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=(f"routing + RAC activation path on all {wl.T} tokens ({t_act:.2f} s); "
+                        f"expert GEMMs for the {len(rows)} rows of the {len(order)} most loaded "
+                        f"of {touched} touched experts ({t_exp:.2f} s, scaled x{touched / len(order):.1f}); "
+                        f"combine ({t_comb:.2f} s); float64 numpy oracle"),
+                seconds_measured=round(t_act + t_exp + t_comb, 3))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the layer is built for one MI355X; see the sharding notes in DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2607_15810_amd import ops, synth
+    from paper_2607_15810_amd import quads as Q
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    Q.lib()
+    wl = synth.WORKLOADS[args.workload]
+    if wl.dense:
+        print("the dense GEMM workload is a parity case, not a bench line", file=sys.stderr)
+        sys.exit(2)
+    t_gen = time.perf_counter()
+    inp = synth.generate(args.workload)
+    t_gen = time.perf_counter() - t_gen
+    print(f"[bench] generated {args.workload} in {t_gen:.1f} s", file=sys.stderr, flush=True)
+    dev = "cuda"
+    x0 = inp.x.to(dev)
+    lg0 = inp.logits.to(dev)
+    w13_0 = ops.quantize_weight(inp.w13.to(dev))
+    w2_0 = ops.quantize_weight(inp.w2.to(dev))
+    torch.cuda.synchronize()
+
+    def clone_bank(b):
+        return ops.NVFP4Tensor(b.codes.clone(), b.scales.clone(), b.gscale.clone(), b.groups,
+                               b.rows, b.cols)
+
+    copies = max(1, args.copies)
+    banks = [(w13_0, w2_0)] + [(clone_bank(w13_0), clone_bank(w2_0)) for _ in range(copies - 1)]
+    xs = [x0] + [x0.clone() for _ in range(copies - 1)]
+    lgs = [lg0] + [lg0.clone() for _ in range(copies - 1)]
+    n_ws = Q.lib().qd_moe_layer_workspace(wl.T, wl.H, wl.E, wl.k, wl.I)
+    ws = torch.empty(n_ws, dtype=torch.uint8, device=dev)
+    layers = [ops.MoELayer(b13, b2, wl.T, wl.k, wl.Ks, ws=ws) for b13, b2 in banks]
+    y = torch.empty((wl.T, wl.H), dtype=torch.bfloat16, device=dev)
+
+    for i in range(args.warmup):
+        c = i % copies
+        layers[c](xs[c], lgs[c], y)
+    torch.cuda.synchronize()
+    counts = np.diff(layers[0].views()["offsets"].cpu().numpy())
+
+    n_ev = len(Q.STAGE_NAMES) + 1
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(args.steps)]
+    for evs in events:          # create the underlying HIP events
+        for e in evs:
+            e.record()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for i in range(args.steps):
+        c = i % copies
+        layers[c](xs[c], lgs[c], y, events=events[i])
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = start.elapsed_time(end)
+    ms_step = ms_total / args.steps
+    stage_ms = np.zeros(n_ev - 1)
+    for evs in events:
+        for s in range(n_ev - 1):
+            stage_ms[s] += evs[s].elapsed_time(evs[s + 1])
+    stage_ms /= args.steps
+
+    alg = algorithmic(wl, counts)
+    tok_s = wl.T / (ms_step * 1e-3)
+    step_gbs = alg["step_bytes"] / (ms_step * 1e-3) / 1e9
+    step_tflops = alg["step_flops"] / (ms_step * 1e-3) / 1e12
+    w13_ms = stage_ms[Q.STAGE_NAMES.index("w13")]
+    decode = args.workload in DECODE
+    if decode:
+        achieved = alg["w13_bytes"] / (w13_ms * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(achieved, 1), peak=PEAK_HBM_GBS, unit="GB/s",
+                    frac=round(achieved / PEAK_HBM_GBS, 4), traffic=None,
+                    kernel="gemm_w4a4_kernel (W13 + residual + SwiGLU)",
+                    algorithmic_bytes=int(alg["w13_bytes"]), avg_ms=round(w13_ms, 5))
+    else:
+        achieved = alg["w13_flops"] / (w13_ms * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(achieved, 1), peak=PEAK_F16_TFLOPS,
+                    unit="TFLOP/s", frac=round(achieved / PEAK_F16_TFLOPS, 4), traffic=None,
+                    kernel="gemm_w4a4_kernel (W13 + residual + SwiGLU)",
+                    algorithmic_flops=alg["w13_flops"], avg_ms=round(w13_ms, 5),
+                    frac_of_fp8_peak=round(achieved / PEAK_FP8_TFLOPS, 4),
+                    frac_of_fp4_peak=round(achieved / PEAK_FP4_TFLOPS, 4))
+    out = {
+        "metric": METRIC,
+        "value": round(tok_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "nvfp4 (e2m1 codes, e4m3 block scales) x f16-exact MFMA, f32 accumulate",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "tokens": wl.T, "hidden": wl.H, "experts": wl.E,
+                   "top_k": wl.k, "intermediate": wl.I, "rac_channels": wl.Ks,
+                   "touched_experts": alg["touched"], "weight_copies": copies},
+        "effective": {"GB/s": round(step_gbs, 1), "frac_hbm": round(step_gbs / PEAK_HBM_GBS, 4),
+                      "TFLOP/s": round(step_tflops, 2),
+                      "frac_f16_mfma": round(step_tflops / PEAK_F16_TFLOPS, 4),
+                      "frac_fp8_mfma": round(step_tflops / PEAK_FP8_TFLOPS, 4),
+                      "frac_fp4_mfma": round(step_tflops / PEAK_FP4_TFLOPS, 4)},
+        "stage_ms": {n: round(float(v), 5) for n, v in zip(Q.STAGE_NAMES, stage_ms)},
+        "wall_ms_per_step": round(wall * 1e3 / args.steps, 5),
+        "roofline": roof,
+    }
+    print(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
+    if not args.no_cpu_baseline:
+        ne = args.cpu_experts or (4 if wl.H <= 2048 else 2)
+        out["cpu_baseline"] = cpu_baseline(inp, ne)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -196,11 +196,13 @@ qd_status rac_residual_gemm(const qd_nvfp4 *rq, const int32_t *sel_idx, int32_t 
  *   epilogue        : QD_EPI_NONE: out bf16 [rows][N] = bf16(v);
  *                     QD_EPI_SWIGLU: N = 2I, gate rows [0,I), up rows
  *                     [I,2I); out bf16 [rows][I] = bf16(silu(g)*u).
- *   amax_partials   : optional float [moe_w4a4_grouped_gemm_amax_count(...)]
- *                     receiving per-workgroup maxima of |out| (as stored);
- *                     their maximum is the tensor amax of out.
+ *   amax_partials   : optional float [moe_w4a4_grouped_gemm_amax_count(rows, N,
+ *                     K, E, Ks, epilogue)] receiving one maximum of |out| (as
+ *                     stored) per workgroup; their maximum is the tensor amax
+ *                     of out.  Every entry is written.
  * ------------------------------------------------------------------- */
-int64_t   moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int32_t E, int32_t epilogue);
+int64_t   moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int64_t K, int32_t E,
+                                           int32_t Ks, int32_t epilogue);
 qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
                                 const int32_t *expert_offsets, int32_t E, int64_t rows,
                                 const qd_nvfp4 *w, const qd_nvfp4 *rq,
@@ -232,6 +234,24 @@ qd_status qd_moe_layer_forward(const void *x, const float *logits, int64_t T, in
                                int32_t E, int32_t k, int64_t I, int32_t Ks, int32_t renorm,
                                const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y,
                                void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Same as qd_moe_layer_forward, recording HIP events at the stage
+ * boundaries: events is a host array of QD_STAGE_COUNT + 1 hipEvent_t (as
+ * void*); events[i] is recorded on `stream` before stage i and
+ * events[QD_STAGE_COUNT] after the last one (stages in the order below;
+ * the select stage records its two events back to back when Ks == 0).
+ * events NULL: no recording.
+ */
+enum {
+  QD_STAGE_ROUTE = 0, QD_STAGE_QUANT_X, QD_STAGE_SELECT, QD_STAGE_W13, QD_STAGE_QUANT_H,
+  QD_STAGE_W2, QD_STAGE_COMBINE, QD_STAGE_COUNT
+};
+qd_status qd_moe_layer_forward_timed(const void *x, const float *logits, int64_t T, int64_t H,
+                                     int32_t E, int32_t k, int64_t I, int32_t Ks, int32_t renorm,
+                                     const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y,
+                                     void *ws, size_t ws_bytes, void *const *events,
+                                     void *stream);
 
 /*
  * Byte offsets of the layer's intermediates inside its workspace (host

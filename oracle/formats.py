@@ -32,32 +32,29 @@ def e2m1_decode(codes):
     return np.where((codes >> 3) & 1, -mag, mag)
 
 
-def e2m1_encode_mag(a, chunk=1 << 20):
+def e2m1_encode_mag(a):
     """Round non-negative float32 magnitudes to the nearest E2M1 magnitude.
 
     Returns the 3-bit magnitude code.  Ties go to the even code (mantissa bit
     0), values above 6 saturate to 6 (6 is the nearest representable value).
-    Brute force: the distance to every one of the eight values is computed in
-    float64 (exact for the float32 inputs at every tie point) and the closest
-    wins.
+    Brute force: the distance to each of the eight values, in turn, is
+    computed in float64 (exact for the float32 inputs at every tie point)
+    and the closest so far is kept; an exact tie keeps the even code.
     """
     a = np.asarray(a, dtype=np.float32).astype(np.float64)
     # every value above 6 has 6 as its nearest magnitude; clamping at 8 keeps
     # the distances below distinguishable in float64 for huge inputs
     a = np.minimum(a, 8.0)
-    out = np.empty(a.shape, dtype=np.uint8)
-    flat_a = a.reshape(-1)
-    flat_o = out.reshape(-1)
-    idx = np.arange(8)
-    for s in range(0, flat_a.size, chunk):
-        d = np.abs(flat_a[s:s + chunk, None] - E2M1_MAG[None, :])
-        dmin = d.min(axis=1, keepdims=True)
-        tie = d == dmin
-        # among equally near candidates prefer the even code; two tied
-        # neighbours always have opposite parity, so exactly one is even
-        score = np.where(tie, np.where(idx % 2 == 0, 0, 1), 2)
-        flat_o[s:s + chunk] = np.argmin(score, axis=1).astype(np.uint8)
-    return out
+    best_d = np.full(a.shape, np.inf)
+    best_c = np.zeros(a.shape, dtype=np.uint8)
+    for c, m in enumerate(E2M1_MAG):
+        d = np.abs(a - m)
+        # candidates are visited in increasing order, so a tie is always
+        # between codes c-1 and c; the even one of the two wins
+        take = (d < best_d) | ((d == best_d) & (c % 2 == 0))
+        best_d = np.where(take, d, best_d)
+        best_c = np.where(take, np.uint8(c), best_c)
+    return best_c
 
 
 # --- E4M3FN ---------------------------------------------------------------

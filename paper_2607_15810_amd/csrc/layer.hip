@@ -43,7 +43,12 @@ Layout make_layout(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I) {
   put(QD_VIEW_RQ_SCALES, T * H / 16);
   put(QD_VIEW_RQ_GSCALE, 8);
   put(QD_VIEW_H, R * I * 2);
-  put(QD_VIEW_H_AMAX, moe_w4a4_grouped_gemm_amax_count(R, 2 * I, E, QD_EPI_SWIGLU) * 4);
+  {
+    // one partial per W13 workgroup; the kernel (and so the count) depends on K_s
+    const int64_t c0 = moe_w4a4_grouped_gemm_amax_count(R, 2 * I, H, E, 0, QD_EPI_SWIGLU);
+    const int64_t c1 = moe_w4a4_grouped_gemm_amax_count(R, 2 * I, H, E, (int32_t)H, QD_EPI_SWIGLU);
+    put(QD_VIEW_H_AMAX, (c0 > c1 ? c0 : c1) * 4);
+  }
   put(QD_VIEW_HQ_CODES, R * I / 2);
   put(QD_VIEW_HQ_SCALES, R * I / 16);
   put(QD_VIEW_HQ_GSCALE, 8);
@@ -74,6 +79,16 @@ extern "C" qd_status qd_moe_layer_forward(const void *x, const float *logits, in
                                           int32_t Ks, int32_t renorm, const qd_nvfp4 *w13,
                                           const qd_nvfp4 *w2, void *y, void *ws,
                                           size_t ws_bytes, void *stream) {
+  return qd_moe_layer_forward_timed(x, logits, T, H, E, k, I, Ks, renorm, w13, w2, y, ws,
+                                    ws_bytes, nullptr, stream);
+}
+
+extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logits, int64_t T,
+                                                int64_t H, int32_t E, int32_t k, int64_t I,
+                                                int32_t Ks, int32_t renorm, const qd_nvfp4 *w13,
+                                                const qd_nvfp4 *w2, void *y, void *ws,
+                                                size_t ws_bytes, void *const *events,
+                                                void *stream) {
   if (!w13 || !w2) return QD_ERR_NULL;
   if (T < 0 || H <= 0 || H % 32 || I <= 0 || I % 32 || E < 1 || k < 1 || k > E) return QD_ERR_SHAPE;
   if (Ks < 0 || Ks > H) return QD_ERR_SHAPE;
@@ -92,12 +107,16 @@ extern "C" qd_status qd_moe_layer_forward(const void *x, const float *logits, in
   char *b = static_cast<char *>(ws);
   auto P = [&](int idx) { return b + L.off[idx]; };
   const int64_t R = T * k;
+  auto mark = [&](int i) {
+    if (events) hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), qdh::S(stream));
+  };
   int32_t *ids = (int32_t *)P(QD_VIEW_TOPK_IDS);
   float *wts = (float *)P(QD_VIEW_TOPK_W);
   int32_t *offs = (int32_t *)P(QD_VIEW_OFFSETS);
   int32_t *row_token = (int32_t *)P(QD_VIEW_ROW_TOKEN);
   int32_t *inv_row = (int32_t *)P(QD_VIEW_INV_ROW);
 
+  mark(QD_STAGE_ROUTE);
   st = moe_route_permute(logits, T, E, k, renorm, ids, wts, offs, row_token, inv_row,
                          b + L.route_ws, moe_route_permute_workspace(T, E, k), stream);
   if (st) return st;
@@ -110,10 +129,12 @@ extern "C" qd_status qd_moe_layer_forward(const void *x, const float *logits, in
   float *ramax = (float *)P(QD_VIEW_RAMAX);
   int32_t *sel = (int32_t *)P(QD_VIEW_SEL);
   const bool rac = Ks > 0;
+  mark(QD_STAGE_QUANT_X);
   st = nvfp4_quantize_act(x, QD_DTYPE_BF16, T, H, nullptr, 0, &xq, rac ? scores : nullptr,
                           rac ? ramax : nullptr, b + L.q1_ws,
                           nvfp4_quantize_act_workspace(T, H), stream);
   if (st) return st;
+  mark(QD_STAGE_SELECT);
   if (rac) {
     st = rac_select_channels(x, &xq, Ks, scores, ramax, 1, sel, &rq, b + L.sel_ws,
                              rac_select_channels_workspace(T, H), stream);
@@ -121,19 +142,26 @@ extern "C" qd_status qd_moe_layer_forward(const void *x, const float *logits, in
   }
   uint16_t *h = (uint16_t *)P(QD_VIEW_H);
   float *hamax = (float *)P(QD_VIEW_H_AMAX);
+  mark(QD_STAGE_W13);
   st = moe_w4a4_grouped_gemm(&xq, row_token, offs, E, R, w13, rac ? &rq : nullptr,
                              rac ? sel : nullptr, Ks, QD_EPI_SWIGLU, h, hamax, stream);
   if (st) return st;
   qd_nvfp4 hq{(uint8_t *)P(QD_VIEW_HQ_CODES), (uint8_t *)P(QD_VIEW_HQ_SCALES),
               (float *)P(QD_VIEW_HQ_GSCALE), 1, R, I};
+  mark(QD_STAGE_QUANT_H);
   st = nvfp4_quantize_act(h, QD_DTYPE_BF16, R, I, hamax,
-                          moe_w4a4_grouped_gemm_amax_count(R, 2 * I, E, QD_EPI_SWIGLU), &hq,
+                          moe_w4a4_grouped_gemm_amax_count(R, 2 * I, H, E, Ks, QD_EPI_SWIGLU), &hq,
                           nullptr, nullptr, b + L.q2_ws, nvfp4_quantize_act_workspace(R, I),
                           stream);
   if (st) return st;
   uint16_t *z = (uint16_t *)P(QD_VIEW_Z);
+  mark(QD_STAGE_W2);
   st = moe_w4a4_grouped_gemm(&hq, nullptr, offs, E, R, w2, nullptr, nullptr, 0, QD_EPI_NONE, z,
                              nullptr, stream);
   if (st) return st;
-  return moe_unpermute_combine(z, inv_row, wts, T, k, H, y, stream);
+  mark(QD_STAGE_COMBINE);
+  st = moe_unpermute_combine(z, inv_row, wts, T, k, H, y, stream);
+  if (st) return st;
+  mark(QD_STAGE_COUNT);
+  return qdh::check_launch();
 }

@@ -142,48 +142,75 @@ __device__ int block_exclusive_scan(int v, int *sh /* 1024 + 32 ints */, int &to
 
 // One workgroup of 1024 threads.  Radix select over 8-bit digits of the u64
 // keys finds the K_s-th largest score theta; channels above theta are taken,
-// then channels equal to theta in ascending index order until K_s.
+// then channels equal to theta in ascending index order until K_s.  Thread i
+// owns channels [i*per, (i+1)*per); with K <= 16384 they stay in registers.
+template <bool REG>
 __global__ __launch_bounds__(1024) void rac_select_kernel(const uint64_t *__restrict__ scores,
                                                           int K, int Ks,
                                                           int32_t *__restrict__ sel_idx,
                                                           uint32_t *__restrict__ bitmap) {
   __shared__ int hist[256];
   __shared__ int sh[1024 + 32];
-  __shared__ uint64_t s_prefix, s_mask;
+  __shared__ uint64_t s_prefix;
   __shared__ int s_remaining;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  constexpr int PER = REG ? 16 : 64;      // channels per thread (K <= 1024 * PER)
   const int per = (K + 1023) / 1024;
-  const int j0 = tid * per, j1 = min(K, j0 + per);
+  const int j0 = tid * per;
+  const int n = max(0, min(K, j0 + per) - j0);
+  uint64_t sv[16];
+  if (REG) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sv[i] = i < n ? scores[j0 + i] : 0ull;
+  }
+  auto key = [&](int i) -> uint64_t { return REG ? sv[i] : scores[j0 + i]; };
   for (int w = tid; w < (K + 31) / 32; w += 1024) bitmap[w] = 0u;
   if (tid == 0) {
     s_prefix = 0ull;
-    s_mask = 0ull;
     s_remaining = Ks;
   }
   __syncthreads();
   if (Ks > 0) {
+    uint64_t msk = 0ull;
     for (int d = 7; d >= 0; --d) {
-      for (int i = tid; i < 256; i += 1024) hist[i] = 0;
+      if (tid < 256) hist[tid] = 0;
       __syncthreads();
-      const uint64_t pre = s_prefix, msk = s_mask;
-      for (int j = j0; j < j1; ++j) {
-        uint64_t v = scores[j];
-        if ((v & msk) == pre) atomicAdd(&hist[(int)((v >> (8 * d)) & 255ull)], 1);
-      }
-      __syncthreads();
-      if (tid == 0) {
-        int rem = s_remaining, above = 0, dig = 0;
-        for (int v = 255; v >= 0; --v) {
-          if (above + hist[v] >= rem) {
-            dig = v;
-            break;
-          }
-          above += hist[v];
+      const uint64_t pre = s_prefix;
+      const int rem = s_remaining;
+      if (REG) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (i < n && (sv[i] & msk) == pre) atomicAdd(&hist[(int)((sv[i] >> (8 * d)) & 255ull)], 1);
+      } else {
+        for (int i = 0; i < n; ++i) {
+          const uint64_t v = key(i);
+          if ((v & msk) == pre) atomicAdd(&hist[(int)((v >> (8 * d)) & 255ull)], 1);
         }
-        s_remaining = rem - above;
-        s_prefix = pre | ((uint64_t)dig << (8 * d));
-        s_mask = msk | (255ull << (8 * d));
       }
+      __syncthreads();
+      if (wid == 0) {
+        // lane l owns bins 255-4l .. 252-4l (descending digit order)
+        const int b = 255 - 4 * lane;
+        const int c0 = hist[b], c1 = hist[b - 1], c2 = hist[b - 2], c3 = hist[b - 3];
+        const int lsum = c0 + c1 + c2 + c3;
+        int incl = lsum;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(incl, o, 64);
+          if (lane >= o) incl += y;
+        }
+        const int excl = incl - lsum;
+        if (excl < rem && rem <= incl) {
+          int above = excl, dig;
+          if (above + c0 >= rem) dig = b;
+          else if ((above += c0) + c1 >= rem) dig = b - 1;
+          else if ((above += c1) + c2 >= rem) dig = b - 2;
+          else { above += c2; dig = b - 3; }
+          s_prefix = pre | ((uint64_t)dig << (8 * d));
+          s_remaining = rem - above;
+        }
+      }
+      msk |= 255ull << (8 * d);
       __syncthreads();
     }
   }
@@ -191,23 +218,24 @@ __global__ __launch_bounds__(1024) void rac_select_kernel(const uint64_t *__rest
   const int take_eq = s_remaining;          // channels equal to theta to keep
   // rank the channels equal to theta by index
   int n_eq = 0;
-  if (Ks > 0)
-    for (int j = j0; j < j1; ++j) n_eq += (scores[j] == theta);
+  if (Ks > 0) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+      if (i < n) n_eq += (key(i) == theta);
+  }
   int tot;
-  int eq_before = block_exclusive_scan(n_eq, sh, tot);
-  // selection flags and their positions
+  const int eq_before = block_exclusive_scan(n_eq, sh, tot);
   int n_sel = 0;
   {
     int eq_seen = eq_before;
-    for (int j = j0; j < j1; ++j) {
-      uint64_t v = scores[j];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (i >= n) break;
+      const uint64_t v = key(i);
       bool take = false;
       if (Ks > 0) {
         if (v > theta) take = true;
-        else if (v == theta) {
-          take = eq_seen < take_eq;
-          ++eq_seen;
-        }
+        else if (v == theta) take = eq_seen++ < take_eq;
       }
       n_sel += take;
     }
@@ -215,17 +243,17 @@ __global__ __launch_bounds__(1024) void rac_select_kernel(const uint64_t *__rest
   int pos = block_exclusive_scan(n_sel, sh, tot);
   {
     int eq_seen = eq_before;
-    for (int j = j0; j < j1; ++j) {
-      uint64_t v = scores[j];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (i >= n) break;
+      const uint64_t v = key(i);
       bool take = false;
       if (Ks > 0) {
         if (v > theta) take = true;
-        else if (v == theta) {
-          take = eq_seen < take_eq;
-          ++eq_seen;
-        }
+        else if (v == theta) take = eq_seen++ < take_eq;
       }
       if (take) {
+        const int j = j0 + i;
         sel_idx[pos++] = j;
         atomicOr(&bitmap[j >> 5], 1u << (j & 31));
       }
@@ -362,8 +390,12 @@ extern "C" qd_status rac_select_channels(const void *x, const qd_nvfp4 *xq, int3
                          xq->codes, xq->scales, xq->gscale, T, K, part, g, scores, ramax);
     }
   }
-  hipLaunchKernelGGL(rac_select_kernel, dim3(1), dim3(1024), 0, s, scores, (int)K, Ks, sel_idx,
-                     bitmap);
+  if (K <= 16384)
+    hipLaunchKernelGGL(rac_select_kernel<true>, dim3(1), dim3(1024), 0, s, scores, (int)K, Ks,
+                       sel_idx, bitmap);
+  else
+    hipLaunchKernelGGL(rac_select_kernel<false>, dim3(1), dim3(1024), 0, s, scores, (int)K, Ks,
+                       sel_idx, bitmap);
   {
     const int64_t total = T * (K / 16);
     int64_t g = (total + 255) / 256;

@@ -162,10 +162,10 @@ def grouped_gemm(a, w, rows, row_token=None, offsets=None, rq=None, sel=None,
     ncol = N // 2 if epilogue == Q.QD_EPI_SWIGLU else N
     out = torch.empty((rows, ncol), dtype=torch.bfloat16, device=dev)
     amax = None
-    if want_amax:
-        cnt = Q.lib().moe_w4a4_grouped_gemm_amax_count(rows, N, E, epilogue)
-        amax = torch.empty(max(cnt, 1), dtype=torch.float32, device=dev)
     Ks = 0 if sel is None else int(sel.numel())
+    if want_amax:
+        cnt = Q.lib().moe_w4a4_grouped_gemm_amax_count(rows, N, a.cols, E, Ks, epilogue)
+        amax = torch.empty(max(cnt, 1), dtype=torch.float32, device=dev)
     Q.call("moe_w4a4_grouped_gemm", _nv(a), _ptr(row_token), _ptr(offsets), E, rows, _nv(w),
            _nv(rq) if Ks else None, _ptr(sel) if Ks else None, Ks, epilogue, out.data_ptr(),
            _ptr(amax), _stream())
@@ -185,7 +185,7 @@ class MoELayer:
     """The whole layer through qd_moe_layer_forward, with a reusable
     workspace; `views()` exposes the intermediates of the last call."""
 
-    def __init__(self, w13, w2, T, k, Ks, renorm=True):
+    def __init__(self, w13, w2, T, k, Ks, renorm=True, ws=None):
         self.w13, self.w2 = w13, w2
         self.E = w13.groups
         self.I = w13.rows // 2
@@ -193,7 +193,9 @@ class MoELayer:
         self.T, self.k, self.Ks, self.renorm = T, k, Ks, renorm
         dev = w13.codes.device
         n = Q.lib().qd_moe_layer_workspace(T, self.H, self.E, k, self.I)
-        self.ws = _ws(n, dev)
+        self.ws = _ws(n, dev) if ws is None else ws
+        if self.ws.numel() < n:
+            raise ValueError("workspace too small")
         import ctypes
         off = (ctypes.c_int64 * len(Q.VIEW_NAMES))()
         Q.call("qd_moe_layer_views", T, self.H, self.E, k, self.I, off)
@@ -201,13 +203,19 @@ class MoELayer:
         self._s13 = w13.struct()
         self._s2 = w2.struct()
 
-    def __call__(self, x, logits, y=None):
+    def __call__(self, x, logits, y=None, events=None):
+        """events: optional list of QD_STAGE_COUNT + 1 recorded torch.cuda.Event
+        objects (enable_timing=True); they are re-recorded at the stage
+        boundaries on the current stream."""
         import ctypes
         if y is None:
             y = torch.empty((self.T, self.H), dtype=torch.bfloat16, device=x.device)
-        Q.call("qd_moe_layer_forward", x.data_ptr(), logits.data_ptr(), self.T, self.H, self.E,
-               self.k, self.I, self.Ks, int(self.renorm), ctypes.byref(self._s13),
-               ctypes.byref(self._s2), y.data_ptr(), self.ws.data_ptr(), self.ws.numel(),
+        evp = None
+        if events is not None:
+            evp = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+        Q.call("qd_moe_layer_forward_timed", x.data_ptr(), logits.data_ptr(), self.T, self.H,
+               self.E, self.k, self.I, self.Ks, int(self.renorm), ctypes.byref(self._s13),
+               ctypes.byref(self._s2), y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), evp,
                _stream())
         return y
 

@@ -25,6 +25,8 @@ QD_DTYPE_F32 = 1
 QD_EPI_NONE = 0
 QD_EPI_SWIGLU = 1
 
+STAGE_NAMES = ["route", "quant_x", "select", "w13", "quant_h", "w2", "combine"]
+
 VIEW_NAMES = ["topk_ids", "topk_w", "offsets", "row_token", "inv_row", "xq_codes",
               "xq_scales", "xq_gscale", "scores", "ramax", "sel", "rq_codes", "rq_scales",
               "rq_gscale", "h", "h_amax", "hq_codes", "hq_scales", "hq_gscale", "z"]
@@ -58,7 +60,8 @@ SIGNATURES = {
                                     c_void_p, PN, c_void_p, c_size_t, c_void_p]),
     "rac_residual_gemm": (c_int, [PN, c_void_p, c_int32, c_void_p, c_void_p, c_int64, PN,
                                   c_void_p, c_void_p]),
-    "moe_w4a4_grouped_gemm_amax_count": (c_int64, [c_int64, c_int64, c_int32, c_int32]),
+    "moe_w4a4_grouped_gemm_amax_count": (c_int64, [c_int64, c_int64, c_int64, c_int32, c_int32,
+                                                   c_int32]),
     "moe_w4a4_grouped_gemm": (c_int, [PN, c_void_p, c_void_p, c_int32, c_int64, PN, PN,
                                       c_void_p, c_int32, c_int32, c_void_p, c_void_p,
                                       c_void_p]),
@@ -68,6 +71,9 @@ SIGNATURES = {
     "qd_moe_layer_forward": (c_int, [c_void_p, c_void_p, c_int64, c_int64, c_int32, c_int32,
                                      c_int64, c_int32, c_int32, PN, PN, c_void_p, c_void_p,
                                      c_size_t, c_void_p]),
+    "qd_moe_layer_forward_timed": (c_int, [c_void_p, c_void_p, c_int64, c_int64, c_int32,
+                                           c_int32, c_int64, c_int32, c_int32, PN, PN, c_void_p,
+                                           c_void_p, c_size_t, c_void_p, c_void_p]),
     "qd_moe_layer_views": (c_int, [c_int64, c_int64, c_int32, c_int32, c_int64,
                                    POINTER(c_int64)]),
 }

@@ -71,3 +71,42 @@ def check_close_bf16(gpu, ref64, mag64, name, rel_l2=1e-3, floor=2.0 ** -20):
 
 def bf16_tensor(a, device="cuda"):
     return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16).to(device)
+
+
+def upload_nvfp4(q, device="cuda"):
+    """Oracle quantize() result -> GPU NVFP4Tensor holding the same bytes
+    (the oracle's own values become the GPU stage's input)."""
+    from paper_2607_15810_amd.ops import NVFP4Tensor
+    packed = np.ascontiguousarray(q["packed"])
+    rows, half = packed.shape
+    t = NVFP4Tensor.empty(1, rows, half * 2, device)
+    t.codes.copy_(torch.from_numpy(packed).view(1, rows, half))
+    t.scales.copy_(torch.from_numpy(np.ascontiguousarray(q["scales"])).view(1, rows, -1))
+    t.gscale.copy_(torch.tensor([[float(q["s_enc"]), float(q["s_dec"])]], dtype=torch.float32))
+    return t
+
+
+def oracle_bank(w_bf16, experts=None):
+    """Oracle quantisation of a bf16 bank [E][N][K]; with `experts` only those
+    experts are quantised (the others stay zero and must not be used)."""
+    w = w_bf16.float().numpy()
+    E, N, K = w.shape
+    if experts is None:
+        return quant.quantize_weight_bank(w)
+    codes = np.zeros((E, N, K), np.uint8)
+    scales = np.zeros((E, N, K // 16), np.uint8)
+    gscale = np.ones((E, 2), np.float32)
+    for e in experts:
+        q = quant.quantize(w[e])
+        codes[e], scales[e] = q["codes"], q["scales"]
+        gscale[e] = (q["s_enc"], q["s_dec"])
+    return dict(codes=codes, scales=scales, gscale=gscale)
+
+
+def assert_bank_equal(gpu_bank, ref_bank, experts):
+    for e in experts:
+        ref = dict(packed=quant.pack(ref_bank["codes"][e]), scales=ref_bank["scales"][e],
+                   s_enc=ref_bank["gscale"][e, 0], s_dec=ref_bank["gscale"][e, 1])
+        assert_nvfp4_equal(dict(packed=gpu_bank.codes[e].cpu().numpy(),
+                                scales=gpu_bank.scales[e].cpu().numpy(),
+                                gscale=gpu_bank.gscale[e].cpu().numpy()), ref, f"W[{e}]")

@@ -119,7 +119,7 @@ def test_gemm_validation(lib):
              FAKE, None, None) == Q.QD_ERR_NULL     # residual without channel list
     assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w), None, None, 0, 0, FAKE + 8,
              None, None) == Q.QD_ERR_ALIGN
-    assert lib.moe_w4a4_grouped_gemm_amax_count(64, 256, 4, 1) > 0
+    assert lib.moe_w4a4_grouped_gemm_amax_count(64, 256, 256, 4, 8, 1) > 0
 
 
 def test_select_and_combine_validation(lib):
