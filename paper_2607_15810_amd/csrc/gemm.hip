@@ -259,437 +259,487 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs p) {
 }
 
 // ---------------------------------------------------------------------------
-// Skinny grouped GEMM for decode-sized batches (few rows per expert).  The
-// weights dominate the traffic, so every weight byte is read exactly once
-// and as many of them as possible are kept in flight:
-//   * a workgroup owns (expert e, 128 weight rows); each of its four waves
-//     streams 32 distinct weight rows (for SwiGLU 16 gate rows and the
-//     matching 16 up rows) straight from HBM into registers, two iterations
-//     ahead of their use;
-//   * the expert's activation rows (up to 64 per pass) are staged once per
-//     iteration into LDS by the whole workgroup and shared by the waves;
-//   * RAC: while a weight chunk sits in registers, its elements in the
-//     selected channels S are decoded into a compact [row][K_s] f16 panel in
-//     LDS; after the K loop a short K_s-long MFMA pass multiplies it with the
-//     compact residual activations, so the residual costs K_s/K of the main
-//     contraction instead of a dense second pass.
+// Decode-shaped grouped GEMM (few rows per expert).  The weights are nearly
+// all of the traffic, so the kernel is built to stream them once at HBM rate
+// with as little per-byte instruction work as possible:
 //
-// K assignment: iteration it covers elements [256*it, 256*it + 256) (128 code
-// bytes, one cache line, and 16 scale bytes per row); lane group g = lane/16
-// owns elements 64g .. 64g+63 of it (32 contiguous code bytes, one scale
-// dword), split into SK_CH = 2 chunks of 32; k-step s of a chunk is its
-// elements 8s .. 8s+7.  The four lane groups of a row therefore read one
-// whole line per iteration.
+//  * Work units.  A unit is (expert e, pass p over 32 of its rows, block nb
+//    of 256 weight rows; for SwiGLU 128 gate rows and the matching 128 up
+//    rows).  Experts without rows have no units.  Every workgroup derives
+//    the unit list from the expert offsets and takes an equal contiguous
+//    share of it (one workgroup per CU), so skewed routing stays balanced;
+//    units are ordered expert-major, so a workgroup mostly stays on one
+//    expert.
+//  * Eight waves, 32 weight rows each.  A wave streams its rows through a
+//    private LDS ring of NS stages with direct global->LDS loads: in-flight
+//    weights cost no registers.  One stage is 256 K-elements of 32 rows
+//    (4 KB of codes, 512 B of scales).
+//  * The 32 activation rows of the pass (with RAC also their masked
+//    residual rows) go through a two-slot LDS ring filled the same way.
+//    The waves decode each stage of them once, together, into an f16 LDS
+//    buffer; every wave then reads its MFMA operands from there.
+//  * Loads are issued in one fixed order per iteration (weights NS stages
+//    ahead right after the stage in hand has been read into registers,
+//    activations two stages ahead once their slot is free), so one explicit
+//    vmcnt wait at the top of each iteration proves that the current stage
+//    has landed; loads past the last stage repeat the last stage's
+//    addresses into slots that are never read again.
+//  * Weights are decoded exactly to f16 in registers (see the top of this
+//    file) and multiplied on MFMA, with straight-line code for each number
+//    of valid 16-row m-tiles.
+//  * RAC: the masked residual is zero outside the selected channels S, so
+//    its contraction with the weights runs over the same decoded weight
+//    fragments, restricted to the k-steps that contain a channel of S (a
+//    per-iteration step mask built from S in the prologue), into its own
+//    accumulator, which meets the main one in the epilogue.
 //
-// XCD-aware placement: workgroup P runs on XCD P % 8; expert e's workgroups
-// all get ids with P % 8 == e % 8, so its activation rows are fetched into
-// one L2 only.
-constexpr int SK_MTMAX = 4;        // 16-row m-tiles per pass (64 rows)
-constexpr int SK_ROWS = 128;       // weight rows per workgroup
-constexpr int SK_CH = 2;           // 32-element chunks per iteration
-constexpr int SK_KSMAX = 256;      // largest K_s of the fused compact residual
-constexpr int SK_KMAX = 16384;     // largest K with the fused residual
+// K assignment inside an iteration: lane group g = lane/16 owns elements
+// 64g .. 64g+63 (32 code bytes, one scale dword), split into two chunks of
+// 32; k-step s of a chunk is its elements 8s .. 8s+7.
+constexpr int SK_WAVES = 8;
+constexpr int SK_THREADS = 64 * SK_WAVES;
+constexpr int SK_ROWS = 32 * SK_WAVES;   // weight rows per unit
+constexpr int SK_PR = 32;                // activation rows per pass
+constexpr int SK_BSTAGE = 4608;          // bytes per wave and weight stage
+constexpr int SK_ASRC = SK_PR * 144;     // raw activation stage of one source
+constexpr int SK_DSRC = SK_PR * 512;     // decoded (f16) stage of one source
+constexpr int SK_KMAX = 65536;
+constexpr int SK_EMAX = 1023;            // experts (offsets and their scan kept in LDS)
+constexpr int SK_LDS_MAX = 160 * 1024;
+constexpr int SK_GRID = 256;             // one workgroup per CU
 
 struct SkLayout {
-  int selmap, prefix, sel, a, as, ares, wc, red, total, stride;
+  int b, a, dec, junk, offs, pu, sw, smask, red, total;
 };
 
-__host__ __device__ inline SkLayout sk_layout(int K, int Ks, bool rac) {
+// nsrc = 1 (activations) or 2 (activations and masked residual)
+__host__ __device__ inline SkLayout sk_layout(int K, int E, int nsrc, int ns) {
   SkLayout L{};
   int o = 0;
   auto take = [&](int bytes) { int at = o; o += (bytes + 15) & ~15; return at; };
-  const int kpad = (Ks + 31) & ~31;
-  L.stride = kpad * 2 + 16;                         // bytes per compact row (+16: banks)
-  L.selmap = take(rac ? (K / 32) * 4 : 0);
-  L.prefix = take(rac ? (K / 32) * 4 : 0);
-  L.sel = take(rac ? Ks * 4 : 0);
-  L.a = take(2 * SK_CH * 4 * SK_MTMAX * 16 * 16);    // [stage][chunk][group][row] x 16 B
-  L.as = take(2 * 4 * SK_MTMAX * 16 * 4);            // [stage][group][row] x 4 B
-  L.ares = take(rac ? SK_MTMAX * 16 * L.stride : 0);
-  L.wc = take(rac ? SK_ROWS * L.stride : 0);
+  L.b = take(SK_WAVES * ns * SK_BSTAGE);
+  L.a = take(2 * nsrc * SK_ASRC);
+  L.dec = take(nsrc * SK_DSRC);
+  L.junk = take(1024);
+  L.offs = take((E + 1) * 4);
+  L.pu = take((E + 1) * 4);
+  L.sw = take(E * 4);
+  L.smask = take(nsrc > 1 ? (K >> 8) * 4 : 0);
   L.red = take(16 * 4);
   L.total = o;
   return L;
 }
 
-// One iteration's weights of a wave (two 16-row fragments x SK_CH chunks)
-// and one thread's share of the activation staging.
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-struct BStage {
-  u32x4 v00, v01, v10, v11;     // v<fragment><chunk>
-  uint32_t sc0, sc1;            // 4 scale bytes per fragment (2 chunks x 2 blocks)
-};
-struct AStage {
-  u32x4 c0, c1;
-  uint32_t sc;
-};
-constexpr int kBLoads = 6;      // vector memory instructions per BStage
-constexpr int kALoads = 3;      // per AStage
-
-// The main loop's loads are issued by inline assembly so that their
-// completion is tracked by hand: the compiler's own wait-counter placement
-// is conservative at the loop header and would force the prefetched stages
-// to complete one iteration early.  wait_* ties the waited registers, so no
-// use of them can be scheduled before the wait.
-__device__ __forceinline__ u32x4 gld16(const uint8_t *p) {
-  u32x4 r;
-  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(p));
-  return r;
+// Direct global->LDS loads: lane l's bytes land at M0 + l * size.  They are
+// issued from inline assembly and their completion is counted by hand; the
+// memory clobbers keep every LDS access on its side of the issue and of the
+// waits.
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(g), "s"(lds_addr) : "memory", "m0");
 }
-__device__ __forceinline__ uint32_t gld4(const uint8_t *p) {
-  uint32_t r;
-  asm volatile("global_load_dword %0, %1, off" : "=v"(r) : "v"(p));
-  return r;
+__device__ __forceinline__ void dma4(const void *g, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :: "v"(g), "s"(lds_addr) : "memory", "m0");
 }
 template <int N>
-__device__ __forceinline__ void wait_b(BStage &b) {
-  asm volatile("s_waitcnt vmcnt(%6)"
-               : "+v"(b.v00), "+v"(b.v01), "+v"(b.v10), "+v"(b.v11), "+v"(b.sc0), "+v"(b.sc1)
-               : "n"(N));
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
-template <int N>
-__device__ __forceinline__ void wait_a(AStage &a) {
-  asm volatile("s_waitcnt vmcnt(%3)" : "+v"(a.c0), "+v"(a.c1), "+v"(a.sc) : "n"(N));
+__device__ __forceinline__ void wait_lds() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
+__device__ __forceinline__ uint32_t uni(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
-__device__ __forceinline__ BStage load_bstage(const uint8_t *bc0, const uint8_t *bc1,
-                                              const uint8_t *bs0, const uint8_t *bs1, int it) {
-  BStage st;
-  st.v00 = gld16(bc0 + it * 128);
-  st.v01 = gld16(bc0 + it * 128 + 16);
-  st.v10 = gld16(bc1 + it * 128);
-  st.v11 = gld16(bc1 + it * 128 + 16);
-  st.sc0 = gld4(bs0 + it * 16);
-  st.sc1 = gld4(bs1 + it * 16);
-  return st;
-}
-__device__ __forceinline__ AStage load_astage(const uint8_t *ac, const uint8_t *as, int it) {
-  AStage st;
-  st.c0 = gld16(ac + it * 128);
-  st.c1 = gld16(ac + it * 128 + 16);
-  st.sc = gld4(as + it * 16);
-  return st;
-}
-__device__ __forceinline__ uint4 as_uint4(u32x4 v) { return make_uint4(v.x, v.y, v.z, v.w); }
-__device__ __forceinline__ void store_astage(uint4 *a_lds, uint32_t *as_lds, const AStage &st,
-                                             int stage, int ag, int arow) {
-  a_lds[((stage * 2 + 0) * 4 + ag) * 64 + arow] = as_uint4(st.c0);
-  a_lds[((stage * 2 + 1) * 4 + ag) * 64 + arow] = as_uint4(st.c1);
-  as_lds[(stage * 4 + ag) * 64 + arow] = st.sc;
-}
-__device__ __forceinline__ uint4 bvec(const BStage &b, int j, int cc) {
-  return as_uint4(j == 0 ? (cc == 0 ? b.v00 : b.v01) : (cc == 0 ? b.v10 : b.v11));
-}
+// Position in a workgroup's stage sequence: unit u = (expert e, pass p,
+// block nb), iteration it over K.  All fields are workgroup-uniform.
+struct SkCur {
+  int u, it, e, p, nb, ob, rows, npass;
+};
 
-__device__ __forceinline__ uint32_t dword_of(uint4 v, uint32_t i) {
-  return i == 0 ? v.x : (i == 1 ? v.y : (i == 2 ? v.z : v.w));
-}
+struct SkUnits {
+  const int32_t *offs;   // LDS: expert offsets [E + 1]
+  const int32_t *pu;     // LDS: first unit of each expert [E + 1]
+  int E, nblk, niter, u1;
 
-template <bool GATHER, bool RAC, int EPI>
-__global__ __launch_bounds__(256) void gemm_skinny_kernel(GemmArgs p, int nblk_n) {
-  extern __shared__ __align__(16) unsigned char lds[];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int lr = lane & 15, g = lane >> 4;
-  const int tid = threadIdx.x;
-  const int K = p.K, N = p.N;
-  const int64_t kb2 = K >> 1, kb16 = K >> 4;
-  const int Ks = RAC ? p.Ks : 0;
-  const SkLayout L = sk_layout(K, Ks, RAC);
-  uint32_t *selmap = reinterpret_cast<uint32_t *>(lds + L.selmap);
-  int32_t *prefix = reinterpret_cast<int32_t *>(lds + L.prefix);
-  int32_t *s_sel = reinterpret_cast<int32_t *>(lds + L.sel);
-  uint4 *a_lds = reinterpret_cast<uint4 *>(lds + L.a);
-  uint32_t *as_lds = reinterpret_cast<uint32_t *>(lds + L.as);
-  unsigned char *ares = lds + L.ares;
-  unsigned char *wc = lds + L.wc;
-  float *red = reinterpret_cast<float *>(lds + L.red);
-
-  const int P = blockIdx.x;
-  const int xcd = P & 7, q = P >> 3;
-  const int nb = q % nblk_n;
-  const int e = (q / nblk_n) * 8 + xcd;
-  const int niter = K >> 8;              // 256 elements per iteration
-  const int kpad = (Ks + 31) & ~31;
-
-  if (RAC) {
-    // channel bitmap, per-word prefix counts, the channel list, zero panels
-    for (int i = tid; i < K / 32; i += 256) selmap[i] = 0u;
-    for (int i = tid; i < Ks; i += 256) s_sel[i] = p.sel[i];
-    for (int i = tid; i < SK_ROWS * (L.stride / 4); i += 256)
-      reinterpret_cast<uint32_t *>(wc)[i] = 0u;
-    __syncthreads();
-    for (int i = tid; i < Ks; i += 256) {
-      const int j = s_sel[i];
-      atomicOr(&selmap[j >> 5], 1u << (j & 31));
+  __device__ void seek(SkCur &c, int u) const {
+    int lo = 0, hi = E;                       // last e with pu[e] <= u
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (pu[mid] <= u) lo = mid; else hi = mid;
     }
-    __syncthreads();
-    // exclusive prefix of popcounts (K/32 <= 512 words; 2 per thread)
-    const int nw = K / 32;
-    const int w0 = 2 * tid;
-    int c0 = w0 < nw ? __popc(selmap[w0]) : 0;
-    int c1 = w0 + 1 < nw ? __popc(selmap[w0 + 1]) : 0;
-    int v = c0 + c1, x = v;
+    c.u = u;
+    c.it = 0;
+    c.e = lo;
+    const int r = u - pu[lo];
+    c.p = r / nblk;
+    c.nb = r - c.p * nblk;
+    c.ob = offs[lo];
+    c.rows = offs[lo + 1] - c.ob;
+    c.npass = (c.rows + SK_PR - 1) / SK_PR;
+  }
+  // next stage; returns false (and leaves c alone) at the last one
+  __device__ bool next(SkCur &c) const {
+    if (c.it + 1 < niter) {
+      ++c.it;
+      return true;
+    }
+    if (c.u + 1 >= u1) return false;
+    if (c.nb + 1 < nblk) {
+      ++c.u;
+      ++c.nb;
+      c.it = 0;
+      return true;
+    }
+    seek(c, c.u + 1);
+    return true;
+  }
+};
+
+// One stage's MFMA work for MTV valid m-tiles: weights decoded from
+// registers, activations (and residual) read decoded from LDS.
+template <bool RAC, int MTV>
+__device__ __forceinline__ void sk_stage(const uint4 (&bv)[2][2], const uint32_t (&bsc)[2],
+                                         const unsigned char *dec, uint32_t sm, int lane,
+                                         f32x4 (&acc)[2][2], f32x4 (&accr)[2][2]) {
+  const int lr = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int c2 = 0; c2 < 2; ++c2) {
+    f16x2 blo[2], bhi[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t sp =
+          scale_pair_f16((bsc[j] >> (16 * c2)) & 0xFFu, (bsc[j] >> (16 * c2 + 8)) & 0xFFu);
+      blo[j] = splat_lo(sp);
+      bhi[j] = splat_hi(sp);
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      f16x8 bf[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) bf[j] = decode8(word_of(bv[j][c2], s), s < 2 ? blo[j] : bhi[j]);
+      const int cs = c2 * 4 + s;
+#pragma unroll
+      for (int i = 0; i < MTV; ++i) {
+        const f16x8 af = *reinterpret_cast<const f16x8 *>(
+            dec + ((cs * 4 + g) * SK_PR + i * 16 + lr) * 16);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma16(af, bf[j], acc[i][j]);
+      }
+      if (RAC && ((sm >> cs) & 1u)) {
+#pragma unroll
+        for (int i = 0; i < MTV; ++i) {
+          const f16x8 rf = *reinterpret_cast<const f16x8 *>(
+              dec + SK_DSRC + ((cs * 4 + g) * SK_PR + i * 16 + lr) * 16);
+#pragma unroll
+          for (int j = 0; j < 2; ++j) accr[i][j] = mfma16(rf, bf[j], accr[i][j]);
+        }
+      }
+    }
+  }
+}
+
+template <bool GATHER, bool RAC, int EPI, int NS>
+__global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int nblk) {
+  constexpr int NSRC = RAC ? 2 : 1;
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int lr = lane & 15, g = lane >> 4;
+  const int K = p.K, N = p.N, E = p.E;
+  const int64_t kb2 = K >> 1, kb16 = K >> 4;
+  const SkLayout L = sk_layout(K, E, NSRC, NS);
+  const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
+  int32_t *offs = reinterpret_cast<int32_t *>(lds + L.offs);
+  int32_t *pu = reinterpret_cast<int32_t *>(lds + L.pu);
+  float *swv = reinterpret_cast<float *>(lds + L.sw);
+  uint32_t *smask = reinterpret_cast<uint32_t *>(lds + L.smask);
+  float *red = reinterpret_cast<float *>(lds + L.red);
+  unsigned char *dec = lds + L.dec;
+  const int niter = K >> 8;
+
+  // ---- the unit list: offsets, weight scales, units per expert (scan)
+  for (int e = tid; e <= E; e += SK_THREADS)
+    offs[e] = p.offsets ? p.offsets[e] : (e == 0 ? 0 : (int)p.rows);
+  for (int e = tid; e < E; e += SK_THREADS) swv[e] = p.w_gs[2 * e + 1];
+  if (RAC) {
+    // k-steps (chunk c, step s -> bit 4c + s) of each iteration that hold a
+    // selected channel for some lane group
+    for (int i = tid; i < niter; i += SK_THREADS) smask[i] = 0u;
+  }
+  __syncthreads();
+  if (RAC) {
+    for (int i = tid; i < p.Ks; i += SK_THREADS) {
+      const int c = min(max(p.sel[i], 0), K - 1);
+      atomicOr(&smask[c >> 8], 1u << (((c >> 5) & 1) * 4 + ((c & 31) >> 3)));
+    }
+  }
+  {
+    // exclusive scan of npass(e) * nblk over e (two experts per thread)
+    const int e0 = 2 * tid;
+    auto units = [&](int e) {
+      if (e >= E) return 0;
+      const int rows = max(offs[e + 1] - offs[e], 0);
+      return (rows + SK_PR - 1) / SK_PR * nblk;
+    };
+    const int c0 = units(e0), c1 = units(e0 + 1);
+    const int v = c0 + c1;
+    int xs = v;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-      int y = __shfl_up(x, o, 64);
-      if (lane >= o) x += y;
+      const int y = __shfl_up(xs, o, 64);
+      if (lane >= o) xs += y;
     }
-    if (lane == 63) red[w] = __int_as_float(x);
+    if (lane == 63) red[w] = __int_as_float(xs);
     __syncthreads();
     int base = 0;
     for (int ww = 0; ww < w; ++ww) base += __float_as_int(red[ww]);
-    const int ex = base + x - v;
-    if (w0 < nw) prefix[w0] = ex;
-    if (w0 + 1 < nw) prefix[w0 + 1] = ex + c0;
+    const int ex = base + xs - v;
+    if (e0 <= E) pu[e0] = ex;
+    if (e0 + 1 <= E) pu[e0 + 1] = ex + c0;
     __syncthreads();
   }
+  const int U = pu[E];
+  const int P = blockIdx.x, G = gridDim.x;
+  const int u0 = (int)((int64_t)P * U / G), u1 = (int)((int64_t)(P + 1) * U / G);
+  const SkUnits S{offs, pu, E, nblk, niter, u1};
 
   float vmax = 0.0f;
-  const int64_t ob = (e < p.E) ? (p.offsets ? p.offsets[e] : 0) : 0;
-  const int64_t oe = (e < p.E) ? (p.offsets ? p.offsets[e + 1] : p.rows) : 0;
-  // this wave's two weight-row fragments (clamped rows are loaded, never stored)
-  int64_t wrow[2];
-  bool bval[2];
-  if (EPI == QD_EPI_SWIGLU) {
-    const int I = N >> 1;
-    const int pr = nb * (SK_ROWS / 2) + w * 16 + lr;
-    bval[0] = bval[1] = pr < I;
-    wrow[0] = pr;
-    wrow[1] = pr + I;
-  } else {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      wrow[j] = (int64_t)nb * SK_ROWS + w * 32 + j * 16 + lr;
-      bval[j] = wrow[j] < N;
-    }
-  }
-  const int eb = e < p.E ? e : 0;
-  const uint8_t *bc[2], *bs[2];
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int64_t wr = bval[j] ? wrow[j] : 0;
-    bc[j] = p.w_codes + ((int64_t)eb * N + wr) * kb2 + g * 32;
-    bs[j] = p.w_scales + ((int64_t)eb * N + wr) * kb16 + g * 4;
-  }
-  const float sw = (e < p.E) ? p.w_gs[2 * e + 1] : 0.0f;
-  const float alpha = p.a_gs[1] * sw;
-  const float alpha_r = RAC ? p.r_gs[1] * sw : 0.0f;
+  if (u0 < u1) {
+    SkCur cc;
+    S.seek(cc, u0);
+    const float a_dec = p.a_gs[1];
+    const float r_dec = RAC ? p.r_gs[1] : 0.0f;
+    // ---- issue cursors and their per-lane addresses
+    SkCur ca = cc, cb = cc;
+    const uint8_t *bc0, *bc1, *bs0, *bs1;
+    auto bind_b = [&](const SkCur &c) {
+      int64_t r0, r1;
+      if (EPI == QD_EPI_SWIGLU) {
+        const int I = N >> 1;
+        const int pr_ = c.nb * (SK_ROWS / 2) + w * 16 + lr;
+        r0 = pr_ < I ? pr_ : 0;
+        r1 = pr_ < I ? pr_ + I : 0;
+      } else {
+        const int r = c.nb * SK_ROWS + w * 32 + lr;
+        r0 = r < N ? r : 0;
+        r1 = r + 16 < N ? r + 16 : 0;
+      }
+      r0 += (int64_t)c.e * N;
+      r1 += (int64_t)c.e * N;
+      bc0 = p.w_codes + r0 * kb2 + g * 32;
+      bc1 = p.w_codes + r1 * kb2 + g * 32;
+      bs0 = p.w_scales + r0 * kb16 + g * 4;
+      bs1 = p.w_scales + r1 * kb16 + g * 4;
+    };
+    // activations: a raw slot holds per source [codes: column block b =
+    // 4 * chunk + lane group, 32 rows x 16 B each][scales: lane group,
+    // 32 rows x 4 B].  Waves 0..3 load the codes of x (two column blocks
+    // each), waves 4..7 those of the residual; waves 0, 1 load the scales
+    // of x, waves 2, 3 those of the residual; spare loads go to a junk area.
+    const int a_row = lane & 31;
+    const int a_blk = 2 * (w & 3) + (lane >> 5);
+    const int a_cb = (a_blk & 3) * 32 + (a_blk >> 2) * 16;
+    const int a_sb = (2 * (w & 1) + (lane >> 5)) * 4;
+    const bool c_res = w >= 4, s_res = (w & 2) != 0;
+    const bool c_live = RAC || !c_res, s_live = w < (RAC ? 4 : 2);
+    const uint8_t *ac, *as;
+    int a_e = -1, a_p = -1;
+    auto bind_a = [&](const SkCur &c) {
+      if (c.e == a_e && c.p == a_p) return;
+      a_e = c.e;
+      a_p = c.p;
+      int64_t r = (int64_t)c.ob + (int64_t)c.p * SK_PR + a_row;
+      r = min(r, (int64_t)c.ob + c.rows - 1);
+      const int64_t src = GATHER ? (int64_t)p.row_token[r] : r;
+      ac = (RAC && c_res ? p.r_codes : p.a_codes) + src * kb2 + a_cb;
+      as = (RAC && s_res ? p.r_scales : p.a_scales) + src * kb16 + a_sb;
+    };
+    const uint32_t bring = lds0 + L.b + w * NS * SK_BSTAGE;
+    const uint32_t junk = lds0 + L.junk;
+    auto issue_b = [&](int sg) {
+      const uint32_t slot = uni(bring + (sg % NS) * SK_BSTAGE);
+      const int off = cb.it * 128;
+      dma16(bc0 + off, slot);
+      dma16(bc0 + off + 16, slot + 1024);
+      dma16(bc1 + off, slot + 2048);
+      dma16(bc1 + off + 16, slot + 3072);
+      dma4(bs0 + cb.it * 16, slot + 4096);
+      dma4(bs1 + cb.it * 16, slot + 4096 + 256);
+    };
+    auto issue_a = [&](int sg) {
+      const uint32_t slot = lds0 + L.a + (sg & 1) * (NSRC * SK_ASRC);
+      const uint32_t cdst = slot + (c_res ? SK_ASRC : 0) + (w & 3) * 1024;
+      const uint32_t sdst = slot + (s_res ? SK_ASRC : 0) + 4096 + (w & 1) * 256;
+      dma16(ac + ca.it * 128, uni(c_live ? cdst : junk));
+      dma4(as + ca.it * 16, uni(s_live ? sdst : junk));
+    };
+    auto adv_b = [&]() {
+      const int e = cb.e, nb = cb.nb;
+      if (S.next(cb) && (cb.e != e || cb.nb != nb)) bind_b(cb);
+    };
+    auto adv_a = [&]() {
+      if (S.next(ca)) bind_a(ca);
+    };
 
-  for (int64_t rg = ob; rg < oe; rg += SK_MTMAX * 16) {
-    const int nrow = (int)min((int64_t)SK_MTMAX * 16, oe - rg);
-    const int mt_valid = (nrow + 15) >> 4;
-    // cooperative activation staging: thread t owns row (t & 63) of lane
-    // group ((t >> 6) & 3) for both chunks of an iteration
-    const int arow = tid & 63, ag = (tid >> 6) & 3;
-    const int64_t gsrc = rg + (arow < nrow ? arow : 0);
-    const int64_t asrc = GATHER ? (int64_t)p.row_token[gsrc] : gsrc;
-    const uint8_t *a_c = p.a_codes + asrc * kb2 + ag * 32;
-    const uint8_t *a_s = p.a_scales + asrc * kb16 + ag * 4;
-    __syncthreads();      // the previous pass's panels are no longer read
-    if (RAC) {
-      // compact residual activations: ares[r][i] = rhat[src(r)][S_i] (f16, exact)
-      for (int idx = tid; idx < SK_MTMAX * 16 * kpad; idx += 256) {
-        const int r = idx / kpad, i = idx - r * kpad;
-        _Float16 v = (_Float16)0.0f;
-        if (r < nrow && i < Ks) {
-          const int64_t gr = rg + r;
-          const int64_t src = GATHER ? (int64_t)p.row_token[gr] : gr;
-          const int j = s_sel[i];
-          const uint32_t byte = p.r_codes[src * kb2 + (j >> 1)];
-          const uint32_t c = (j & 1) ? (byte >> 4) : (byte & 15u);
-          float f = e2m1_value(c) * e4m3_to_f32(p.r_scales[src * kb16 + (j >> 4)]);
-          v = (_Float16)((c & 8u) ? -f : f);
-        }
-        *reinterpret_cast<_Float16 *>(ares + r * L.stride + i * 2) = v;
+    // ---- prologue: the steady-state issue order for the virtual
+    // iterations -NS .. -1 (weights of stage i + NS, activations of i + 2)
+    bind_b(cb);
+    bind_a(ca);
+    for (int i = -NS; i < 0; ++i) {
+      issue_b(i + NS);
+      adv_b();
+      if (i + 2 >= 0) {
+        issue_a(i + 2);
+        adv_a();
       }
     }
-    f32x4 acc[SK_MTMAX][2];
-#pragma unroll
-    for (int i = 0; i < SK_MTMAX; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const uint8_t *bc0 = bc[0], *bc1 = bc[1], *bs0 = bs[0], *bs1 = bs[1];
-    // Software pipeline.  Weights: a ring of three register stages (named,
-    // never indexed or moved); the weights of iteration m are issued at the
-    // end of iteration m-3, the activations of iteration m at the end of
-    // iteration m-2 and stored to LDS at the end of iteration m-1.  Issue
-    // order, identical in the prologue and every iteration:
-    //     ... A(m-1) B(m) | A(m) B(m+1) | A(m+1) B(m+2) ...
-    // so B(m) is complete once at most 2*(kALoads+kBLoads) younger loads are
-    // outstanding, and A(m+1) once kBLoads are.  Loads past the last
-    // iteration re-read the last one (never used; they keep the counts
-    // uniform) and are drained before the registers are released.
-    const int last = niter - 1;
-    BStage b0, b1, b2;
-    AStage ast;
-    __syncthreads();     // every earlier load has completed (fence), LDS panels written
-    b0 = load_bstage(bc0, bc1, bs0, bs1, 0);
-    {
-      AStage a0 = load_astage(a_c, a_s, 0);
-      b1 = load_bstage(bc0, bc1, bs0, bs1, min(1, last));
-      ast = load_astage(a_c, a_s, min(1, last));
-      b2 = load_bstage(bc0, bc1, bs0, bs1, min(2, last));
-      wait_a<2 * kBLoads + kALoads>(a0);
-      store_astage(a_lds, as_lds, a0, 0, ag, arow);
-    }
-    __syncthreads();
-
-    auto body = [&](const int it, BStage &bb) {
-      const int stage = it & 1;
-      wait_b<2 * (kALoads + kBLoads)>(bb);
-      // f16 scale factors (value/256) of this iteration: pair (block 2cc, 2cc+1)
-      uint32_t bsp[2][SK_CH];
+    f32x4 acc[2][2], accr[2][2];   // [m-tile][fragment]
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const uint32_t sc = j ? bb.sc1 : bb.sc0;
-#pragma unroll
-        for (int cc = 0; cc < SK_CH; ++cc)
-          bsp[j][cc] = scale_pair_f16((sc >> (16 * cc)) & 0xFFu, (sc >> (16 * cc + 8)) & 0xFFu);
+        acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        accr[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
+
+    for (int sg = 0;; ++sg) {
+      const int nrow = min(SK_PR, cc.rows - cc.p * SK_PR);
+      const int mtv = nrow > 16 ? 2 : 1;
+      // after the activations of stage sg come the weights of stage
+      // sg + NS - 1 and the activations of stage sg + 1: 6 + 2 loads
+      wait_vm<8>();
+      __syncthreads();       // every wave's activations of stage sg have landed
+      const unsigned char *bsl = lds + L.b + (w * NS + sg % NS) * SK_BSTAGE;
+      uint4 bv[2][2];
+      uint32_t bsc[2];
 #pragma unroll
-      for (int cc = 0; cc < SK_CH; ++cc) {
-        // selected channels among this lane group's 32 elements of the chunk
-        const uint32_t word = RAC ? selmap[it * 8 + g * 2 + cc] : 0u;
-        const int base = RAC ? prefix[it * 8 + g * 2 + cc] : 0;
-        const bool any_sel = RAC && __any((int)(word != 0u));
-        uint32_t asp[SK_MTMAX];
+      for (int j = 0; j < 2; ++j) {
 #pragma unroll
-        for (int i = 0; i < SK_MTMAX; ++i) {
-          if (i < mt_valid) {
-            const uint32_t asv = as_lds[(stage * 4 + g) * (SK_MTMAX * 16) + i * 16 + lr];
-            asp[i] = scale_pair_f16((asv >> (16 * cc)) & 0xFFu, (asv >> (16 * cc + 8)) & 0xFFu);
-          }
+        for (int c2 = 0; c2 < 2; ++c2)
+          bv[j][c2] = *reinterpret_cast<const uint4 *>(bsl + (j * 2 + c2) * 1024 + lane * 16);
+        bsc[j] = *reinterpret_cast<const uint32_t *>(bsl + 4096 + j * 256 + lane * 4);
+      }
+      const uint32_t sm = RAC ? smask[cc.it] : 0u;
+      // decode the stage's activation (and residual) rows of the valid
+      // m-tiles: one unit = 8 elements (row, chunk, step, lane group)
+      {
+        const unsigned char *asl = lds + L.a + (sg & 1) * (NSRC * SK_ASRC);
+        const int nunit = mtv * 16 * 32;
+        for (int u = tid; u < NSRC * nunit; u += SK_THREADS) {
+          const int src = u >= nunit ? 1 : 0;
+          const int v = u - src * nunit;
+          const int row = v & 15 | ((v >> 9) << 4);
+          const int cgs = (v >> 4) & 31;            // (chunk * 4 + step) * 4 + lane group
+          const int gg = cgs & 3, cs = cgs >> 2, c2 = cs >> 2, s = cs & 3;
+          const unsigned char *ssl = asl + src * SK_ASRC;
+          const uint32_t word =
+              *reinterpret_cast<const uint32_t *>(ssl + ((c2 * 4 + gg) * SK_PR + row) * 16 + s * 4);
+          const uint32_t sc = *reinterpret_cast<const uint32_t *>(ssl + 4096 + (gg * SK_PR + row) * 4);
+          const uint32_t sb = (sc >> (8 * (c2 * 2 + (s >> 1)))) & 0xFFu;
+          const f16x8 d = decode8(word, splat_lo(scale_pair_f16(sb, 0u)));
+          *reinterpret_cast<f16x8 *>(dec + src * SK_DSRC + (cgs * SK_PR + row) * 16) = d;
         }
+      }
+      // the weight slot is in registers: refill it with the stage NS ahead
+      wait_lds();
+      issue_b(sg + NS);
+      adv_b();
+      __syncthreads();       // the decoded stage is visible; the raw slot is free
+      issue_a(sg + 2);
+      adv_a();
+
+      if (mtv == 1) sk_stage<RAC, 1>(bv, bsc, dec, sm, lane, acc, accr);
+      else sk_stage<RAC, 2>(bv, bsc, dec, sm, lane, acc, accr);
+
+      if (cc.it == niter - 1) {
+        // ---- end of a unit: epilogue
+        const float sw = swv[cc.e];
+        const float alpha = a_dec * sw, alpha_r = r_dec * sw;
+        const int64_t rg = (int64_t)cc.ob + (int64_t)cc.p * SK_PR;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          f16x8 bf[2];
+        for (int i = 0; i < 2; ++i) {
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-            bf[j] = decode8(word_of(bvec(bb, j, cc), s),
-                            s < 2 ? splat_lo(bsp[j][cc]) : splat_hi(bsp[j][cc]));
+          for (int q = 0; q < 4; ++q) {
+            const int rl = i * 16 + g * 4 + q;
+            if (rl < nrow) {
+              const int64_t row = rg + rl;
+              if (EPI == QD_EPI_SWIGLU) {
+                const int I = N >> 1;
+                const int col = cc.nb * (SK_ROWS / 2) + w * 16 + lr;
+                if (col < I) {
+                  float gv = alpha * acc[i][0][q];
+                  float uv = alpha * acc[i][1][q];
+                  if (RAC) {
+                    gv = gv - alpha_r * accr[i][0][q];
+                    uv = uv - alpha_r * accr[i][1][q];
+                  }
+                  const float h = gv / (1.0f + expf(-gv)) * uv;
+                  const uint32_t hb = f32_to_bf16_bits(h);
+                  p.out[row * I + col] = (uint16_t)hb;
+                  vmax = fmaxf(vmax, fabsf(bf16_bits_to_f32(hb)));
+                }
+              } else {
 #pragma unroll
-          for (int i = 0; i < SK_MTMAX; ++i) {
-            if (i < mt_valid) {
-              const uint4 av = a_lds[((stage * SK_CH + cc) * 4 + g) * (SK_MTMAX * 16) + i * 16 + lr];
-              const f16x8 af = decode8(word_of(av, s), s < 2 ? splat_lo(asp[i]) : splat_hi(asp[i]));
-#pragma unroll
-              for (int j = 0; j < 2; ++j) acc[i][j] = mfma16(af, bf[j], acc[i][j]);
-            }
-          }
-          if (any_sel) {
-            // the decoded values of selected channels -> compact weight panel
-            const uint32_t m8 = (word >> (8 * s)) & 0xFFu;
-            if (m8) {
-              const int pos0 = base + __popc(word & ((1u << (8 * s)) - 1u));
-#pragma unroll
-              for (int e8 = 0; e8 < 8; ++e8) {
-                if ((m8 >> e8) & 1u) {
-                  const int pos = pos0 + __popc(m8 & ((1u << e8) - 1u));
-#pragma unroll
-                  for (int j = 0; j < 2; ++j) {
-                    const int rloc = w * 32 + j * 16 + lr;
-                    *reinterpret_cast<_Float16 *>(wc + rloc * L.stride + pos * 2) = bf[j][e8];
+                for (int j = 0; j < 2; ++j) {
+                  const int col = cc.nb * SK_ROWS + w * 32 + j * 16 + lr;
+                  if (col < N) {
+                    float v = alpha * acc[i][j][q];
+                    if (RAC) v = v - alpha_r * accr[i][j][q];
+                    const uint32_t hb = f32_to_bf16_bits(v);
+                    p.out[row * N + col] = (uint16_t)hb;
+                    vmax = fmaxf(vmax, fabsf(bf16_bits_to_f32(hb)));
                   }
                 }
               }
             }
           }
         }
-      }
-      wait_a<kBLoads>(ast);
-      store_astage(a_lds, as_lds, ast, (it + 1) & 1, ag, arow);
-      ast = load_astage(a_c, a_s, min(it + 2, last));
-      bb = load_bstage(bc0, bc1, bs0, bs1, min(it + 3, last));
-      __syncthreads();
-    };
-    for (int it = 0; it < niter; it += 3) {
-      body(it, b0);
-      if (it + 1 < niter) body(it + 1, b1);
-      if (it + 2 < niter) body(it + 2, b2);
-    }
-    // drain the loads still in flight before their registers are reused
-    wait_b<0>(b0);
-    wait_b<0>(b1);
-    wait_b<0>(b2);
-    wait_a<0>(ast);
-    // residual pass over the compact panels
-    f32x4 accr[SK_MTMAX][2];
 #pragma unroll
-    for (int i = 0; i < SK_MTMAX; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j) accr[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (RAC) {
-      for (int ks = 0; ks < kpad; ks += 32) {
-        f16x8 bf[2];
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          bf[j] = *reinterpret_cast<const f16x8 *>(wc + (w * 32 + j * 16 + lr) * L.stride +
-                                                   (ks + g * 8) * 2);
-#pragma unroll
-        for (int i = 0; i < SK_MTMAX; ++i) {
-          if (i < mt_valid) {
-            const f16x8 af =
-                *reinterpret_cast<const f16x8 *>(ares + (i * 16 + lr) * L.stride + (ks + g * 8) * 2);
-#pragma unroll
-            for (int j = 0; j < 2; ++j) accr[i][j] = mfma16(af, bf[j], accr[i][j]);
-          }
-        }
-      }
-    }
-    // epilogue for this pass
-#pragma unroll
-    for (int i = 0; i < SK_MTMAX; ++i) {
-#pragma unroll
-      for (int qq = 0; qq < 4; ++qq) {
-        const int rl = i * 16 + g * 4 + qq;
-        if (rl >= nrow) continue;
-        const int64_t row = rg + rl;
-        if (EPI == QD_EPI_SWIGLU) {
-          const int I = N >> 1;
-          if (bval[0]) {
-            float gv = alpha * acc[i][0][qq];
-            float uv = alpha * acc[i][1][qq];
-            if (RAC) {
-              gv = gv - alpha_r * accr[i][0][qq];
-              uv = uv - alpha_r * accr[i][1][qq];
-            }
-            const float h = gv / (1.0f + expf(-gv)) * uv;
-            const uint32_t hb = f32_to_bf16_bits(h);
-            p.out[row * I + wrow[0]] = (uint16_t)hb;
-            vmax = fmaxf(vmax, fabsf(bf16_bits_to_f32(hb)));
-          }
-        } else {
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int j = 0; j < 2; ++j) {
-            if (bval[j]) {
-              float v = alpha * acc[i][j][qq];
-              if (RAC) v = v - alpha_r * accr[i][j][qq];
-              const uint32_t hb = f32_to_bf16_bits(v);
-              p.out[row * N + wrow[j]] = (uint16_t)hb;
-              vmax = fmaxf(vmax, fabsf(bf16_bits_to_f32(hb)));
-            }
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            accr[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
           }
-        }
       }
+      if (!S.next(cc)) break;
     }
+    // loads past the last stage still target this workgroup's LDS
+    wait_vm<0>();
   }
   const float m = block_max(vmax, red);
-  if (p.amax_part && threadIdx.x == 0) p.amax_part[P] = m;
+  if (p.amax_part && tid == 0) p.amax_part[P] = m;
 }
+
+// host-side plan of the decode kernel
+struct SkPlan {
+  bool ok;
+  int ns, nblk, grid;
+  size_t lds;
+};
 
 inline int64_t skinny_nblk(int64_t N, int epilogue) {
   return epilogue == QD_EPI_SWIGLU ? ((N / 2) + SK_ROWS / 2 - 1) / (SK_ROWS / 2)
                                    : (N + SK_ROWS - 1) / SK_ROWS;
 }
-inline int64_t skinny_grid(int64_t N, int E, int epilogue) {
-  return (int64_t)((E + 7) / 8) * 8 * skinny_nblk(N, epilogue);
-}
-// decode-sized problems: few rows per expert, K a multiple of 256 (whole
-// iterations per quarter) and, with RAC, K_s and K within the panel limits
-inline bool use_skinny(int64_t rows, int E, int64_t K, int Ks) {
-  return K % 256 == 0 && rows <= (int64_t)E * 48 && Ks <= SK_KSMAX &&
-         (Ks == 0 || K <= SK_KMAX);
+
+// Decode-sized problems: few rows per expert and whole 256-element
+// iterations.  With RAC the activation stages carry the residual as well
+// and the weight ring is two stages deep (three without).
+inline SkPlan skinny_plan(int64_t rows, int E, int64_t N, int64_t K, int Ks, int epilogue) {
+  SkPlan pl{};
+  const bool rac = Ks > 0;
+  if (K < 256 || K % 256 != 0 || K > SK_KMAX || E > SK_EMAX || rows > (int64_t)E * 48) return pl;
+  pl.ns = rac ? 2 : 3;
+  const int64_t nblk = skinny_nblk(N, epilogue);
+  pl.nblk = (int)nblk;
+  pl.grid = (int)std::min<int64_t>(SK_GRID, (int64_t)E * nblk * 4);
+  pl.lds = (size_t)sk_layout((int)K, E, rac ? 2 : 1, pl.ns).total;
+  if (pl.lds > (size_t)SK_LDS_MAX) return pl;
+  pl.ok = true;
+  return pl;
 }
 
 inline int64_t grid_x(int64_t rows, int E, bool grouped) {
@@ -699,16 +749,22 @@ inline int64_t grid_y(int64_t N, int epilogue) {
   return epilogue == QD_EPI_SWIGLU ? ((N / 2) + 31) / 32 : (N + BN - 1) / BN;
 }
 
+template <bool GATHER, bool RAC, int EPI, int NS>
+void launch_skinny(const GemmArgs &p, const SkPlan &pl, hipStream_t s) {
+  auto kern = gemm_skinny_kernel<GATHER, RAC, EPI, NS>;
+  static const bool attr = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               SK_LDS_MAX) == hipSuccess;
+  (void)attr;
+  hipLaunchKernelGGL(kern, dim3((unsigned)pl.grid), dim3(SK_THREADS), pl.lds, s, p, pl.nblk);
+}
+
 template <bool GATHER, bool RAC>
-void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, bool skinny, int nblk_n) {
-  if (skinny) {
-    const size_t lds = (size_t)sk_layout(p.K, RAC ? p.Ks : 0, RAC).total;
-    if (epi == QD_EPI_SWIGLU)
-      hipLaunchKernelGGL((gemm_skinny_kernel<GATHER, RAC, QD_EPI_SWIGLU>), grid, dim3(256), lds, s,
-                         p, nblk_n);
-    else
-      hipLaunchKernelGGL((gemm_skinny_kernel<GATHER, RAC, QD_EPI_NONE>), grid, dim3(256), lds, s,
-                         p, nblk_n);
+void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, const SkPlan &pl) {
+  if (pl.ok) {
+    constexpr int NS = RAC ? 2 : 3;
+    if (epi == QD_EPI_SWIGLU) launch_skinny<GATHER, RAC, QD_EPI_SWIGLU, NS>(p, pl, s);
+    else launch_skinny<GATHER, RAC, QD_EPI_NONE, NS>(p, pl, s);
     return;
   }
   if (epi == QD_EPI_SWIGLU)
@@ -722,7 +778,8 @@ void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, bool skinn
 extern "C" int64_t moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int64_t K,
                                                     int32_t E, int32_t Ks, int32_t epilogue) {
   if (rows < 0 || N <= 0 || K <= 0 || E < 1 || Ks < 0) return 0;
-  if (use_skinny(rows, E, K, Ks)) return skinny_grid(N, E, epilogue);
+  const SkPlan pl = skinny_plan(rows, E, N, K, Ks, epilogue);
+  if (pl.ok) return pl.grid;
   return grid_x(rows, E, true) * grid_y(N, epilogue);
 }
 
@@ -783,16 +840,15 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
   }
   p.out = static_cast<uint16_t *>(out);
   p.amax_part = amax_partials;
-  const bool skinny = use_skinny(rows, E, K, rac ? Ks : 0);
-  const int nblk_n = (int)skinny_nblk(N, epilogue);
-  dim3 grid = skinny ? dim3((unsigned)skinny_grid(N, E, epilogue)) : dim3((unsigned)gx, (unsigned)gy);
+  const SkPlan pl = skinny_plan(rows, E, N, K, rac ? Ks : 0, epilogue);
+  dim3 grid((unsigned)gx, (unsigned)gy);
   hipStream_t s = qdh::S(stream);
   if (row_token) {
-    if (rac) launch_epi<true, true>(p, epilogue, grid, s, skinny, nblk_n);
-    else launch_epi<true, false>(p, epilogue, grid, s, skinny, nblk_n);
+    if (rac) launch_epi<true, true>(p, epilogue, grid, s, pl);
+    else launch_epi<true, false>(p, epilogue, grid, s, pl);
   } else {
-    if (rac) launch_epi<false, true>(p, epilogue, grid, s, skinny, nblk_n);
-    else launch_epi<false, false>(p, epilogue, grid, s, skinny, nblk_n);
+    if (rac) launch_epi<false, true>(p, epilogue, grid, s, pl);
+    else launch_epi<false, false>(p, epilogue, grid, s, pl);
   }
   return qdh::check_launch();
 }
