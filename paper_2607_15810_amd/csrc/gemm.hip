@@ -275,16 +275,16 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs p) {
 //    weights cost no registers.  One stage is 256 K-elements of 32 rows
 //    (4 KB of codes, 512 B of scales).
 //  * The 32 activation rows of the pass (with RAC also their masked
-//    residual rows) go through a two-slot LDS ring filled the same way.
-//    The waves decode each stage of them once, together, into an f16 LDS
-//    buffer; every wave then reads its MFMA operands from there.
-//  * Loads are issued in one fixed order per iteration (weights NS stages
-//    ahead right after the stage in hand has been read into registers,
-//    activations two stages ahead once their slot is free), so one explicit
-//    vmcnt wait at the top of each iteration proves that the current stage
-//    has landed; loads past the last stage repeat the last stage's
-//    addresses into slots that are never read again.
-//  * Weights are decoded exactly to f16 in registers (see the top of this
+//    residual rows) go through a four-slot LDS ring filled the same way
+//    and shared by the waves; each wave decodes the fragments it needs.
+//  * Loads are issued in one fixed order per iteration: the activations,
+//    then the weights of the stage three ahead, spread over the k-steps.
+//    Loads complete in issue order, so one explicit "vmcnt <= 16" at the
+//    top of each iteration proves that both have landed for the stage in
+//    hand while the next two stages stay in flight.  Loads past the last
+//    stage repeat the last stage's addresses into slots that are never
+//    read again.
+//  * Operands are decoded exactly to f16 in registers (see the top of this
 //    file) and multiplied on MFMA, with straight-line code for each number
 //    of valid 16-row m-tiles.
 //  * RAC: the masked residual is zero outside the selected channels S, so
@@ -302,14 +302,14 @@ constexpr int SK_ROWS = 32 * SK_WAVES;   // weight rows per unit
 constexpr int SK_PR = 32;                // activation rows per pass
 constexpr int SK_BSTAGE = 4608;          // bytes per wave and weight stage
 constexpr int SK_ASRC = SK_PR * 144;     // raw activation stage of one source
-constexpr int SK_DSRC = SK_PR * 512;     // decoded (f16) stage of one source
+constexpr int SK_NA = 4;                 // activation slots
 constexpr int SK_KMAX = 65536;
-constexpr int SK_EMAX = 1023;            // experts (offsets and their scan kept in LDS)
+constexpr int SK_EMAX = 512;             // experts (offsets and their scan kept in LDS)
 constexpr int SK_LDS_MAX = 160 * 1024;
 constexpr int SK_GRID = 256;             // one workgroup per CU
 
 struct SkLayout {
-  int b, a, dec, junk, offs, pu, sw, smask, red, total;
+  int b, a, junk, offs, pu, sw, smask, red, total;
 };
 
 // nsrc = 1 (activations) or 2 (activations and masked residual)
@@ -318,8 +318,7 @@ __host__ __device__ inline SkLayout sk_layout(int K, int E, int nsrc, int ns) {
   int o = 0;
   auto take = [&](int bytes) { int at = o; o += (bytes + 15) & ~15; return at; };
   L.b = take(SK_WAVES * ns * SK_BSTAGE);
-  L.a = take(2 * nsrc * SK_ASRC);
-  L.dec = take(nsrc * SK_DSRC);
+  L.a = take(SK_NA * nsrc * SK_ASRC);
   L.junk = take(1024);
   L.offs = take((E + 1) * 4);
   L.pu = take((E + 1) * 4);
@@ -354,7 +353,7 @@ __device__ __forceinline__ uint32_t uni(uint32_t v) { return __builtin_amdgcn_re
 // Position in a workgroup's stage sequence: unit u = (expert e, pass p,
 // block nb), iteration it over K.  All fields are workgroup-uniform.
 struct SkCur {
-  int u, it, e, p, nb, ob, rows, npass;
+  int u, it, e, p, nb, ob, rows;
 };
 
 struct SkUnits {
@@ -366,17 +365,17 @@ struct SkUnits {
     int lo = 0, hi = E;                       // last e with pu[e] <= u
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
-      if (pu[mid] <= u) lo = mid; else hi = mid;
+      if ((int)uni((uint32_t)pu[mid]) <= u) lo = mid; else hi = mid;
     }
+    // (LDS loads land in vector registers; the values are uniform)
     c.u = u;
     c.it = 0;
-    c.e = lo;
-    const int r = u - pu[lo];
+    c.e = (int)uni((uint32_t)lo);
+    const int r = u - (int)uni((uint32_t)pu[c.e]);
     c.p = r / nblk;
     c.nb = r - c.p * nblk;
-    c.ob = offs[lo];
-    c.rows = offs[lo + 1] - c.ob;
-    c.npass = (c.rows + SK_PR - 1) / SK_PR;
+    c.ob = (int)uni((uint32_t)offs[c.e]);
+    c.rows = (int)uni((uint32_t)offs[c.e + 1]) - c.ob;
   }
   // next stage; returns false (and leaves c alone) at the last one
   __device__ bool next(SkCur &c) const {
@@ -396,43 +395,91 @@ struct SkUnits {
   }
 };
 
-// One stage's MFMA work for MTV valid m-tiles: weights decoded from
-// registers, activations (and residual) read decoded from LDS.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// One weight stage of a wave: fragment j (16 rows) x chunk c of 16 code
+// bytes per lane, and the lane's scale dword of each fragment.
+struct BReg {
+  u32x4 c00, c01, c10, c11;
+  uint32_t s0, s1;
+};
+// Raw activation (and residual) data of one stage for MTV m-tiles, read
+// from the LDS slot in the same batch as the weights.
+template <int MTV>
+struct ARaw {
+  uint4 x[2][MTV];      // [chunk][m-tile]: the lane's 16 code bytes
+  uint32_t xs[MTV];     // the lane's scale dword
+  uint4 r[2][MTV];      // the same for the residual
+  uint32_t rs[MTV];
+};
 template <bool RAC, int MTV>
-__device__ __forceinline__ void sk_stage(const uint4 (&bv)[2][2], const uint32_t (&bsc)[2],
-                                         const unsigned char *dec, uint32_t sm, int lane,
-                                         f32x4 (&acc)[2][2], f32x4 (&accr)[2][2]) {
+__device__ __forceinline__ void load_araw(ARaw<MTV> &a, const unsigned char *asl, bool res,
+                                          int lane) {
   const int lr = lane & 15, g = lane >> 4;
 #pragma unroll
-  for (int c2 = 0; c2 < 2; ++c2) {
-    f16x2 blo[2], bhi[2];
+  for (int i = 0; i < MTV; ++i) {
+    const int rr = i * 16 + lr;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const uint32_t sp =
-          scale_pair_f16((bsc[j] >> (16 * c2)) & 0xFFu, (bsc[j] >> (16 * c2 + 8)) & 0xFFu);
-      blo[j] = splat_lo(sp);
-      bhi[j] = splat_hi(sp);
+    for (int c2 = 0; c2 < 2; ++c2)
+      a.x[c2][i] = *reinterpret_cast<const uint4 *>(asl + ((c2 * 4 + g) * SK_PR + rr) * 16);
+    a.xs[i] = *reinterpret_cast<const uint32_t *>(asl + 4096 + (g * SK_PR + rr) * 4);
+    if (RAC && res) {
+      const unsigned char *rsl = asl + SK_ASRC;
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2)
+        a.r[c2][i] = *reinterpret_cast<const uint4 *>(rsl + ((c2 * 4 + g) * SK_PR + rr) * 16);
+      a.rs[i] = *reinterpret_cast<const uint32_t *>(rsl + 4096 + (g * SK_PR + rr) * 4);
+    }
+  }
+}
+
+// f16 pair (value / 256) of E4M3 scale bytes (b >> sh) & 0xFF and the next
+__device__ __forceinline__ uint32_t scale_pair_at(uint32_t b, int sh) {
+  return scale_pair_f16((b >> sh) & 0xFFu, (b >> (sh + 8)) & 0xFFu);
+}
+
+// One stage's MFMA work for MTV valid m-tiles, all operands decoded to f16
+// from registers.  hook(k) runs before k-step k (0..7): the caller issues
+// its loads for later stages there, spread over the stage.
+template <bool RAC, int MTV, typename Hook>
+__device__ __forceinline__ void sk_stage(const BReg &b, const ARaw<MTV> &a, uint32_t sm,
+                                         f32x4 (&acc)[2][2], f32x4 (&accr)[2][2], Hook &&hook) {
+#pragma unroll
+  for (int c2 = 0; c2 < 2; ++c2) {
+    const u32x4 bv0 = c2 ? b.c01 : b.c00;
+    const u32x4 bv1 = c2 ? b.c11 : b.c10;
+    const uint32_t sp0 = scale_pair_at(b.s0, 16 * c2), sp1 = scale_pair_at(b.s1, 16 * c2);
+    const f16x2 b0lo = splat_lo(sp0), b0hi = splat_hi(sp0);
+    const f16x2 b1lo = splat_lo(sp1), b1hi = splat_hi(sp1);
+    f16x2 alo[MTV], ahi[MTV], rlo[MTV], rhi[MTV];
+    const bool rchunk = RAC && ((sm >> (4 * c2)) & 15u) != 0u;
+#pragma unroll
+    for (int i = 0; i < MTV; ++i) {
+      const uint32_t ap = scale_pair_at(a.xs[i], 16 * c2);
+      alo[i] = splat_lo(ap);
+      ahi[i] = splat_hi(ap);
+      if (rchunk) {
+        const uint32_t rp = scale_pair_at(a.rs[i], 16 * c2);
+        rlo[i] = splat_lo(rp);
+        rhi[i] = splat_hi(rp);
+      }
     }
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      f16x8 bf[2];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) bf[j] = decode8(word_of(bv[j][c2], s), s < 2 ? blo[j] : bhi[j]);
-      const int cs = c2 * 4 + s;
+      hook(c2 * 4 + s);
+      const f16x8 bf0 = decode8(bv0[s], s < 2 ? b0lo : b0hi);
+      const f16x8 bf1 = decode8(bv1[s], s < 2 ? b1lo : b1hi);
 #pragma unroll
       for (int i = 0; i < MTV; ++i) {
-        const f16x8 af = *reinterpret_cast<const f16x8 *>(
-            dec + ((cs * 4 + g) * SK_PR + i * 16 + lr) * 16);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma16(af, bf[j], acc[i][j]);
+        const f16x8 af = decode8(word_of(a.x[c2][i], s), s < 2 ? alo[i] : ahi[i]);
+        acc[i][0] = mfma16(af, bf0, acc[i][0]);
+        acc[i][1] = mfma16(af, bf1, acc[i][1]);
       }
-      if (RAC && ((sm >> cs) & 1u)) {
+      if (RAC && ((sm >> (4 * c2 + s)) & 1u)) {
 #pragma unroll
         for (int i = 0; i < MTV; ++i) {
-          const f16x8 rf = *reinterpret_cast<const f16x8 *>(
-              dec + SK_DSRC + ((cs * 4 + g) * SK_PR + i * 16 + lr) * 16);
-#pragma unroll
-          for (int j = 0; j < 2; ++j) accr[i][j] = mfma16(rf, bf[j], accr[i][j]);
+          const f16x8 rf = decode8(word_of(a.r[c2][i], s), s < 2 ? rlo[i] : rhi[i]);
+          accr[i][0] = mfma16(rf, bf0, accr[i][0]);
+          accr[i][1] = mfma16(rf, bf1, accr[i][1]);
         }
       }
     }
@@ -455,7 +502,6 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
   float *swv = reinterpret_cast<float *>(lds + L.sw);
   uint32_t *smask = reinterpret_cast<uint32_t *>(lds + L.smask);
   float *red = reinterpret_cast<float *>(lds + L.red);
-  unsigned char *dec = lds + L.dec;
   const int niter = K >> 8;
 
   // ---- the unit list: offsets, weight scales, units per expert (scan)
@@ -499,7 +545,7 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     if (e0 + 1 <= E) pu[e0 + 1] = ex + c0;
     __syncthreads();
   }
-  const int U = pu[E];
+  const int U = (int)uni((uint32_t)pu[E]);
   const int P = blockIdx.x, G = gridDim.x;
   const int u0 = (int)((int64_t)P * U / G), u1 = (int)((int64_t)(P + 1) * U / G);
   const SkUnits S{offs, pu, E, nblk, niter, u1};
@@ -568,7 +614,7 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
       dma4(bs1 + cb.it * 16, slot + 4096 + 256);
     };
     auto issue_a = [&](int sg) {
-      const uint32_t slot = lds0 + L.a + (sg & 1) * (NSRC * SK_ASRC);
+      const uint32_t slot = lds0 + L.a + (sg % SK_NA) * (NSRC * SK_ASRC);
       const uint32_t cdst = slot + (c_res ? SK_ASRC : 0) + (w & 3) * 1024;
       const uint32_t sdst = slot + (s_res ? SK_ASRC : 0) + 4096 + (w & 1) * 256;
       dma16(ac + ca.it * 128, uni(c_live ? cdst : junk));
@@ -583,16 +629,14 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     };
 
     // ---- prologue: the steady-state issue order for the virtual
-    // iterations -NS .. -1 (weights of stage i + NS, activations of i + 2)
+    // iterations -3 .. -1 (activations, then weights, of stage i + 3)
     bind_b(cb);
     bind_a(ca);
-    for (int i = -NS; i < 0; ++i) {
-      issue_b(i + NS);
+    for (int i = 0; i < 3; ++i) {
+      issue_a(i);
+      adv_a();
+      issue_b(i);
       adv_b();
-      if (i + 2 >= 0) {
-        issue_a(i + 2);
-        adv_a();
-      }
     }
 
     f32x4 acc[2][2], accr[2][2];   // [m-tile][fragment]
@@ -607,51 +651,57 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     for (int sg = 0;; ++sg) {
       const int nrow = min(SK_PR, cc.rows - cc.p * SK_PR);
       const int mtv = nrow > 16 ? 2 : 1;
-      // after the activations of stage sg come the weights of stage
-      // sg + NS - 1 and the activations of stage sg + 1: 6 + 2 loads
-      wait_vm<8>();
+      // after the weights of stage sg come the loads of stages sg + 1 and
+      // sg + 2: 2 x 8
+      wait_vm<16>();
       __syncthreads();       // every wave's activations of stage sg have landed
       const unsigned char *bsl = lds + L.b + (w * NS + sg % NS) * SK_BSTAGE;
-      uint4 bv[2][2];
-      uint32_t bsc[2];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-#pragma unroll
-        for (int c2 = 0; c2 < 2; ++c2)
-          bv[j][c2] = *reinterpret_cast<const uint4 *>(bsl + (j * 2 + c2) * 1024 + lane * 16);
-        bsc[j] = *reinterpret_cast<const uint32_t *>(bsl + 4096 + j * 256 + lane * 4);
-      }
+      BReg b;
+      b.c00 = *reinterpret_cast<const u32x4 *>(bsl + 0 * 1024 + lane * 16);
+      b.c01 = *reinterpret_cast<const u32x4 *>(bsl + 1 * 1024 + lane * 16);
+      b.c10 = *reinterpret_cast<const u32x4 *>(bsl + 2 * 1024 + lane * 16);
+      b.c11 = *reinterpret_cast<const u32x4 *>(bsl + 3 * 1024 + lane * 16);
+      b.s0 = *reinterpret_cast<const uint32_t *>(bsl + 4096 + lane * 4);
+      b.s1 = *reinterpret_cast<const uint32_t *>(bsl + 4096 + 256 + lane * 4);
       const uint32_t sm = RAC ? smask[cc.it] : 0u;
-      // decode the stage's activation (and residual) rows of the valid
-      // m-tiles: one unit = 8 elements (row, chunk, step, lane group)
-      {
-        const unsigned char *asl = lds + L.a + (sg & 1) * (NSRC * SK_ASRC);
-        const int nunit = mtv * 16 * 32;
-        for (int u = tid; u < NSRC * nunit; u += SK_THREADS) {
-          const int src = u >= nunit ? 1 : 0;
-          const int v = u - src * nunit;
-          const int row = v & 15 | ((v >> 9) << 4);
-          const int cgs = (v >> 4) & 31;            // (chunk * 4 + step) * 4 + lane group
-          const int gg = cgs & 3, cs = cgs >> 2, c2 = cs >> 2, s = cs & 3;
-          const unsigned char *ssl = asl + src * SK_ASRC;
-          const uint32_t word =
-              *reinterpret_cast<const uint32_t *>(ssl + ((c2 * 4 + gg) * SK_PR + row) * 16 + s * 4);
-          const uint32_t sc = *reinterpret_cast<const uint32_t *>(ssl + 4096 + (gg * SK_PR + row) * 4);
-          const uint32_t sb = (sc >> (8 * (c2 * 2 + (s >> 1)))) & 0xFFu;
-          const f16x8 d = decode8(word, splat_lo(scale_pair_f16(sb, 0u)));
-          *reinterpret_cast<f16x8 *>(dec + src * SK_DSRC + (cgs * SK_PR + row) * 16) = d;
+      const unsigned char *asl = lds + L.a + (sg % SK_NA) * (NSRC * SK_ASRC);
+      // loads of stage sg + 3, one before each k-step: the activations into
+      // the slot every wave has finished with, then the weights into the
+      // slot just read
+      auto hook = [&](int k) {
+        if (k < 2) {
+          const uint32_t slot = lds0 + L.a + ((sg + 3) % SK_NA) * (NSRC * SK_ASRC);
+          if (k == 0) {
+            const uint32_t cdst = slot + (c_res ? SK_ASRC : 0) + (w & 3) * 1024;
+            dma16(ac + ca.it * 128, uni(c_live ? cdst : junk));
+          } else {
+            const uint32_t sdst = slot + (s_res ? SK_ASRC : 0) + 4096 + (w & 1) * 256;
+            dma4(as + ca.it * 16, uni(s_live ? sdst : junk));
+          }
+        } else {
+          const uint32_t slot = uni(bring + (sg % NS) * SK_BSTAGE);
+          const int off = cb.it * 128, soff = cb.it * 16;
+          if (k == 2) dma16(bc0 + off, slot);
+          if (k == 3) dma16(bc0 + off + 16, slot + 1024);
+          if (k == 4) dma16(bc1 + off, slot + 2048);
+          if (k == 5) dma16(bc1 + off + 16, slot + 3072);
+          if (k == 6) dma4(bs0 + soff, slot + 4096);
+          if (k == 7) dma4(bs1 + soff, slot + 4096 + 256);
         }
+      };
+      if (mtv == 1) {
+        ARaw<1> a;
+        load_araw<RAC, 1>(a, asl, sm != 0u, lane);
+        wait_lds();          // the weight slot may be refilled from here on
+        sk_stage<RAC, 1>(b, a, sm, acc, accr, hook);
+      } else {
+        ARaw<2> a;
+        load_araw<RAC, 2>(a, asl, sm != 0u, lane);
+        wait_lds();
+        sk_stage<RAC, 2>(b, a, sm, acc, accr, hook);
       }
-      // the weight slot is in registers: refill it with the stage NS ahead
-      wait_lds();
-      issue_b(sg + NS);
-      adv_b();
-      __syncthreads();       // the decoded stage is visible; the raw slot is free
-      issue_a(sg + 2);
       adv_a();
-
-      if (mtv == 1) sk_stage<RAC, 1>(bv, bsc, dec, sm, lane, acc, accr);
-      else sk_stage<RAC, 2>(bv, bsc, dec, sm, lane, acc, accr);
+      adv_b();
 
       if (cc.it == niter - 1) {
         // ---- end of a unit: epilogue
@@ -716,9 +766,10 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
 // host-side plan of the decode kernel
 struct SkPlan {
   bool ok;
-  int ns, nblk, grid;
+  int nblk, grid;
   size_t lds;
 };
+constexpr int SK_NS = 3;                 // weight ring depth
 
 inline int64_t skinny_nblk(int64_t N, int epilogue) {
   return epilogue == QD_EPI_SWIGLU ? ((N / 2) + SK_ROWS / 2 - 1) / (SK_ROWS / 2)
@@ -726,17 +777,15 @@ inline int64_t skinny_nblk(int64_t N, int epilogue) {
 }
 
 // Decode-sized problems: few rows per expert and whole 256-element
-// iterations.  With RAC the activation stages carry the residual as well
-// and the weight ring is two stages deep (three without).
+// iterations.
 inline SkPlan skinny_plan(int64_t rows, int E, int64_t N, int64_t K, int Ks, int epilogue) {
   SkPlan pl{};
   const bool rac = Ks > 0;
   if (K < 256 || K % 256 != 0 || K > SK_KMAX || E > SK_EMAX || rows > (int64_t)E * 48) return pl;
-  pl.ns = rac ? 2 : 3;
   const int64_t nblk = skinny_nblk(N, epilogue);
   pl.nblk = (int)nblk;
   pl.grid = (int)std::min<int64_t>(SK_GRID, (int64_t)E * nblk * 4);
-  pl.lds = (size_t)sk_layout((int)K, E, rac ? 2 : 1, pl.ns).total;
+  pl.lds = (size_t)sk_layout((int)K, E, rac ? 2 : 1, SK_NS).total;
   if (pl.lds > (size_t)SK_LDS_MAX) return pl;
   pl.ok = true;
   return pl;
@@ -749,9 +798,9 @@ inline int64_t grid_y(int64_t N, int epilogue) {
   return epilogue == QD_EPI_SWIGLU ? ((N / 2) + 31) / 32 : (N + BN - 1) / BN;
 }
 
-template <bool GATHER, bool RAC, int EPI, int NS>
+template <bool GATHER, bool RAC, int EPI>
 void launch_skinny(const GemmArgs &p, const SkPlan &pl, hipStream_t s) {
-  auto kern = gemm_skinny_kernel<GATHER, RAC, EPI, NS>;
+  auto kern = gemm_skinny_kernel<GATHER, RAC, EPI, SK_NS>;
   static const bool attr = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize,
                                                SK_LDS_MAX) == hipSuccess;
@@ -762,9 +811,8 @@ void launch_skinny(const GemmArgs &p, const SkPlan &pl, hipStream_t s) {
 template <bool GATHER, bool RAC>
 void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, const SkPlan &pl) {
   if (pl.ok) {
-    constexpr int NS = RAC ? 2 : 3;
-    if (epi == QD_EPI_SWIGLU) launch_skinny<GATHER, RAC, QD_EPI_SWIGLU, NS>(p, pl, s);
-    else launch_skinny<GATHER, RAC, QD_EPI_NONE, NS>(p, pl, s);
+    if (epi == QD_EPI_SWIGLU) launch_skinny<GATHER, RAC, QD_EPI_SWIGLU>(p, pl, s);
+    else launch_skinny<GATHER, RAC, QD_EPI_NONE>(p, pl, s);
     return;
   }
   if (epi == QD_EPI_SWIGLU)
