@@ -7,9 +7,11 @@
 //   rac_amax_kernel / rac_scores_kernel  the score pass when the quantiser did
 //                        not fuse it (reads x and its NVFP4 codes, recomputes
 //                        r = x_hat - x, fixed-point u64 sums).
-//   rac_select_kernel    one workgroup: radix select of the K_s largest u64
-//                        scores (ties to the lower channel), ascending list and
-//                        a channel bitmap.
+//   rac_select_ballot_kernel / rac_select_kernel  one workgroup: the K_s
+//                        largest u64 scores (ties to the lower channel) by a
+//                        radix select (4-bit digits counted with wave ballots for
+//                        K <= 16384, 8-bit LDS histograms above); ascending list
+//                        and a channel bitmap.
 //   rac_resq_kernel      residual quantised over all channels with its own
 //                        tensor scale (max|r|), then masked to S.
 //   rac_residual_gemm_kernel  the residual contraction over S alone (f32 out).
@@ -126,7 +128,8 @@ __device__ int block_exclusive_scan(int v, int *sh /* 1024 + 32 ints */, int &to
   __syncthreads();
   if (tid == 0) {
     int run = 0;
-    for (int w = 0; w < 16; ++w) {
+    const int nwv = (int)(blockDim.x >> 6);
+    for (int w = 0; w < nwv; ++w) {
       int c = sh[1024 + w];
       sh[1024 + w] = run;
       run += c;
@@ -261,6 +264,141 @@ __global__ __launch_bounds__(1024) void rac_select_kernel(const uint64_t *__rest
   }
 }
 
+// Selection for K <= 16384 channels: radix select on 4-bit digits from the
+// highest non-zero digit of the largest score down.  Digit counts come from
+// wave ballots (no atomics: most channels share their leading digits, which
+// would serialise histogram atomics).  Each wave posts its 16 counts, one
+// barrier, and every wave then derives the same digit from the posted
+// counts (double-buffered, so one barrier per digit).  Thread i owns
+// channels i, i + 512, ... in registers.  Channels above the threshold theta
+// are taken, then channels equal to it in ascending order until K_s (a
+// popcount scan over a bitmap of the equal ones); a popcount scan of the
+// selection bitmap emits S in ascending order.
+constexpr int kSelThreads = 512;
+constexpr int kSelWaves = kSelThreads / 64;
+
+template <int PER>
+__global__ __launch_bounds__(kSelThreads) void rac_select_ballot_kernel(
+    const uint64_t *__restrict__ scores, int K, int Ks, int32_t *__restrict__ sel_idx,
+    uint32_t *__restrict__ bitmap) {
+  __shared__ int cnt[2][kSelWaves][16];     // [pass parity][wave][digit]
+  __shared__ uint32_t gt[16384 / 32], eq[16384 / 32];
+  __shared__ int sh[1024 + 32];
+  __shared__ uint64_t s_max[kSelWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int nw = (K + 31) / 32;
+  uint64_t sv[PER];
+  bool live[PER];
+  uint64_t mx = 0ull;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int j = tid + kSelThreads * i;
+    live[i] = j < K;
+    sv[i] = live[i] ? scores[j] : 0ull;
+    mx = sv[i] > mx ? sv[i] : mx;
+  }
+  for (int w = tid; w < nw; w += kSelThreads) {
+    gt[w] = 0u;
+    eq[w] = 0u;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t y = __shfl_xor(mx, o, 64);
+    mx = y > mx ? y : mx;
+  }
+  if (lane == 0) s_max[wid] = mx;
+  __syncthreads();
+  mx = 0ull;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) mx = s_max[w] > mx ? s_max[w] : mx;
+  // theta = the K_s-th largest score; every wave tracks (prefix, remaining)
+  uint64_t pre = 0ull, msk = 0ull;
+  int rem = Ks;
+  if (Ks > 0 && mx != 0ull) {
+    const int top = (63 - __clzll((long long)mx)) >> 2;
+    for (int d = top, par = 0; d >= 0; --d, par ^= 1) {
+      // per-lane digit counts packed as 16-bit fields: digit q lives in
+      // word q >> 2, bits 16 (q & 3) .. +15; summed over the wave's lanes
+      // (at most 64 * PER < 2^16 per digit)
+      uint64_t pk[4] = {0ull, 0ull, 0ull, 0ull};
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const bool m = live[i] && (sv[i] & msk) == pre;
+        const int dig = (int)((sv[i] >> (4 * d)) & 15ull);
+        const uint64_t inc = m ? (1ull << (16 * (dig & 3))) : 0ull;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) pk[q] += (dig >> 2) == q ? inc : 0ull;
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) pk[q] += __shfl_xor(pk[q], o, 64);
+      // lane b < 16: this wave's count of digit b
+      int mine = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if ((lane >> 2) == q) mine = (int)((pk[q] >> (16 * (lane & 3))) & 0xFFFFull);
+      if (lane < 16) cnt[par][wid][lane] = mine;
+      __syncthreads();
+      // lane l < 16 holds digit 15 - l; an inclusive scan over the lanes
+      // counts the candidates at or above each digit
+      const int b = 15 - (lane & 15);
+      int c = 0;
+#pragma unroll
+      for (int w = 0; w < kSelWaves; ++w) c += cnt[par][w][b];
+      c = lane < 16 ? c : 0;
+      int incl = c;
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        const int y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      const uint64_t hit = __ballot(lane < 16 && incl >= rem);
+      const int L = __ffsll((long long)hit) - 1;
+      const int above = __shfl(incl - c, L, 64);
+      pre |= (uint64_t)(15 - L) << (4 * d);
+      rem -= above;
+      msk |= 15ull << (4 * d);
+    }
+  }
+  const uint64_t theta = pre;
+  const int take_eq = Ks > 0 ? rem : 0;    // channels equal to theta to keep
+  if (Ks > 0) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int j = tid + kSelThreads * i;
+      if (live[i]) {
+        if (sv[i] > theta) atomicOr(&gt[j >> 5], 1u << (j & 31));
+        else if (sv[i] == theta) atomicOr(&eq[j >> 5], 1u << (j & 31));
+      }
+    }
+  }
+  __syncthreads();
+  // nw <= 512: one word per thread
+  const uint32_t e = tid < nw ? eq[tid] : 0u;
+  int tot;
+  const int eq_before = block_exclusive_scan(__popc(e), sh, tot);
+  uint32_t word = tid < nw ? gt[tid] : 0u;
+  {
+    int need = take_eq - eq_before;
+    uint32_t m = e;
+    while (need > 0 && m) {
+      word |= m & (0u - m);         // lowest remaining equal channel
+      m &= m - 1u;
+      --need;
+    }
+  }
+  int pos = block_exclusive_scan(__popc(word), sh, tot);
+  if (tid < nw) {
+    bitmap[tid] = word;
+    uint32_t m = word;
+    while (m) {
+      sel_idx[pos++] = tid * 32 + (__ffs(m) - 1);
+      m &= m - 1u;
+    }
+  }
+}
+
 // Masked residual quantisation: one thread per 16-element block of [T][K].
 __global__ __launch_bounds__(256) void rac_resq_kernel(
     const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
@@ -390,9 +528,15 @@ extern "C" qd_status rac_select_channels(const void *x, const qd_nvfp4 *xq, int3
                          xq->codes, xq->scales, xq->gscale, T, K, part, g, scores, ramax);
     }
   }
-  if (K <= 16384)
-    hipLaunchKernelGGL(rac_select_kernel<true>, dim3(1), dim3(1024), 0, s, scores, (int)K, Ks,
-                       sel_idx, bitmap);
+  if (K <= 2048)
+    hipLaunchKernelGGL(rac_select_ballot_kernel<4>, dim3(1), dim3(kSelThreads), 0, s, scores,
+                       (int)K, Ks, sel_idx, bitmap);
+  else if (K <= 4096)
+    hipLaunchKernelGGL(rac_select_ballot_kernel<8>, dim3(1), dim3(kSelThreads), 0, s, scores,
+                       (int)K, Ks, sel_idx, bitmap);
+  else if (K <= 16384)
+    hipLaunchKernelGGL(rac_select_ballot_kernel<32>, dim3(1), dim3(kSelThreads), 0, s, scores,
+                       (int)K, Ks, sel_idx, bitmap);
   else
     hipLaunchKernelGGL(rac_select_kernel<false>, dim3(1), dim3(1024), 0, s, scores, (int)K, Ks,
                        sel_idx, bitmap);

@@ -193,6 +193,26 @@ def test_dense_gemm_with_rac():
     assert e_rac < e_plain
 
 
+@pytest.mark.parametrize("K,Ks", [(4096, 128), (4096, 4096), (8192, 200), (20480, 333)])
+def test_select_sizes(K, Ks):
+    """Channel selection and masked residual across the selection kernels'
+    size ranges (sorting network up to 4096 channels, radix select above),
+    including K_s = K and ties from duplicated columns."""
+    rng = np.random.default_rng(K + Ks)
+    T = 6
+    xf = rng.standard_normal((T, K)).astype(np.float32)
+    xf[:, rng.choice(K, size=max(1, K // 100), replace=False)] *= 20.0
+    xf[:, 7] = xf[:, 3]           # equal residual columns: ties broken by index
+    x = bf16_tensor(xf)
+    xb = np_bf16(x)
+    xq, scores, ramax = ops.quantize_act(x.to(DEV), rac=True)
+    act = OR.rac_activation(xb, Ks)
+    assert np.array_equal(scores.cpu().numpy().view(np.uint64), act["scores"])
+    sel, rq, _, _ = ops.select_channels(x.to(DEV), xq, Ks, scores, ramax)
+    assert np.array_equal(sel.cpu().numpy(), act["sel"])
+    assert_nvfp4_equal(rq, act["rq"], "rq")
+
+
 def test_dequantize_modes():
     rng = np.random.default_rng(5)
     w = bf16_tensor(rng.standard_normal((3, 32, 64)) * 0.05)
