@@ -221,13 +221,16 @@ qd_status moe_unpermute_combine(const void *z, const int32_t *inv_row, const flo
 /* ---------------------------------------------------------------------
  * qd_moe_layer_forward -- the whole rollout-side layer in one call: route,
  * quantise X with fused RAC scores, select, W13 GEMM with fused residual
- * and SwiGLU, quantise h, W2 GEMM, combine.  Equivalent to the seven calls
- * above in that order.
+ * and SwiGLU, quantise h, W2 GEMM, combine.  Same results as the seven
+ * calls above in that order (bit for bit); routing and the X chain are
+ * independent, so their kernels share launches here.
  *   x      : bf16 [T][H]; logits: f32 [T][E];
  *   w13    : E groups of [2I][H]; w2: E groups of [H][I];
  *   y      : bf16 [T][H];
  *   ws     : at least qd_moe_layer_workspace(T, H, E, k, I) bytes; the
  *            intermediates live there (see qd_moe_layer_views).
+ * Errors: QD_ERR_SHAPE as the calls above (E <= 1024, k <= 32);
+ * QD_ERR_UNSUPPORTED for Ks > 0 with H > 16384.
  * ------------------------------------------------------------------- */
 size_t    qd_moe_layer_workspace(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I);
 qd_status qd_moe_layer_forward(const void *x, const float *logits, int64_t T, int64_t H,
@@ -239,9 +242,11 @@ qd_status qd_moe_layer_forward(const void *x, const float *logits, int64_t T, in
  * Same as qd_moe_layer_forward, recording HIP events at the stage
  * boundaries: events is a host array of QD_STAGE_COUNT + 1 hipEvent_t (as
  * void*); events[i] is recorded on `stream` before stage i and
- * events[QD_STAGE_COUNT] after the last one (stages in the order below;
- * the select stage records its two events back to back when Ks == 0).
- * events NULL: no recording.
+ * events[QD_STAGE_COUNT] after the last one (stages in the order below).
+ * With the shared launches the first three stages are: ROUTE = routing
+ * top-k with the amax pass over X; QUANT_X = routing ranks with the X
+ * quantiser; SELECT = routing scatter with the channel selection, then the
+ * masked residual (scatter alone when Ks == 0).  events NULL: no recording.
  */
 enum {
   QD_STAGE_ROUTE = 0, QD_STAGE_QUANT_X, QD_STAGE_SELECT, QD_STAGE_W13, QD_STAGE_QUANT_H,

@@ -3,9 +3,79 @@
 // masked residual, W13 grouped GEMM with the fused residual and SwiGLU,
 // quantisation of h, W2 grouped GEMM, weighted combine.  Intermediates are
 // carved from the caller's workspace at the offsets qd_moe_layer_views gives.
-#include "common.h"
+#include "quant_dev.h"
+#include "rac_dev.h"
+#include "route_dev.h"
 
 namespace {
+
+// The steps before the W13 GEMM form two independent chains -- routing
+// (top-k, ranks, scatter) and X (amax, quantise + RAC scores, channel
+// select) -- so each launch below runs one step of each chain side by side
+// in disjoint workgroups: three launches instead of six.
+
+// routing top-k (ntopk workgroups) | amax partials of X (ga workgroups; with
+// RAC they also clear the score and residual-amax accumulators)
+__global__ __launch_bounds__(256) void layer_pre1_kernel(
+    const float *__restrict__ logits, int64_t T, int E, int k, int renorm,
+    int32_t *__restrict__ ids, float *__restrict__ wts, int ntopk, const void *__restrict__ x,
+    int64_t n16, float *__restrict__ part, int ga, uint64_t *__restrict__ scores, int64_t H,
+    float *__restrict__ ramax) {
+  const int b = blockIdx.x;
+  if (b < ntopk) qdr::route_topk_body(b, logits, T, E, k, renorm, ids, wts);
+  else qdq::amax_partial_body<uint16_t>(b - ntopk, ga, x, n16, part, scores, scores ? H : 0, ramax);
+}
+
+// routing ranks (nr workgroups) | X quantiser (+ RAC scores) on a (gx, gy) grid
+template <bool RAC>
+__global__ __launch_bounds__(256) void layer_pre2_kernel(
+    int64_t T, int E, int k, const int32_t *__restrict__ ids, int32_t *__restrict__ counts,
+    int32_t *__restrict__ ranks, int nr, const void *__restrict__ x, int64_t H,
+    const float *__restrict__ part, int np, uint8_t *__restrict__ codes,
+    uint8_t *__restrict__ scales, float *__restrict__ gscale, uint64_t *__restrict__ scores,
+    float *__restrict__ ramax, int gx, int gy) {
+  const int b = blockIdx.x;
+  if (b < nr) {
+    qdr::route_rank_body(b, T, E, k, ids, counts, ranks);
+  } else {
+    const int q = b - nr;
+    qdq::quantize_act_body<uint16_t, RAC>(q % gx, q / gx, gy, x, T, H, part, np, codes, scales,
+                                          gscale, scores, ramax);
+  }
+}
+
+// routing scatter (nr workgroups) | RAC channel selection (one workgroup)
+template <int PER>
+__global__ __launch_bounds__(256) void layer_pre3_kernel(
+    int64_t T, int E, int k, int nr, const int32_t *__restrict__ ids,
+    const int32_t *__restrict__ counts, const int32_t *__restrict__ ranks,
+    int32_t *__restrict__ offsets, int32_t *__restrict__ row_token, int32_t *__restrict__ inv_row,
+    const uint64_t *__restrict__ scores, int K, int Ks, int32_t *__restrict__ sel,
+    uint32_t *__restrict__ bitmap) {
+  const int b = blockIdx.x;
+  if (b < nr)
+    qdr::route_scatter_body(b, T, E, k, nr, ids, counts, ranks, offsets, row_token, inv_row);
+  else
+    qdc::rac_select_body<PER>(scores, K, Ks, sel, bitmap);
+}
+
+__global__ __launch_bounds__(256) void layer_scatter_kernel(
+    int64_t T, int E, int k, int nr, const int32_t *__restrict__ ids,
+    const int32_t *__restrict__ counts, const int32_t *__restrict__ ranks,
+    int32_t *__restrict__ offsets, int32_t *__restrict__ row_token,
+    int32_t *__restrict__ inv_row) {
+  qdr::route_scatter_body(blockIdx.x, T, E, k, nr, ids, counts, ranks, offsets, row_token,
+                          inv_row);
+}
+
+__global__ __launch_bounds__(256) void layer_resq_kernel(
+    const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
+    const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
+    const float *__restrict__ ramax, const uint32_t *__restrict__ bitmap,
+    uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales, float *__restrict__ rgs) {
+  qdc::rac_resq_body(blockIdx.x, gridDim.x, x, xcodes, xscales, xgs, T, K, ramax, bitmap, rcodes,
+                     rscales, rgs);
+}
 
 struct Layout {
   int64_t off[QD_VIEW_COUNT];
@@ -92,6 +162,9 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   if (!w13 || !w2) return QD_ERR_NULL;
   if (T < 0 || H <= 0 || H % 32 || I <= 0 || I % 32 || E < 1 || k < 1 || k > E) return QD_ERR_SHAPE;
   if (Ks < 0 || Ks > H) return QD_ERR_SHAPE;
+  // routing limits (as moe_route_permute) and the fused channel selection
+  if (E > qdr::kMaxE || k > qdr::kMaxK || T * (int64_t)k > 0x7fffffffLL) return QD_ERR_SHAPE;
+  if (Ks > 0 && H > qdc::kSelMaxK) return QD_ERR_UNSUPPORTED;
   qd_status st = qdh::check_nvfp4(w13, E, 2 * I, H);
   if (st) return st;
   st = qdh::check_nvfp4(w2, E, H, I);
@@ -116,11 +189,6 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   int32_t *row_token = (int32_t *)P(QD_VIEW_ROW_TOKEN);
   int32_t *inv_row = (int32_t *)P(QD_VIEW_INV_ROW);
 
-  mark(QD_STAGE_ROUTE);
-  st = moe_route_permute(logits, T, E, k, renorm, ids, wts, offs, row_token, inv_row,
-                         b + L.route_ws, moe_route_permute_workspace(T, E, k), stream);
-  if (st) return st;
-
   qd_nvfp4 xq{(uint8_t *)P(QD_VIEW_XQ_CODES), (uint8_t *)P(QD_VIEW_XQ_SCALES),
               (float *)P(QD_VIEW_XQ_GSCALE), 1, T, H};
   qd_nvfp4 rq{(uint8_t *)P(QD_VIEW_RQ_CODES), (uint8_t *)P(QD_VIEW_RQ_SCALES),
@@ -129,17 +197,59 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   float *ramax = (float *)P(QD_VIEW_RAMAX);
   int32_t *sel = (int32_t *)P(QD_VIEW_SEL);
   const bool rac = Ks > 0;
+  hipStream_t s = qdh::S(stream);
+  // routing scratch, amax partials of X and the channel bitmap (the same
+  // carving the standalone calls use)
+  const int nr = (int)((T + qdr::kTokBlock - 1) / qdr::kTokBlock);
+  int32_t *counts = reinterpret_cast<int32_t *>(b + L.route_ws);
+  int32_t *ranks = reinterpret_cast<int32_t *>(b + L.route_ws +
+                                               qdh::align_up((size_t)nr * E * 4));
+  float *part = reinterpret_cast<float *>(b + L.q1_ws);
+  uint32_t *bitmap = reinterpret_cast<uint32_t *>(b + L.sel_ws);
+  const int ntopk = (int)((T + 3) / 4);
+  const int64_t n16 = T * H / 16;
+  const int ga = qdq::amax_grid(n16);
+  int gx, gy;
+  qdq::quant_grid(T, H, rac, gx, gy);
+
+  mark(QD_STAGE_ROUTE);
+  hipLaunchKernelGGL(layer_pre1_kernel, dim3((unsigned)(ntopk + ga)), dim3(256), 0, s, logits, T,
+                     E, k, renorm, ids, wts, ntopk, x, n16, part, ga, rac ? scores : nullptr, H,
+                     rac ? ramax : nullptr);
   mark(QD_STAGE_QUANT_X);
-  st = nvfp4_quantize_act(x, QD_DTYPE_BF16, T, H, nullptr, 0, &xq, rac ? scores : nullptr,
-                          rac ? ramax : nullptr, b + L.q1_ws,
-                          nvfp4_quantize_act_workspace(T, H), stream);
-  if (st) return st;
+  if (rac)
+    hipLaunchKernelGGL(layer_pre2_kernel<true>, dim3((unsigned)(nr + gx * gy)), dim3(256), 0, s,
+                       T, E, k, ids, counts, ranks, nr, x, H, part, ga, xq.codes, xq.scales,
+                       xq.gscale, scores, ramax, gx, gy);
+  else
+    hipLaunchKernelGGL(layer_pre2_kernel<false>, dim3((unsigned)(nr + gx * gy)), dim3(256), 0, s,
+                       T, E, k, ids, counts, ranks, nr, x, H, part, ga, xq.codes, xq.scales,
+                       xq.gscale, nullptr, nullptr, gx, gy);
   mark(QD_STAGE_SELECT);
   if (rac) {
-    st = rac_select_channels(x, &xq, Ks, scores, ramax, 1, sel, &rq, b + L.sel_ws,
-                             rac_select_channels_workspace(T, H), stream);
-    if (st) return st;
+    const dim3 g3((unsigned)(nr + 1));
+    if (H <= 2048)
+      hipLaunchKernelGGL(layer_pre3_kernel<8>, g3, dim3(256), 0, s, T, E, k, nr, ids, counts,
+                         ranks, offs, row_token, inv_row, scores, (int)H, Ks, sel, bitmap);
+    else if (H <= 4096)
+      hipLaunchKernelGGL(layer_pre3_kernel<16>, g3, dim3(256), 0, s, T, E, k, nr, ids, counts,
+                         ranks, offs, row_token, inv_row, scores, (int)H, Ks, sel, bitmap);
+    else
+      hipLaunchKernelGGL(layer_pre3_kernel<64>, g3, dim3(256), 0, s, T, E, k, nr, ids, counts,
+                         ranks, offs, row_token, inv_row, scores, (int)H, Ks, sel, bitmap);
+    const int64_t total = T * (H / 16);
+    int64_t g = (total + 255) / 256;
+    if (g > 4096) g = 4096;
+    if (g < 1) g = 1;
+    hipLaunchKernelGGL(layer_resq_kernel, dim3((unsigned)g), dim3(256), 0, s,
+                       static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
+                       ramax, bitmap, rq.codes, rq.scales, rq.gscale);
+  } else {
+    hipLaunchKernelGGL(layer_scatter_kernel, dim3((unsigned)nr), dim3(256), 0, s, T, E, k, nr,
+                       ids, counts, ranks, offs, row_token, inv_row);
   }
+  st = qdh::check_launch();
+  if (st) return st;
   uint16_t *h = (uint16_t *)P(QD_VIEW_H);
   float *hamax = (float *)P(QD_VIEW_H_AMAX);
   mark(QD_STAGE_W13);

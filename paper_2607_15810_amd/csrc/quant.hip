@@ -6,141 +6,32 @@
 // (activation QDQ and its residual), Eq. (weight-error-def) and
 // Eq. (w4a16-qat-forward) (weight QDQ shared with the trainer), Eq.
 // (channel-score) (per-channel residual norm, accumulated in the same pass).
-#include "common.h"
+#include "quant_dev.h"
 
 namespace {
 
 using namespace qd;
+using qdq::Loader;
 
-constexpr int kAmaxPartials = 256;      // per-call partial maxima (workspace)
+using qdq::kAmaxPartials;
+using qdq::amax_grid;
 
-template <typename T> struct Loader;
-template <> struct Loader<uint16_t> {   // bf16 storage
-  // 16 consecutive elements starting at element index i (16-aligned)
-  __device__ static void load16(const void *base, int64_t i, float (&x)[16]) {
-    const uint4 *p = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(base) + i);
-    uint4 a = p[0], b = p[1];
-    uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      x[2 * j] = __uint_as_float(w[j] << 16);
-      x[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
-    }
-  }
-};
-template <> struct Loader<float> {
-  __device__ static void load16(const void *base, int64_t i, float (&x)[16]) {
-    const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(base) + i);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float4 v = p[j];
-      x[4 * j] = v.x; x[4 * j + 1] = v.y; x[4 * j + 2] = v.z; x[4 * j + 3] = v.w;
-    }
-  }
-};
-
-// Per-workgroup max|x| over a flat array of n16 16-element blocks; also zeroes
-// the RAC statistics buffers when given (they are accumulated by the next
-// kernel on the same stream).
 template <typename T>
 __global__ __launch_bounds__(256) void amax_partial_kernel(const void *__restrict__ x,
                                                            int64_t n16, float *__restrict__ part,
                                                            uint64_t *__restrict__ zero_u64,
                                                            int64_t n_zero_u64,
                                                            float *__restrict__ zero_f32) {
-  __shared__ float red[16];
-  float m = 0.0f;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < n16; b += stride) {
-    float v[16];
-    Loader<T>::load16(x, b * 16, v);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) m = fmaxf(m, fabsf(v[i]));
-  }
-  if (zero_u64) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_zero_u64; i += stride)
-      zero_u64[i] = 0ull;
-  }
-  if (zero_f32 && blockIdx.x == 0 && threadIdx.x == 0) zero_f32[0] = 0.0f;
-  m = block_max(m, red);
-  if (threadIdx.x == 0) part[blockIdx.x] = m;
+  qdq::amax_partial_body<T>(blockIdx.x, gridDim.x, x, n16, part, zero_u64, n_zero_u64, zero_f32);
 }
 
-// Q_A over [rows][cols].  Thread (tx, ty) of a 16x16 workgroup owns column
-// block (blockIdx.x*16 + tx) and rows ty, ty+16*gridDim.y, ...  With RAC the
-// same pass forms r = x_hat - x and accumulates the fixed-point channel
-// scores (u64, order independent) and max|r|.
 template <typename T, bool RAC>
 __global__ __launch_bounds__(256) void quantize_act_kernel(
     const void *__restrict__ x, int64_t rows, int64_t cols, const float *__restrict__ amax_part,
     int n_part, uint8_t *__restrict__ codes, uint8_t *__restrict__ scales,
     float *__restrict__ gscale, uint64_t *__restrict__ scores, float *__restrict__ ramax) {
-  __shared__ float red[16];
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  // tensor amax from the partial maxima
-  float a = 0.0f;
-  for (int i = threadIdx.x; i < n_part; i += blockDim.x) a = fmaxf(a, amax_part[i]);
-  const float amax = block_max(a, red);
-  float s_enc, s_dec;
-  tensor_scale(amax, s_enc, s_dec);
-  const bool zero_tensor = !(amax >= kZeroAmax);
-  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
-    gscale[0] = s_enc;
-    gscale[1] = s_dec;
-  }
-  const int64_t nbc = cols >> 4;
-  const int64_t cb = (int64_t)blockIdx.x * 16 + tx;
-  const bool active = cb < nbc;
-
-  int F = 0;
-  if (RAC) {
-    int e;
-    frexpf(amax, &e);
-    F = 36 - 2 * e;
-  }
-  uint64_t acc[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) acc[i] = 0ull;
-  float rmax = 0.0f;
-
-  if (active) {
-    for (int64_t r = (int64_t)blockIdx.y * 16 + ty; r < rows; r += (int64_t)gridDim.y * 16) {
-      float v[16];
-      Loader<T>::load16(x, r * cols + cb * 16, v);
-      uint32_t lo, hi;
-      uint32_t sb = quantize_block(v, s_enc, zero_tensor, lo, hi);
-      reinterpret_cast<uint2 *>(codes + r * (cols >> 1))[cb] = make_uint2(lo, hi);
-      scales[r * nbc + cb] = (uint8_t)sb;
-      if (RAC) {
-        const float sbf = e4m3_to_f32(sb);
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          uint32_t c = ((i < 8 ? lo : hi) >> (4 * (i & 7))) & 15u;
-          float xh = dequant_value(c, sbf, s_dec);
-          float rr = xh - v[i];
-          rmax = fmaxf(rmax, fabsf(rr));
-          float sq = rr * rr;
-          double d = ldexp((double)sq, F);
-          acc[i] += (uint64_t)d;       // truncation toward zero; d < 2^37
-        }
-      }
-    }
-  }
-  if (RAC) {
-    // reduce the per-thread sums over ty, then one atomic per channel
-    __shared__ uint64_t part[16][256];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) part[ty][tx * 16 + i] = acc[i];
-    __syncthreads();
-    uint64_t s = 0;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) s += part[j][threadIdx.x];
-    const int64_t ch = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (ch < cols && s != 0ull) atomicAdd((unsigned long long *)&scores[ch], (unsigned long long)s);
-    float m = block_max(rmax, red);
-    if (threadIdx.x == 0 && m > 0.0f)
-      atomicMax(reinterpret_cast<unsigned int *>(ramax), __float_as_uint(m));
-  }
+  qdq::quantize_act_body<T, RAC>(blockIdx.x, blockIdx.y, gridDim.y, x, rows, cols, amax_part,
+                                 n_part, codes, scales, gscale, scores, ramax);
 }
 
 // Weight amax per group: grid (P, G); part[g * P + p].
@@ -227,11 +118,6 @@ __global__ __launch_bounds__(256) void dequantize_kernel(
   }
 }
 
-inline int amax_grid(int64_t n16) {
-  int64_t g = (n16 + 255) / 256;
-  return (int)(g < kAmaxPartials ? (g < 1 ? 1 : g) : kAmaxPartials);
-}
-
 }  // namespace
 
 extern "C" size_t nvfp4_quantize_act_workspace(int64_t rows, int64_t cols) {
@@ -284,13 +170,8 @@ extern "C" qd_status nvfp4_quantize_act(const void *x, int x_dtype, int64_t rows
     ap = amax_partials;
     np = (int)n_partials;
   }
-  const int64_t nbc = cols / 16;
-  const int gx = (int)((nbc + 15) / 16);
-  int64_t gy = (rows + 15) / 16;
-  const int64_t cap = rac ? 256 : 4096;
-  int64_t lim = cap / gx;
-  if (lim < 1) lim = 1;
-  if (gy > lim) gy = lim;
+  int gx, gy;
+  qdq::quant_grid(rows, cols, rac, gx, gy);
   dim3 grid(gx, (unsigned)gy);
   if (x_dtype == QD_DTYPE_BF16) {
     if (rac)

@@ -1,0 +1,257 @@
+// Device bodies of the RAC selection (Eq. (channel-select)) and the masked
+// residual quantisation (Eq. (residual-recon)): launched alone by rac.hip, or
+// fused with the routing work by the layer.
+#pragma once
+#include "common.h"
+
+namespace qdc {
+
+using namespace qd;
+
+__device__ __forceinline__ void load_bf16x16(const uint16_t *p, float (&x)[16]) {
+  const uint4 *q = reinterpret_cast<const uint4 *>(p);
+  uint4 a = q[0], b = q[1];
+  uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    x[2 * j] = __uint_as_float(w[j] << 16);
+    x[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+  }
+}
+
+// residual r = fl(x_hat - x) of one 16-block from its codes and scale
+__device__ __forceinline__ void block_residual(const float (&x)[16], uint2 cw, uint32_t sb,
+                                               float s_dec, float (&r)[16]) {
+  const float sbf = e4m3_to_f32(sb);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    uint32_t c = ((i < 8 ? cw.x : cw.y) >> (4 * (i & 7))) & 15u;
+    r[i] = dequant_value(c, sbf, s_dec) - x[i];
+  }
+}
+
+// Block-wide exclusive scan of one int per thread (1024 threads).
+__device__ int block_exclusive_scan(int v, int *sh /* 1024 + 32 ints */, int &total) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  // inclusive scan inside the wave
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sh[1024 + wid] = x;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    const int nwv = (int)(blockDim.x >> 6);
+    for (int w = 0; w < nwv; ++w) {
+      int c = sh[1024 + w];
+      sh[1024 + w] = run;
+      run += c;
+    }
+    sh[1024 + 16] = run;
+  }
+  __syncthreads();
+  int res = x - v + sh[1024 + wid];
+  total = sh[1024 + 16];
+  __syncthreads();
+  return res;
+}
+
+// Selection for K <= 16384 channels: radix select on 4-bit digits from the
+// highest non-zero digit of the largest score down.  Digit counts come from
+// wave ballots (no atomics: most channels share their leading digits, which
+// would serialise histogram atomics).  Each wave posts its 16 counts, one
+// barrier, and every wave then derives the same digit from the posted
+// counts (double-buffered, so one barrier per digit).  Thread i owns
+// channels i, i + 256, ... in registers.  Channels above the threshold theta
+// are taken, then channels equal to it in ascending order until K_s (a
+// popcount scan over a bitmap of the equal ones); a popcount scan of the
+// selection bitmap emits S in ascending order.
+constexpr int kSelThreads = 256;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kSelMaxK = 16384;
+
+template <int PER>
+__device__ __forceinline__ void rac_select_body(const uint64_t *__restrict__ scores, int K, int Ks,
+                                                int32_t *__restrict__ sel_idx,
+                                                uint32_t *__restrict__ bitmap) {
+  __shared__ int cnt[2][kSelWaves][16];     // [pass parity][wave][digit]
+  __shared__ uint32_t gt[16384 / 32], eq[16384 / 32];
+  __shared__ int sh[1024 + 32];
+  __shared__ uint64_t s_max[kSelWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int nw = (K + 31) / 32;
+  uint64_t sv[PER];
+  bool live[PER];
+  uint64_t mx = 0ull;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int j = tid + kSelThreads * i;
+    live[i] = j < K;
+    sv[i] = live[i] ? scores[j] : 0ull;
+    mx = sv[i] > mx ? sv[i] : mx;
+  }
+  for (int w = tid; w < nw; w += kSelThreads) {
+    gt[w] = 0u;
+    eq[w] = 0u;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t y = __shfl_xor(mx, o, 64);
+    mx = y > mx ? y : mx;
+  }
+  if (lane == 0) s_max[wid] = mx;
+  __syncthreads();
+  mx = 0ull;
+#pragma unroll
+  for (int w = 0; w < kSelWaves; ++w) mx = s_max[w] > mx ? s_max[w] : mx;
+  // theta = the K_s-th largest score; every wave tracks (prefix, remaining)
+  uint64_t pre = 0ull, msk = 0ull;
+  int rem = Ks;
+  if (Ks > 0 && mx != 0ull) {
+    const int top = (63 - __clzll((long long)mx)) >> 2;
+    for (int d = top, par = 0; d >= 0; --d, par ^= 1) {
+      // per-lane digit counts packed as 16-bit fields: digit q lives in
+      // word q >> 2, bits 16 (q & 3) .. +15; summed over the wave's lanes
+      // (at most 64 * PER < 2^16 per digit)
+      uint64_t pk[4] = {0ull, 0ull, 0ull, 0ull};
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const bool m = live[i] && (sv[i] & msk) == pre;
+        const int dig = (int)((sv[i] >> (4 * d)) & 15ull);
+        const uint64_t inc = m ? (1ull << (16 * (dig & 3))) : 0ull;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) pk[q] += (dig >> 2) == q ? inc : 0ull;
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) pk[q] += __shfl_xor(pk[q], o, 64);
+      // lane b < 16: this wave's count of digit b
+      int mine = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if ((lane >> 2) == q) mine = (int)((pk[q] >> (16 * (lane & 3))) & 0xFFFFull);
+      if (lane < 16) cnt[par][wid][lane] = mine;
+      __syncthreads();
+      // lane l < 16 holds digit 15 - l; an inclusive scan over the lanes
+      // counts the candidates at or above each digit
+      const int b = 15 - (lane & 15);
+      int c = 0;
+#pragma unroll
+      for (int w = 0; w < kSelWaves; ++w) c += cnt[par][w][b];
+      c = lane < 16 ? c : 0;
+      int incl = c;
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        const int y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      const uint64_t hit = __ballot(lane < 16 && incl >= rem);
+      const int L = __ffsll((long long)hit) - 1;
+      const int above = __shfl(incl - c, L, 64);
+      pre |= (uint64_t)(15 - L) << (4 * d);
+      rem -= above;
+      msk |= 15ull << (4 * d);
+    }
+  }
+  const uint64_t theta = pre;
+  const int take_eq = Ks > 0 ? rem : 0;    // channels equal to theta to keep
+  if (Ks > 0) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int j = tid + kSelThreads * i;
+      if (live[i]) {
+        if (sv[i] > theta) atomicOr(&gt[j >> 5], 1u << (j & 31));
+        else if (sv[i] == theta) atomicOr(&eq[j >> 5], 1u << (j & 31));
+      }
+    }
+  }
+  __syncthreads();
+  // nw <= 512 words: two per thread (2 tid, 2 tid + 1), scanned as a pair
+  uint32_t e2[2], w2[2];
+  int ce = 0;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int w = 2 * tid + q;
+    e2[q] = w < nw ? eq[w] : 0u;
+    w2[q] = w < nw ? gt[w] : 0u;
+    ce += __popc(e2[q]);
+  }
+  int tot;
+  int eq_before = block_exclusive_scan(ce, sh, tot);
+  int cw = 0;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    int need = take_eq - eq_before;
+    uint32_t m = e2[q];
+    eq_before += __popc(m);
+    while (need > 0 && m) {
+      w2[q] |= m & (0u - m);        // lowest remaining equal channel
+      m &= m - 1u;
+      --need;
+    }
+    cw += __popc(w2[q]);
+  }
+  int pos = block_exclusive_scan(cw, sh, tot);
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int w = 2 * tid + q;
+    if (w < nw) {
+      bitmap[w] = w2[q];
+      uint32_t m = w2[q];
+      while (m) {
+        sel_idx[pos++] = w * 32 + (__ffs(m) - 1);
+        m &= m - 1u;
+      }
+    }
+  }
+}
+
+// Masked residual quantisation: one thread per 16-element block of [T][K];
+// workgroup bid of nblk.
+__device__ __forceinline__ void rac_resq_body(
+    int bid, int nblk, const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
+    const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
+    const float *__restrict__ ramax, const uint32_t *__restrict__ bitmap,
+    uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales, float *__restrict__ rgs) {
+  const float amax_r = ramax[0];
+  float s_enc, s_dec;
+  tensor_scale(amax_r, s_enc, s_dec);
+  const bool zero_tensor = !(amax_r >= kZeroAmax);
+  if (bid == 0 && threadIdx.x == 0) {
+    rgs[0] = s_enc;
+    rgs[1] = s_dec;
+  }
+  const float xs_dec = xgs[1];
+  const int64_t nbc = K >> 4;
+  const int64_t total = T * nbc;
+  const int64_t stride = (int64_t)nblk * blockDim.x;
+  for (int64_t b = (int64_t)bid * blockDim.x + threadIdx.x; b < total; b += stride) {
+    const int64_t cb = b % nbc;
+    const uint32_t m16 = (bitmap[cb >> 1] >> (16 * (cb & 1))) & 0xFFFFu;
+    uint32_t lo = 0u, hi = 0u, sb = 0u;
+    if (m16) {
+      const int64_t t = b / nbc;
+      float v[16], r[16];
+      load_bf16x16(x + t * K + cb * 16, v);
+      uint2 cw = reinterpret_cast<const uint2 *>(xcodes)[b];
+      block_residual(v, cw, xscales[b], xs_dec, r);
+      sb = quantize_block(r, s_enc, zero_tensor, lo, hi);
+      uint32_t mlo = 0u, mhi = 0u;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if ((m16 >> i) & 1u) mlo |= 15u << (4 * i);
+        if ((m16 >> (i + 8)) & 1u) mhi |= 15u << (4 * i);
+      }
+      lo &= mlo;
+      hi &= mhi;
+    }
+    reinterpret_cast<uint2 *>(rcodes)[b] = make_uint2(lo, hi);
+    rscales[b] = (uint8_t)sb;
+  }
+}
+
+}  // namespace qdc

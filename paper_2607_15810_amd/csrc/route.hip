@@ -1,170 +1,32 @@
-// Top-k expert routing and the canonical token -> row permutation of the
-// MoE layer (the paper's MoE rollout layer, Sec. 3.3 / Sec. 4.1; the router
-// itself is not specified there: top-k of the logits with ties to the lower
-// expert index, softmax weights over the selected logits).
-//
-// Three kernels:
-//   route_topk_kernel    one wavefront per token: k rounds of a wave-wide
-//                        arg-max, then the softmax weights.
-//   route_rank_kernel    per block of 256 tokens: expert bitmasks in LDS give
-//                        every (token, slot) its rank among the block's tokens
-//                        of the same expert, and per-block expert counts.
-//   route_scatter_kernel scan of the counts -> expert offsets; row =
-//                        offset[e] + rows of e in earlier blocks + rank.
-// No atomic slot claims: the row order (expert asc, token asc) is a pure
-// function of the routing, so the permutation is bit-reproducible.
-#include "common.h"
+// moe_route_permute: top-k routing and the token -> row permutation of the
+// MoE layer (Sec. 3.3 / Sec. 4.1; readings in route_dev.h), three kernels.
+#include "route_dev.h"
 
 namespace {
 
-constexpr int kTokBlock = 256;
-constexpr int kMaxE = 1024;
-constexpr int kMaxK = 32;
+using qdr::kTokBlock;
+using qdr::kMaxE;
+using qdr::kMaxK;
 
-// (value desc, index asc)
-__device__ __forceinline__ bool better(float v1, int e1, float v2, int e2) {
-  return v1 > v2 || (v1 == v2 && e1 < e2);
+__global__ __launch_bounds__(256) void route_topk_kernel(const float *__restrict__ logits,
+                                                         int64_t T, int E, int k, int renorm,
+                                                         int32_t *__restrict__ ids,
+                                                         float *__restrict__ wts) {
+  qdr::route_topk_body(blockIdx.x, logits, T, E, k, renorm, ids, wts);
 }
-
-// One wavefront per token, four tokens per workgroup.
-__global__ __launch_bounds__(256) void route_topk_kernel(
-    const float *__restrict__ logits, int64_t T, int E, int k, int renorm,
-    int32_t *__restrict__ ids, float *__restrict__ wts) {
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int64_t t = (int64_t)blockIdx.x * 4 + wid;
-  if (t >= T) return;
-  const int per_lane = (E + 63) / 64;
-  float v[16];
-#pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    int e = lane + 64 * j;
-    v[j] = (j < per_lane && e < E) ? logits[t * E + e] : -INFINITY;
-  }
-  uint32_t used = 0u;
-  float top_v = 0.0f, denom = 0.0f, my_v = 0.0f;
-  int my_e = 0;
-  for (int s = 0; s < k; ++s) {
-    // best unused candidate of this lane
-    float bv = -INFINITY;
-    int be = 0x7fffffff;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      int e = lane + 64 * j;
-      if (j < per_lane && e < E && !((used >> j) & 1u) && better(v[j], e, bv, be)) {
-        bv = v[j];
-        be = e;
-      }
-    }
-    // wave-wide arg-max; the order is total, so every lane ends with the winner
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      float ov = __shfl_xor(bv, o, 64);
-      int oe = __shfl_xor(be, o, 64);
-      if (better(ov, oe, bv, be)) {
-        bv = ov;
-        be = oe;
-      }
-    }
-    if ((be & 63) == lane) used |= 1u << (be >> 6);
-    if (s == 0) top_v = bv;
-    if (renorm) denom += expf(bv - top_v);        // slot order 0..k-1
-    if (lane == s) {
-      my_v = bv;
-      my_e = be;
-    }
-  }
-  if (!renorm) {           // full softmax denominator over all E experts
-    float part = 0.0f;
-    for (int j = 0; j < per_lane; ++j) {
-      int e = lane + 64 * j;
-      if (e < E) part += expf(v[j] - top_v);
-    }
-    for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
-    denom = part;
-  }
-  if (lane < k) {
-    ids[t * k + lane] = my_e;
-    wts[t * k + lane] = expf(my_v - top_v) / denom;
-  }
-}
-
-// Per block of 256 tokens: expert bitmasks in LDS give every (token, slot)
-// its rank among the block's tokens routed to the same expert, and the
-// block's per-expert counts.
 __global__ __launch_bounds__(256) void route_rank_kernel(int64_t T, int E, int k,
                                                          const int32_t *__restrict__ ids,
                                                          int32_t *__restrict__ counts,
                                                          int32_t *__restrict__ ranks) {
-  __shared__ uint32_t mask[kMaxE][kTokBlock / 32];
-  const int64_t t0 = (int64_t)blockIdx.x * kTokBlock;
-  for (int i = threadIdx.x; i < E * (kTokBlock / 32); i += blockDim.x) (&mask[0][0])[i] = 0u;
-  __syncthreads();
-  const int tl = threadIdx.x;
-  const int64_t t = t0 + tl;
-  if (t < T) {
-    for (int s = 0; s < k; ++s) atomicOr(&mask[ids[t * k + s]][tl >> 5], 1u << (tl & 31));
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < E; e += blockDim.x) {
-    int c = 0;
-#pragma unroll
-    for (int w = 0; w < kTokBlock / 32; ++w) c += __popc(mask[e][w]);
-    counts[(int64_t)blockIdx.x * E + e] = c;
-  }
-  if (t < T) {
-    for (int s = 0; s < k; ++s) {
-      const int e = ids[t * k + s];
-      int r = 0;
-      for (int w = 0; w < (tl >> 5); ++w) r += __popc(mask[e][w]);
-      r += __popc(mask[e][tl >> 5] & ((1u << (tl & 31)) - 1u));
-      ranks[t * k + s] = r;
-    }
-  }
+  qdr::route_rank_body(blockIdx.x, T, E, k, ids, counts, ranks);
 }
-
 __global__ __launch_bounds__(256) void route_scatter_kernel(
     int64_t T, int E, int k, int nblk, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ counts, const int32_t *__restrict__ ranks,
     int32_t *__restrict__ offsets, int32_t *__restrict__ row_token,
     int32_t *__restrict__ inv_row) {
-  __shared__ int32_t base[kMaxE];
-  __shared__ int32_t total[kMaxE];
-  const int b = blockIdx.x;
-  for (int e = threadIdx.x; e < E; e += blockDim.x) {
-    int tot = 0, pre = 0;
-    for (int bb = 0; bb < nblk; ++bb) {
-      int c = counts[(int64_t)bb * E + e];
-      tot += c;
-      if (bb < b) pre += c;
-    }
-    total[e] = tot;
-    base[e] = pre;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {            // exclusive scan over experts (E <= 1024)
-    int run = 0;
-    for (int e = 0; e < E; ++e) {
-      int c = total[e];
-      total[e] = run;
-      run += c;
-    }
-    if (b == 0) offsets[E] = run;
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < E; e += blockDim.x) {
-    if (b == 0) offsets[e] = total[e];
-    base[e] += total[e];
-  }
-  __syncthreads();
-  const int64_t t = (int64_t)b * kTokBlock + threadIdx.x;
-  if (t < T) {
-    for (int s = 0; s < k; ++s) {
-      const int e = ids[t * k + s];
-      const int row = base[e] + ranks[t * k + s];
-      row_token[row] = (int32_t)t;
-      inv_row[t * k + s] = row;
-    }
-  }
+  qdr::route_scatter_body(blockIdx.x, T, E, k, nblk, ids, counts, ranks, offsets, row_token,
+                          inv_row);
 }
 
 }  // namespace
