@@ -134,6 +134,20 @@ __device__ __forceinline__ f16x8 decode8(uint32_t codes, f16x2 sc) {
   return r;
 }
 
+// The two E4M3 scale bytes 2c, 2c+1 of a scale dword as an f16 pair
+// (value/256 each, as scale_pair_f16): one byte permute and one shift.
+__device__ __forceinline__ f16x2 scale_pair_of(uint32_t sdw, int c) {
+  const uint32_t v = __builtin_amdgcn_perm(0u, sdw, c ? 0x0C030C02u : 0x0C010C00u);
+  return __builtin_bit_cast(f16x2, v << 7);
+}
+// decode8 with the scale taken from the low (hi = false) or high half of a
+// pair; the half is selected by the packed multiply's operand selection
+__device__ __forceinline__ f16x8 decode8_sel(uint32_t codes, f16x2 pair, bool hi) {
+  const f16x2 sc = hi ? __builtin_shufflevector(pair, pair, 1, 1)
+                      : __builtin_shufflevector(pair, pair, 0, 0);
+  return decode8(codes, sc);
+}
+
 __device__ __forceinline__ f16x2 splat_lo(uint32_t pair) {
   uint32_t v = (pair & 0xFFFFu) | (pair << 16);
   return __builtin_bit_cast(f16x2, v);

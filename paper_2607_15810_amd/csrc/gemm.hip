@@ -432,11 +432,6 @@ __device__ __forceinline__ void load_araw(ARaw<MTV> &a, const unsigned char *asl
   }
 }
 
-// f16 pair (value / 256) of E4M3 scale bytes (b >> sh) & 0xFF and the next
-__device__ __forceinline__ uint32_t scale_pair_at(uint32_t b, int sh) {
-  return scale_pair_f16((b >> sh) & 0xFFu, (b >> (sh + 8)) & 0xFFu);
-}
-
 // One stage's MFMA work for MTV valid m-tiles, all operands decoded to f16
 // from registers.  hook(k) runs before k-step k (0..7): the caller issues
 // its loads for later stages there, spread over the stage.
@@ -447,37 +442,29 @@ __device__ __forceinline__ void sk_stage(const BReg &b, const ARaw<MTV> &a, uint
   for (int c2 = 0; c2 < 2; ++c2) {
     const u32x4 bv0 = c2 ? b.c01 : b.c00;
     const u32x4 bv1 = c2 ? b.c11 : b.c10;
-    const uint32_t sp0 = scale_pair_at(b.s0, 16 * c2), sp1 = scale_pair_at(b.s1, 16 * c2);
-    const f16x2 b0lo = splat_lo(sp0), b0hi = splat_hi(sp0);
-    const f16x2 b1lo = splat_lo(sp1), b1hi = splat_hi(sp1);
-    f16x2 alo[MTV], ahi[MTV], rlo[MTV], rhi[MTV];
+    const f16x2 sp0 = scale_pair_of(b.s0, c2), sp1 = scale_pair_of(b.s1, c2);
+    f16x2 ap[MTV], rp[MTV];
     const bool rchunk = RAC && ((sm >> (4 * c2)) & 15u) != 0u;
 #pragma unroll
     for (int i = 0; i < MTV; ++i) {
-      const uint32_t ap = scale_pair_at(a.xs[i], 16 * c2);
-      alo[i] = splat_lo(ap);
-      ahi[i] = splat_hi(ap);
-      if (rchunk) {
-        const uint32_t rp = scale_pair_at(a.rs[i], 16 * c2);
-        rlo[i] = splat_lo(rp);
-        rhi[i] = splat_hi(rp);
-      }
+      ap[i] = scale_pair_of(a.xs[i], c2);
+      if (rchunk) rp[i] = scale_pair_of(a.rs[i], c2);
     }
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       hook(c2 * 4 + s);
-      const f16x8 bf0 = decode8(bv0[s], s < 2 ? b0lo : b0hi);
-      const f16x8 bf1 = decode8(bv1[s], s < 2 ? b1lo : b1hi);
+      const f16x8 bf0 = decode8_sel(bv0[s], sp0, s >= 2);
+      const f16x8 bf1 = decode8_sel(bv1[s], sp1, s >= 2);
 #pragma unroll
       for (int i = 0; i < MTV; ++i) {
-        const f16x8 af = decode8(word_of(a.x[c2][i], s), s < 2 ? alo[i] : ahi[i]);
+        const f16x8 af = decode8_sel(word_of(a.x[c2][i], s), ap[i], s >= 2);
         acc[i][0] = mfma16(af, bf0, acc[i][0]);
         acc[i][1] = mfma16(af, bf1, acc[i][1]);
       }
       if (RAC && ((sm >> (4 * c2 + s)) & 1u)) {
 #pragma unroll
         for (int i = 0; i < MTV; ++i) {
-          const f16x8 rf = decode8(word_of(a.r[c2][i], s), s < 2 ? rlo[i] : rhi[i]);
+          const f16x8 rf = decode8_sel(word_of(a.r[c2][i], s), rp[i], s >= 2);
           accr[i][0] = mfma16(rf, bf0, accr[i][0]);
           accr[i][1] = mfma16(rf, bf1, accr[i][1]);
         }
