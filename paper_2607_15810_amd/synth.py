@@ -26,8 +26,9 @@ give):
                              scale is subnormal or underflows to zero.
 
 Random streams: SeedSequence(2607158100 + index).spawn(6) ->
-(logits, X, outlier channels, W13, W2, edge cases).  Weights are drawn one
-expert at a time in expert order.
+(logits, X, outlier channels, W13, W2, edge cases).  Expert e's weights come
+from the W13 (W2) sequence with spawn key e appended, so a test can draw any
+subset of the experts on its own and leave the rest zero.
 """
 
 from dataclasses import dataclass, field
@@ -92,9 +93,12 @@ def to_bf16(a):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16)
 
 
+def _seeds(index):
+    return np.random.SeedSequence(BASE_SEED + index).spawn(6)
+
+
 def _streams(index):
-    ss = np.random.SeedSequence(BASE_SEED + index).spawn(6)
-    return [np.random.default_rng(s) for s in ss]
+    return [np.random.default_rng(s) for s in _seeds(index)]
 
 
 def make_logits(wl, rng, T=None):
@@ -142,12 +146,19 @@ def make_acts(wl, rng_x, rng_o, rng_edge, T=None, H=None):
     return x
 
 
-def make_bank(rng, E, N, K, std):
-    """[E][N][K] bfloat16 weights, drawn one expert at a time."""
-    out = torch.empty((E, N, K), dtype=torch.bfloat16)
-    for e in range(E):
-        w = rng.standard_normal((N, K), dtype=np.float32) * np.float32(std)
-        out[e] = to_bf16(w)
+def expert_weights(seed_seq, e, N, K, std):
+    """Expert e's [N][K] float32 weights from its own stream (the bank's seed
+    sequence with spawn key e), so any subset of experts can be drawn alone."""
+    ss = np.random.SeedSequence(seed_seq.entropy, spawn_key=tuple(seed_seq.spawn_key) + (e,))
+    return np.random.default_rng(ss).standard_normal((N, K), dtype=np.float32) * np.float32(std)
+
+
+def make_bank(seed_seq, E, N, K, std, experts=None):
+    """[E][N][K] bfloat16 weights.  experts: the experts to draw (default all);
+    the others are zero (full-size tests that check a sample of experts)."""
+    out = torch.zeros((E, N, K), dtype=torch.bfloat16)
+    for e in (range(E) if experts is None else experts):
+        out[e] = to_bf16(expert_weights(seed_seq, int(e), N, K, std))
     return out
 
 
@@ -161,21 +172,23 @@ class Inputs:
     extra: dict = field(default_factory=dict)
 
 
-def generate(name, T=None, with_weights=True):
+def generate(name, T=None, with_weights=True, experts=None):
     """Generate a workload's inputs on the CPU.  T overrides the token count
-    (same distributions, smaller batch) for oracle-sized parity cases."""
+    (same distributions, smaller batch) for oracle-sized parity cases;
+    experts restricts the drawn expert weights (others zero)."""
     wl = WORKLOADS[name]
-    r_logit, r_x, r_o, r_w13, r_w2, r_edge = _streams(wl.index)
+    r_logit, r_x, r_o, _r_w13, _r_w2, r_edge = _streams(wl.index)
+    s_w13, s_w2 = _seeds(wl.index)[3:5]
     T = wl.T if T is None else T
     x = to_bf16(make_acts(wl, r_x, r_o, r_edge, T=T))
     if wl.dense:
-        w = make_bank(r_w13, 1, wl.N, wl.H, wl.w_std) if with_weights else None
+        w = make_bank(s_w13, 1, wl.N, wl.H, wl.w_std) if with_weights else None
         return Inputs(wl, x, w13=w)
     logits = torch.from_numpy(make_logits(wl, r_logit, T=T))
     w13 = w2 = None
     if with_weights:
-        w13 = make_bank(r_w13, wl.E, 2 * wl.I, wl.H, wl.w_std)
-        w2 = make_bank(r_w2, wl.E, wl.H, wl.I, wl.w_std)
+        w13 = make_bank(s_w13, wl.E, 2 * wl.I, wl.H, wl.w_std, experts)
+        w2 = make_bank(s_w2, wl.E, wl.H, wl.I, wl.w_std, experts)
     return Inputs(wl, x, logits=logits, w13=w13, w2=w2)
 
 
@@ -186,9 +199,10 @@ def small_moe(name, T, H, E, k, I, Ks, seed=0, acts="normal", routing="normal",
                   k=k, I=I, Ks=Ks, outlier_frac=outlier_frac,
                   outlier_scale=outlier_scale, routing=routing, acts=acts,
                   edge_cases=edge_cases)
-    r_logit, r_x, r_o, r_w13, r_w2, r_edge = _streams(wl.index)
+    r_logit, r_x, r_o, _r_w13, _r_w2, r_edge = _streams(wl.index)
+    s_w13, s_w2 = _seeds(wl.index)[3:5]
     x = to_bf16(make_acts(wl, r_x, r_o, r_edge))
     logits = torch.from_numpy(make_logits(wl, r_logit))
-    w13 = make_bank(r_w13, E, 2 * I, H, wl.w_std)
-    w2 = make_bank(r_w2, E, H, I, wl.w_std)
+    w13 = make_bank(s_w13, E, 2 * I, H, wl.w_std)
+    w2 = make_bank(s_w2, E, H, I, wl.w_std)
     return Inputs(wl, x, logits=logits, w13=w13, w2=w2)

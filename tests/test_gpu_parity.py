@@ -288,3 +288,127 @@ def test_empty_batch():
     y = lay(x, lg)
     torch.cuda.synchronize()
     assert y.shape == (0, 128)
+
+
+FULL = ["moe_decode_t256_h2048", "moe_prefill_t8192_h2048", "moe_zipf_decode_t64_h4096",
+        "moe_prefill_t4096_h4096"]
+
+
+def _sampled_experts(counts):
+    """The most and least loaded non-empty experts and one in between."""
+    nz = np.nonzero(counts)[0]
+    order = nz[np.argsort(counts[nz], kind="stable")]
+    return sorted({int(order[-1]), int(order[0]), int(order[len(order) // 2])})
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_sampled(name):
+    """A MoE workload at its full size through the whole-layer call the
+    benchmark times (same shapes, hence the same kernels and grids).
+
+    Three experts carry their real weights; the rest are zero.  The kernels do
+    the same work either way, and the zero experts make every output
+    computable by the oracle: their rows of h and z and their shares of y are
+    exactly zero, so h's tensor amax comes from the sampled rows alone.
+    Routing, the activation quantisation and the channel selection are
+    compared in full, bit for bit."""
+    wl = synth.WORKLOADS[name]
+    lg = synth.generate(name, with_weights=False).logits.numpy()
+    ref_ids = ORt.topk_fast(lg, wl.k)
+    perm = ORt.permute(ref_ids, wl.E)
+    offs_np = perm["offsets"]
+    S = _sampled_experts(np.diff(offs_np))
+    zero_e = next(e for e in range(wl.E) if e not in S)
+    inp = synth.generate(name, experts=S)
+    T, H, E, k, I, Ks = wl.T, wl.H, wl.E, wl.k, wl.I, wl.Ks
+    R = T * k
+    print(f"{name}: experts {S}, rows {[int(offs_np[e + 1] - offs_np[e]) for e in S]}", flush=True)
+
+    x = inp.x.to(DEV)
+    logits = inp.logits.to(DEV)
+    w13 = ops.quantize_weight(inp.w13.to(DEV))
+    w2 = ops.quantize_weight(inp.w2.to(DEV))
+    lay = ops.MoELayer(w13, w2, T, k, Ks)
+    y = lay(x, logits)
+    torch.cuda.synchronize()
+    v = lay.views()
+
+    W13 = oracle_bank(inp.w13, S + [zero_e])
+    W2 = oracle_bank(inp.w2, S + [zero_e])
+    assert_bank_equal(w13, W13, S + [zero_e])
+    assert_bank_equal(w2, W2, S + [zero_e])
+    # A1-A2
+    assert np.array_equal(v["ids"].cpu().numpy(), ref_ids)
+    assert np.array_equal(v["offsets"].cpu().numpy(), offs_np)
+    assert np.array_equal(v["row_token"].cpu().numpy(), perm["row_token"])
+    assert np.array_equal(v["inv_row"].cpu().numpy(), perm["inv_row"])
+    ref_w = ORt.weights(lg, ref_ids, True)
+    np.testing.assert_allclose(v["w"].cpu().numpy(), ref_w, rtol=2e-6, atol=1e-7)
+    # A3-A5 in full
+    act = OR.rac_activation(np_bf16(inp.x), Ks)
+    assert_nvfp4_equal(dict(packed=v["xq_codes"].cpu().numpy(), scales=v["xq_scales"].cpu().numpy(),
+                            gscale=v["xq_gscale"].cpu().numpy()), act["xq"], "xq")
+    assert np.array_equal(v["scores"].cpu().numpy().view(np.uint64), act["scores"])
+    assert v["ramax"].item() == np.max(np.abs(act["r"]))
+    assert np.array_equal(v["sel"].cpu().numpy(), act["sel"])
+    assert_nvfp4_equal(dict(packed=v["rq_codes"].cpu().numpy(), scales=v["rq_scales"].cpu().numpy(),
+                            gscale=v["rq_gscale"].cpu().numpy()), act["rq"], "rq")
+
+    # A6 on the sampled rows; every other row of h is exactly zero
+    rows = np.concatenate([np.arange(offs_np[e], offs_np[e + 1]) for e in S])
+    other = np.ones(R, bool)
+    other[rows] = False
+    gu, mag_gu = OL.w13_stage(act["xq"], act["rq"] if Ks else None, perm["row_token"], offs_np,
+                              W13, rows=rows)
+    h_or = OL.swiglu(gu, I)
+    mag_h = (np.abs(OL.silu(gu[:, :I])) * mag_gu[:, I:] +
+             1.1 * np.abs(gu[:, I:]) * mag_gu[:, :I])
+    h_gpu = v["h"]
+    check_close_bf16(np_bf16(h_gpu[torch.from_numpy(rows).to(DEV)]), h_or, mag_h, "h (SwiGLU)")
+    assert h_gpu[torch.from_numpy(other).to(DEV)].abs().max().item() == 0.0
+
+    # A7 on the oracle's h (zero outside the sampled rows), bit-exact; a
+    # zero row appended to the oracle's input gives the expected zero rows
+    hq_or = OQ.quantize(np.vstack([h_or, np.zeros((1, I))]).astype(np.float32))
+    h_full = torch.zeros((R, I), dtype=torch.bfloat16, device=DEV)
+    rows_dev = torch.from_numpy(rows).to(DEV)
+    h_full[rows_dev] = bf16_tensor(h_or)
+    hq, _, _ = ops.quantize_act(h_full)
+    hq_c, hq_s = hq.codes[0], hq.scales[0]
+    assert np.array_equal(hq_c[rows_dev].cpu().numpy(), hq_or["packed"][:-1])
+    assert np.array_equal(hq_s[rows_dev].cpu().numpy(), hq_or["scales"][:-1])
+    od = torch.from_numpy(other).to(DEV)
+    assert bool((hq_c[od] == torch.from_numpy(hq_or["packed"][-1]).to(DEV)).all())
+    assert bool((hq_s[od] == torch.from_numpy(hq_or["scales"][-1]).to(DEV)).all())
+    assert hq.gscale[0].cpu().numpy().view(np.uint32).tolist() == \
+        np.array([hq_or["s_enc"], hq_or["s_dec"]], np.float32).view(np.uint32).tolist()
+
+    # A8 on that hq: the oracle's rows, compacted (row_token maps a row to
+    # its place among the sampled rows)
+    z, _ = ops.grouped_gemm(hq, w2, R, None, v["offsets"])
+    hh = OQ.dequantize_f64(hq_or["codes"][:-1], hq_or["scales"][:-1], hq_or["s_dec"])
+    place = np.zeros(R, np.int64)
+    place[rows] = np.arange(rows.size)
+    z_or, mag_z = OL.grouped_gemm(hh, place, offs_np, W2, rows=rows)
+    check_close_bf16(np_bf16(z[rows_dev]), z_or, mag_z, "z")
+    assert z[od].abs().max().item() == 0.0
+
+    # A9 on the oracle's z (zero row appended for the zero experts' rows)
+    from oracle.formats import bf16_round_f64
+    zb = np.vstack([bf16_round_f64(z_or), np.zeros((1, H))])
+    place[other] = rows.size
+    w32 = ref_w.astype(np.float32)
+    z_full = torch.zeros((R, H), dtype=torch.bfloat16, device=DEV)
+    z_full[rows_dev] = bf16_tensor(zb[:-1])
+    y_st = ops.unpermute_combine(z_full, v["inv_row"], torch.from_numpy(w32).to(DEV))
+    inv_c = place[perm["inv_row"]]
+    y_or, mag_y = OL.combine(zb, inv_c, w32)
+    check_close_bf16(np_bf16(y_st), y_or, mag_y, "y")
+
+    # free-running: the layer's own y against the oracle's chain
+    yb = bf16_round_f64(y_or)
+    yg = np_bf16(y)
+    rel = np.linalg.norm(yg - yb) / max(np.linalg.norm(yb), 1e-30)
+    assert rel <= 1e-3, f"free-running rel-L2 {rel:.3e}"
+    untouched = ~np.isin(perm["inv_row"], rows).any(axis=1)
+    assert np.all(yg[untouched] == 0.0)
