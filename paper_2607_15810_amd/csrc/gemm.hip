@@ -341,6 +341,15 @@ __device__ __forceinline__ void dma4(const void *g, uint32_t lds_addr) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
                :: "v"(g), "s"(lds_addr) : "memory", "m0");
 }
+// the same with a uniform 64-bit base in SGPRs and a 32-bit per-lane offset
+__device__ __forceinline__ void dma16s(const void *base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(voff), "s"(base), "s"(lds_addr) : "memory", "m0");
+}
+__device__ __forceinline__ void dma4s(const void *base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :: "v"(voff), "s"(base), "s"(lds_addr) : "memory", "m0");
+}
 template <int N>
 __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
@@ -349,6 +358,12 @@ __device__ __forceinline__ void wait_lds() {
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 __device__ __forceinline__ uint32_t uni(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+template <typename T>
+__device__ __forceinline__ const T *uni_ptr(const T *p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint64_t r = ((uint64_t)uni((uint32_t)(v >> 32)) << 32) | uni((uint32_t)v);
+  return reinterpret_cast<const T *>((uintptr_t)r);
+}
 
 // Position in a workgroup's stage sequence: unit u = (expert e, pass p,
 // block nb), iteration it over K.  All fields are workgroup-uniform.
@@ -750,6 +765,312 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
   if (p.amax_part && tid == 0) p.amax_part[P] = m;
 }
 
+// ---------------------------------------------------------------------------
+// Prefill-shaped grouped GEMM (hundreds of rows per expert): MFMA-bound.
+//
+//  * Workgroup tile 256 rows x 128 weight rows (SwiGLU: 64 gate rows and
+//    the matching 64 up rows); four waves in a 2 x 2 grid, each 128 x 64 on
+//    v_mfma_f32_32x32x16_f16 (4 x 2 fragments, 128 accumulators), two
+//    workgroups per CU.  Two waves share each SIMD, so one wave's decode
+//    VALU work runs under the other's MFMAs, and one workgroup's prologue
+//    and epilogue under the other's main loop.  A tile of at most 128 rows
+//    (an expert's remainder) splits its rows 64 / 64 between the wave rows
+//    instead, and fragments wholly past the expert's last row are skipped.
+//  * Operand codes are decoded to f16 in registers right before use.
+//  * M-tiles never straddle experts.  The grid is an upper bound on the
+//    tile count; every workgroup derives the real tiles from the expert
+//    offsets, and tile indices run contiguously within an XCD (workgroups
+//    are dealt to the eight XCDs in turn), so the tiles in flight on an
+//    XCD share an expert's weights or a block of activation rows in its L2.
+//  * K goes through a ring of TL_NS LDS slots of 64-element stages filled
+//    by direct global->LDS loads (five per wave and stage) TL_NS - 1 stages
+//    ahead.  A wave reads a stage's raw codes and scales into registers one
+//    stage before it multiplies them: halfway through stage s it waits for
+//    stage s + 1, meets the other waves at a barrier, issues the loads of
+//    stage s + TL_NS - 1 into the slot of stage s - 1 (read during stage
+//    s - 2) and reads stage s + 1 while the MFMAs of stage s drain.
+//
+// Stage slot: A codes [8 fragments][64 lanes][16 B], B codes [4 fragments]
+// likewise, then A scale dwords [256 rows] and B scale dwords [128 rows].
+// Lane l of a fragment holds row l % 32, elements 32 (l / 32) .. +31 of the
+// stage; MFMA k-step s (0..3) takes elements 8s .. 8s+7 of each half, for A
+// and B alike.
+constexpr int TL_THREADS = 256;
+constexpr int TL_M = 256;
+constexpr int TL_N = 128;
+constexpr int TL_K = 64;
+constexpr int TL_NS = 4;
+constexpr int TL_ACODE = 0;
+constexpr int TL_BCODE = 8192;
+constexpr int TL_ASCL = 12288;
+constexpr int TL_BSCL = 13312;
+constexpr int TL_STAGE = 13824;
+constexpr int TL_LDS = TL_NS * TL_STAGE;
+constexpr int TL_EMAX = 1024;            // experts handled by the tile scan (4 per thread)
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ f32x16 mfma32(f16x8 a, f16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+// the tile's weight row tb (0..127): for SwiGLU, fragments (32 rows) 0, 1
+// are gate rows and 2, 3 the matching up rows
+template <int EPI>
+__device__ __forceinline__ int tile_wrow(int tb, int nt, int N) {
+  if (EPI == QD_EPI_SWIGLU) {
+    const int f = tb >> 5, r = tb & 31;
+    return (f < 2 ? 0 : (N >> 1)) + nt * 64 + (f & 1) * 32 + r;
+  }
+  return nt * TL_N + tb;
+}
+
+// a wave's raw operands of one stage: A fragments fa0 .. fa0 + 3 and B
+// fragments fb0, fb0 + fbs
+struct TlRaw {
+  uint4 a[4], b[2];
+  uint32_t as[4], bs[2];
+};
+
+template <int MTV>
+__device__ __forceinline__ void tl_read(TlRaw &R, const unsigned char *sl, int fa0, int fb0,
+                                        int fbs, int lane) {
+  const int r = lane & 31;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int fb = fb0 + j * fbs;
+    R.b[j] = *reinterpret_cast<const uint4 *>(sl + TL_BCODE + (fb * 64 + lane) * 16);
+    R.bs[j] = *reinterpret_cast<const uint32_t *>(sl + TL_BSCL + (fb * 32 + r) * 4);
+  }
+#pragma unroll
+  for (int i = 0; i < MTV; ++i) {
+    const int fa = fa0 + i;
+    R.a[i] = *reinterpret_cast<const uint4 *>(sl + TL_ACODE + (fa * 64 + lane) * 16);
+    R.as[i] = *reinterpret_cast<const uint32_t *>(sl + TL_ASCL + (fa * 32 + r) * 4);
+  }
+}
+
+// One stage of MFMA work on MTV A fragments and two B fragments; mid() runs
+// between k-steps 1 and 2.
+template <int MTV, typename Mid>
+__device__ __forceinline__ void tl_stage(const TlRaw &R, f32x16 (&acc)[4][2], int lane, Mid &&mid) {
+  const int h = lane >> 5;
+  f16x2 ap[MTV], bp[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) bp[j] = scale_pair_of(R.bs[j], h);
+#pragma unroll
+  for (int i = 0; i < MTV; ++i) ap[i] = scale_pair_of(R.as[i], h);
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    if (s == 2) mid();
+    f16x8 bf[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) bf[j] = decode8_sel(word_of(R.b[j], s), bp[j], s >= 2);
+#pragma unroll
+    for (int i = 0; i < MTV; ++i) {
+      const f16x8 af = decode8_sel(word_of(R.a[i], s), ap[i], s >= 2);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(af, bf[j], acc[i][j]);
+    }
+  }
+}
+
+// silu(g) * u from f32 g and u: exp on the transcendental unit and one
+// reciprocal (a few f32 ulp, far inside the bf16 rounding that follows)
+__device__ __forceinline__ float swiglu_fast(float g, float u) {
+  const float e = __builtin_amdgcn_exp2f(-g * 1.4426950408889634f);
+  return g * __builtin_amdgcn_rcpf(1.0f + e) * u;
+}
+
+template <bool GATHER, int EPI>
+__global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, int ntn) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  __shared__ int sh_w[4];
+  __shared__ int sh_t[4];
+  __shared__ float red[16];
+  const int tid = threadIdx.x, lane = tid & 63, w = (int)uni((uint32_t)tid >> 6);
+  const int K = p.K, N = p.N, E = p.E;
+  const int64_t kb2 = K >> 1, kb16 = K >> 4;
+
+  // ---- M-tiles per expert (exclusive scan, four experts per thread)
+  int cnt[4], tsum = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * tid + q;
+    int c = 0;
+    if (p.offsets) c = e < E ? p.offsets[e + 1] - p.offsets[e] : 0;
+    else c = e == 0 ? (int)p.rows : 0;
+    cnt[q] = (max(c, 0) + TL_M - 1) / TL_M;
+    tsum += cnt[q];
+  }
+  int xs = tsum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(xs, o, 64);
+    if (lane >= o) xs += y;
+  }
+  if (lane == 63) sh_w[w] = xs;
+  if (tid == 0) sh_t[0] = -1;
+  __syncthreads();
+  const int mt_total = sh_w[0] + sh_w[1] + sh_w[2] + sh_w[3];
+  // this workgroup's tile: XCD x = b % 8 takes tiles x * per .. x * per + per - 1
+  const int b = blockIdx.x;
+  const int ntile = mt_total * ntn;
+  const int per = (ntile + 7) >> 3;
+  const int slot = b >> 3;
+  const int L = (b & 7) * per + slot;
+  const bool live = slot < per && L < ntile;
+  const int mt = live ? L / ntn : -1, nt = live ? L - (L / ntn) * ntn : 0;
+  {
+    int base = xs - tsum;
+    for (int ww = 0; ww < w; ++ww) base += sh_w[ww];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (mt >= base && mt < base + cnt[q]) {
+        const int e = 4 * tid + q;
+        const int o0 = p.offsets ? p.offsets[e] : 0;
+        const int o1 = p.offsets ? p.offsets[e + 1] : (int)p.rows;
+        const int r0 = o0 + (mt - base) * TL_M;
+        sh_t[0] = e;
+        sh_t[1] = r0;
+        sh_t[2] = min(TL_M, o1 - r0);
+      }
+      base += cnt[q];
+    }
+  }
+  __syncthreads();
+  const int e = (int)uni((uint32_t)sh_t[0]);
+  float vmax = 0.0f;
+  if (e >= 0) {
+    const int row0 = (int)uni((uint32_t)sh_t[1]);
+    const int nrows = (int)uni((uint32_t)sh_t[2]);
+    const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
+    // ---- per-lane load offsets from uniform bases (rows past the tile
+    // repeat its first row; one operand of one expert < 4 GiB)
+    auto arow = [&](int r) __attribute__((always_inline)) -> uint32_t {
+      const int rr = r < nrows ? r : 0;
+      return GATHER ? (uint32_t)p.row_token[row0 + rr] : (uint32_t)(row0 + rr);
+    };
+    const uint32_t hb = 16u * (uint32_t)(lane >> 5);
+    const uint32_t oa0 = arow(64 * w + (lane & 31)) * (uint32_t)kb2 + hb;
+    const uint32_t oa1 = arow(64 * w + 32 + (lane & 31)) * (uint32_t)kb2 + hb;
+    const uint32_t ob = (uint32_t)tile_wrow<EPI>(32 * w + (lane & 31), nt, N) * (uint32_t)kb2 + hb;
+    const uint32_t oas = arow(64 * w + lane) * (uint32_t)kb16;
+    const uint32_t obs = (uint32_t)tile_wrow<EPI>(64 * (w & 1) + lane, nt, N) * (uint32_t)kb16;
+    const uint8_t *wc = uni_ptr(p.w_codes + (int64_t)e * N * kb2);
+    const uint8_t *ws = uni_ptr(p.w_scales + (int64_t)e * N * kb16);
+    const int nst = K / TL_K;
+    // five loads per wave and stage (waves 0 / 2 and 1 / 3 load the same B
+    // scale half: equal bytes to equal places)
+    auto issue = [&](int s, int q) __attribute__((always_inline)) {
+      s = min(s, nst - 1);
+      const uint32_t sb = uni(lds0 + q * TL_STAGE);
+      const uint8_t *ac = uni_ptr(p.a_codes + s * 32), *as_ = uni_ptr(p.a_scales + s * 4);
+      const uint8_t *bc = uni_ptr(wc + s * 32), *bs_ = uni_ptr(ws + s * 4);
+      dma16s(ac, oa0, sb + TL_ACODE + (2 * w) * 1024);
+      dma16s(ac, oa1, sb + TL_ACODE + (2 * w + 1) * 1024);
+      dma16s(bc, ob, sb + TL_BCODE + w * 1024);
+      dma4s(as_, oas, sb + TL_ASCL + w * 256);
+      dma4s(bs_, obs, sb + TL_BSCL + (w & 1) * 256);
+    };
+    const float alpha = p.a_gs[1] * p.w_gs[2 * e + 1];
+    const int wm = w & 1, wn = w >> 1;
+    const bool wide = nrows > 128;
+    const int fa0 = wide ? 4 * wm : 2 * wm;
+    const int mtv = wide ? min(max((nrows - 128 * wm + 31) >> 5, 0), 4)
+                         : min(max((nrows - 64 * wm + 31) >> 5, 0), 2);
+    const int fb0 = EPI == QD_EPI_SWIGLU ? wn : 2 * wn;
+    const int fbs = EPI == QD_EPI_SWIGLU ? 2 : 1;
+
+    // one straight-line loop per number of valid fragments
+    auto run = [&](auto mtv_c) __attribute__((always_inline)) {
+      constexpr int MTV = decltype(mtv_c)::value;
+      f32x16 acc[4][2];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int t = 0; t < 16; ++t) acc[i][j][t] = 0.0f;
+      TlRaw R0, R1;
+#pragma unroll
+      for (int t = 0; t < TL_NS - 1; ++t) issue(t, t);
+      wait_vm<(TL_NS - 2) * 5>();
+      __syncthreads();
+      if constexpr (MTV > 0) tl_read<MTV>(R0, lds, fa0, fb0, fbs, lane);
+      auto body = [&](const TlRaw &Rc, TlRaw &Rn, int s) __attribute__((always_inline)) {
+        auto mid = [&]() __attribute__((always_inline)) {
+          wait_vm<(TL_NS - 3) * 5>();
+          __syncthreads();
+          issue(s + TL_NS - 1, (s + TL_NS - 1) % TL_NS);
+          if constexpr (MTV > 0)
+            tl_read<MTV>(Rn, lds + ((s + 1) % TL_NS) * TL_STAGE, fa0, fb0, fbs, lane);
+        };
+        if constexpr (MTV > 0) tl_stage<MTV>(Rc, acc, lane, mid);
+        else mid();
+      };
+      for (int s = 0; s < nst; s += 2) {     // nst is even
+        body(R0, R1, s);
+        body(R1, R0, s + 1);
+      }
+      wait_vm<0>();
+      // ---- epilogue: tensor scales, SwiGLU or plain, bf16 pairs of
+      // adjacent columns swapped between neighbouring lanes so that every
+      // store writes 4 bytes
+      const int h = lane >> 5;
+      const bool odd = (lane & 1) != 0;
+      const int cpair = (lane & 31) & ~1;
+      constexpr int NO = EPI == QD_EPI_SWIGLU ? 1 : 2;
+      const int ldo = EPI == QD_EPI_SWIGLU ? (N >> 1) : N;
+      const bool full = nrows == TL_M;
+      unsigned char *obase = reinterpret_cast<unsigned char *>(p.out);
+#pragma unroll
+      for (int i = 0; i < MTV; ++i) {
+        const int rl = 32 * (fa0 + i) + 4 * h + (odd ? 1 : 0);
+#pragma unroll
+        for (int jj = 0; jj < NO; ++jj) {
+          const int fb = fb0 + jj * fbs;
+          const int cb = EPI == QD_EPI_SWIGLU ? nt * 64 + (fb & 1) * 32 : nt * TL_N + 32 * fb;
+          const uint32_t voff = (uint32_t)((row0 + rl) * ldo + cb + cpair) * 2u;
+          float v[16];
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            if (EPI == QD_EPI_SWIGLU)
+              v[q] = swiglu_fast(alpha * acc[i][0][q], alpha * acc[i][1][q]);
+            else
+              v[q] = alpha * acc[i][jj][q];
+          }
+#pragma unroll
+          for (int q = 0; q < 16; q += 2) {
+            const float send = odd ? v[q] : v[q + 1];
+            const float x = __int_as_float(
+                __builtin_amdgcn_mov_dpp(__float_as_int(send), 0xB1, 0xF, 0xF, false));
+            const f32x2_t pr = odd ? f32x2_t{x, v[q + 1]} : f32x2_t{v[q], x};
+            const uint32_t pk = __builtin_bit_cast(uint32_t, __builtin_convertvector(pr, bf16x2_t));
+            const int qr = 8 * (q >> 2) + (q & 3);
+            if (full || rl + qr < nrows) {
+              *reinterpret_cast<uint32_t *>(obase + (size_t)(qr * ldo * 2) + voff) = pk;
+              vmax = fmaxf(vmax, fmaxf(fabsf(__uint_as_float(pk << 16)),
+                                       fabsf(__uint_as_float(pk & 0xFFFF0000u))));
+            }
+          }
+        }
+      }
+    };
+    switch (mtv) {
+      case 4: run(std::integral_constant<int, 4>{}); break;
+      case 3: run(std::integral_constant<int, 3>{}); break;
+      case 2: run(std::integral_constant<int, 2>{}); break;
+      case 1: run(std::integral_constant<int, 1>{}); break;
+      default: run(std::integral_constant<int, 0>{}); break;
+    }
+  }
+  const float m = block_max(vmax, red);
+  if (p.amax_part && tid == 0) p.amax_part[blockIdx.x] = m;
+}
+
 // host-side plan of the decode kernel
 struct SkPlan {
   bool ok;
@@ -795,11 +1116,49 @@ void launch_skinny(const GemmArgs &p, const SkPlan &pl, hipStream_t s) {
   hipLaunchKernelGGL(kern, dim3((unsigned)pl.grid), dim3(SK_THREADS), pl.lds, s, p, pl.nblk);
 }
 
+// host-side plan of the prefill kernel
+struct TlPlan {
+  bool ok;
+  int ntn, grid;
+};
+
+inline TlPlan tile_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac) {
+  TlPlan pl{};
+  if (rac || K < 4 * TL_K || K % (2 * TL_K) != 0 || N % TL_N != 0 || E > TL_EMAX) return pl;
+  // byte offsets inside one activation matrix or one expert's weights, and
+  // output offsets, fit 32 bits
+  if (N * K / 2 >= (1LL << 32) || (rows + 1) * K / 2 >= (1LL << 32)) return pl;
+  if ((rows + TL_M) * N * 2 >= (1LL << 32)) return pl;
+  pl.ntn = (int)(N / TL_N);
+  int64_t g = ((rows + TL_M - 1) / TL_M + E) * pl.ntn;
+  g = (g + 7) / 8 * 8;
+  if (g > 0x7fffffffLL) return pl;
+  pl.grid = (int)g;
+  pl.ok = true;
+  return pl;
+}
+
+template <bool GATHER, int EPI>
+void launch_tile(const GemmArgs &p, const TlPlan &pl, hipStream_t s) {
+  auto kern = gemm_tile_kernel<GATHER, EPI>;
+  static const bool attr = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               TL_LDS) == hipSuccess;
+  (void)attr;
+  hipLaunchKernelGGL(kern, dim3((unsigned)pl.grid), dim3(TL_THREADS), TL_LDS, s, p, pl.ntn);
+}
+
 template <bool GATHER, bool RAC>
-void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, const SkPlan &pl) {
+void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, const SkPlan &pl,
+                const TlPlan &tp) {
   if (pl.ok) {
     if (epi == QD_EPI_SWIGLU) launch_skinny<GATHER, RAC, QD_EPI_SWIGLU>(p, pl, s);
     else launch_skinny<GATHER, RAC, QD_EPI_NONE>(p, pl, s);
+    return;
+  }
+  if (!RAC && tp.ok) {
+    if (epi == QD_EPI_SWIGLU) launch_tile<GATHER, QD_EPI_SWIGLU>(p, tp, s);
+    else launch_tile<GATHER, QD_EPI_NONE>(p, tp, s);
     return;
   }
   if (epi == QD_EPI_SWIGLU)
@@ -815,6 +1174,8 @@ extern "C" int64_t moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int
   if (rows < 0 || N <= 0 || K <= 0 || E < 1 || Ks < 0) return 0;
   const SkPlan pl = skinny_plan(rows, E, N, K, Ks, epilogue);
   if (pl.ok) return pl.grid;
+  const TlPlan tp = tile_plan(rows, E, N, K, Ks > 0);
+  if (tp.ok) return tp.grid;
   return grid_x(rows, E, true) * grid_y(N, epilogue);
 }
 
@@ -876,14 +1237,15 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
   p.out = static_cast<uint16_t *>(out);
   p.amax_part = amax_partials;
   const SkPlan pl = skinny_plan(rows, E, N, K, rac ? Ks : 0, epilogue);
+  const TlPlan tp = tile_plan(rows, E, N, K, rac);
   dim3 grid((unsigned)gx, (unsigned)gy);
   hipStream_t s = qdh::S(stream);
   if (row_token) {
-    if (rac) launch_epi<true, true>(p, epilogue, grid, s, pl);
-    else launch_epi<true, false>(p, epilogue, grid, s, pl);
+    if (rac) launch_epi<true, true>(p, epilogue, grid, s, pl, tp);
+    else launch_epi<true, false>(p, epilogue, grid, s, pl, tp);
   } else {
-    if (rac) launch_epi<false, true>(p, epilogue, grid, s, pl);
-    else launch_epi<false, false>(p, epilogue, grid, s, pl);
+    if (rac) launch_epi<false, true>(p, epilogue, grid, s, pl, tp);
+    else launch_epi<false, false>(p, epilogue, grid, s, pl, tp);
   }
   return qdh::check_launch();
 }

@@ -51,6 +51,10 @@ SMALL = [
     ("skinny_w2", 64, 256, 8, 2, 256, 8, {}),
     ("skinny_passes_zipf", 160, 256, 8, 2, 256, 8, dict(routing="zipf")),
     ("skinny_multitile", 64, 1024, 128, 4, 512, 16, {}),
+    # many rows per expert and weight rows a multiple of 256: the 256 x 256
+    # tile kernel (several n-tiles, partial m-tiles, skewed routing)
+    ("tile", 256, 256, 4, 2, 128, 0, {}),
+    ("tile_ragged_zipf", 300, 512, 8, 2, 256, 0, dict(routing="zipf")),
     # many rows per expert: the tiled (prefill) kernel instead of the skinny one
     ("many_rows", 256, 256, 4, 2, 64, 8, {}),
     ("many_rows_ktail", 300, 384, 4, 2, 96, 12, {}),
