@@ -165,6 +165,20 @@ qd_status rac_select_channels(const void *x, const qd_nvfp4 *xq, int32_t Ks,
                               void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------
+ * rac_gather_selected -- the masked residual restricted to the selected
+ * channels S, compacted per row: the operand r_S of the residual term
+ * W[:, S] r_S of Eq. (residual-recon) without its tensor scale,
+ *   out[t][j] = e2m1(code of rq[t][sel_idx[j]]) * e4m3(its block scale)
+ * for j < Ks (exact in f16), and 0 for Ks <= j < rac_selected_width(Ks).
+ *   rq, sel_idx, Ks : from rac_select_channels.
+ *   out             : f16 [rq->rows][rac_selected_width(Ks)], 16-byte aligned.
+ * moe_w4a4_grouped_gemm takes it as rq_sel.
+ * ------------------------------------------------------------------- */
+int32_t   rac_selected_width(int32_t Ks);
+qd_status rac_gather_selected(const qd_nvfp4 *rq, const int32_t *sel_idx, int32_t Ks,
+                              void *out, void *stream);
+
+/* ---------------------------------------------------------------------
  * rac_residual_gemm -- the residual contraction of Eq. (residual-recon)
  * pushed through the linear layer:
  *   out[r][n] = s_dec_r * s_dec_w[e] * sum_{j in S} rhat[src(r)][j] * what[e][n][j]
@@ -192,7 +206,13 @@ qd_status rac_residual_gemm(const qd_nvfp4 *rq, const int32_t *sel_idx, int32_t 
  *   expert_offsets  : int32 [E+1] row ranges per expert (NULL: E must be 1).
  *   rows            : number of grouped rows (T*k for the MoE layer).
  *   w               : E groups of [N][K].
- *   rq, sel_idx, Ks : the masked residual (NULL / 0: plain W4A4).
+ *   rq, sel_idx, Ks : the masked residual (NULL / 0: plain W4A4; Ks > 0
+ *                     needs rq).
+ *   rq_sel          : rac_gather_selected(rq, sel_idx, Ks) (f16, 16-byte
+ *                     aligned).  The kernel for many rows per expert
+ *                     contracts the residual in this compact form and
+ *                     returns QD_ERR_NULL without it; other shapes ignore
+ *                     it (NULL allowed).
  *   epilogue        : QD_EPI_NONE: out bf16 [rows][N] = bf16(v);
  *                     QD_EPI_SWIGLU: N = 2I, gate rows [0,I), up rows
  *                     [I,2I); out bf16 [rows][I] = bf16(silu(g)*u).
@@ -206,8 +226,9 @@ int64_t   moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int64_t K, i
 qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
                                 const int32_t *expert_offsets, int32_t E, int64_t rows,
                                 const qd_nvfp4 *w, const qd_nvfp4 *rq,
-                                const int32_t *sel_idx, int32_t Ks, int32_t epilogue,
-                                void *out, float *amax_partials, void *stream);
+                                const int32_t *sel_idx, int32_t Ks, const void *rq_sel,
+                                int32_t epilogue, void *out, float *amax_partials,
+                                void *stream);
 
 /* ---------------------------------------------------------------------
  * moe_unpermute_combine -- weighted sum of the k expert outputs per token:
@@ -268,7 +289,7 @@ enum {
   QD_VIEW_XQ_CODES, QD_VIEW_XQ_SCALES, QD_VIEW_XQ_GSCALE, QD_VIEW_SCORES, QD_VIEW_RAMAX,
   QD_VIEW_SEL, QD_VIEW_RQ_CODES, QD_VIEW_RQ_SCALES, QD_VIEW_RQ_GSCALE, QD_VIEW_H,
   QD_VIEW_H_AMAX, QD_VIEW_HQ_CODES, QD_VIEW_HQ_SCALES, QD_VIEW_HQ_GSCALE, QD_VIEW_Z,
-  QD_VIEW_COUNT
+  QD_VIEW_RQ_SEL, QD_VIEW_COUNT
 };
 qd_status qd_moe_layer_views(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I,
                              int64_t *off /* host, QD_VIEW_COUNT */);

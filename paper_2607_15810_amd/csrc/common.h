@@ -207,4 +207,8 @@ namespace qdi {
 void launch_reduce_max(const float *in, int64_t n, float *out, hipStream_t s);
 // Fill n int32 with a value (a kernel, so it is safe inside captured graphs).
 void launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
+// Whether moe_w4a4_grouped_gemm on these sizes contracts the residual from
+// its compact form (rq_sel).
+bool gemm_wants_rq_sel(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
+                       int32_t epilogue);
 }  // namespace qdi

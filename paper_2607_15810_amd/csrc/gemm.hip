@@ -41,6 +41,8 @@ struct GemmArgs {
   const float *r_gs;
   const int32_t *sel;
   int Ks;
+  const uint16_t *r_sel;   // f16 [a rows][ksa]: the residual at the selected channels
+  int ksa;                 // row length of r_sel (Ks rounded up to 16)
   uint16_t *out;
   float *amax_part;
 };
@@ -790,6 +792,16 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
 //    stage s + TL_NS - 1 into the slot of stage s - 1 (read during stage
 //    s - 2) and reads stage s + 1 while the MFMAs of stage s drain.
 //
+//  * RAC: the residual contraction runs over the selected channels alone,
+//    compacted.  While a stage is in LDS the workgroup copies the selected
+//    channels of its weight rows out of it, decoded to f16, into a compact
+//    [128 rows][K_s] LDS table; after the K loop the accumulators are
+//    rescaled by -s_dec_x / s_dec_r and the residual (compacted per token,
+//    f16, from the caller) is multiplied onto them against that table, so
+//    the epilogue's single scale -s_dec_r * s_dec_w yields
+//    s_dec_x s_dec_w acc - s_dec_r s_dec_w accr with one extra f32 rounding
+//    of the main sum.  A ring of three slots leaves LDS room for the table.
+//
 // Stage slot: A codes [8 fragments][64 lanes][16 B], B codes [4 fragments]
 // likewise, then A scale dwords [256 rows] and B scale dwords [128 rows].
 // Lane l of a fragment holds row l % 32, elements 32 (l / 32) .. +31 of the
@@ -799,14 +811,20 @@ constexpr int TL_THREADS = 256;
 constexpr int TL_M = 256;
 constexpr int TL_N = 128;
 constexpr int TL_K = 64;
-constexpr int TL_NS = 4;
 constexpr int TL_ACODE = 0;
 constexpr int TL_BCODE = 8192;
 constexpr int TL_ASCL = 12288;
 constexpr int TL_BSCL = 13312;
 constexpr int TL_STAGE = 13824;
-constexpr int TL_LDS = TL_NS * TL_STAGE;
 constexpr int TL_EMAX = 1024;            // experts handled by the tile scan (4 per thread)
+constexpr int TL_LDS_MAX = 160 * 1024 - 1024;   // dynamic LDS beside the static arrays
+
+__host__ __device__ constexpr int tl_ns(bool rac) { return rac ? 3 : 4; }   // ring depth
+// LDS: ring, then (RAC) the compact weight table [128][ksa + 8] f16 and the
+// selected channels [ksa]
+__host__ __device__ inline int tl_lds_bytes(bool rac, int ksa) {
+  return tl_ns(rac) * TL_STAGE + (rac ? TL_N * (ksa + 8) * 2 + ksa * 4 : 0);
+}
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -884,8 +902,9 @@ __device__ __forceinline__ float swiglu_fast(float g, float u) {
   return g * __builtin_amdgcn_rcpf(1.0f + e) * u;
 }
 
-template <bool GATHER, int EPI>
+template <bool GATHER, bool RAC, int EPI>
 __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, int ntn) {
+  constexpr int NS = tl_ns(RAC);
   extern __shared__ __align__(16) unsigned char lds[];
   __shared__ int sh_w[4];
   __shared__ int sh_t[4];
@@ -975,7 +994,27 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
       dma4s(as_, oas, sb + TL_ASCL + w * 256);
       dma4s(bs_, obs, sb + TL_BSCL + (w & 1) * 256);
     };
-    const float alpha = p.a_gs[1] * p.w_gs[2 * e + 1];
+    const float a_dec = p.a_gs[1], sw = p.w_gs[2 * e + 1];
+    float alpha = a_dec * sw;
+    // RAC: acc -> acc * inv_c + accr, then alpha = -s_dec_r * s_dec_w.  A
+    // residual whose tensor scale is below 2^-60 of the activation's is
+    // left out (its share of any output is far below f32 resolution).
+    float inv_c = 0.0f;
+    bool res_on = false;
+    const int ksa = RAC ? p.ksa : 0, ksp = ksa + 8;
+    unsigned char *bres = lds + NS * TL_STAGE;
+    int32_t *sel_l = reinterpret_cast<int32_t *>(bres + TL_N * ksp * 2);
+    if (RAC) {
+      const float r_dec = p.r_gs[1];
+      inv_c = -(a_dec / r_dec);
+      res_on = r_dec > 0.0f && fabsf(inv_c) <= 0x1p60f;
+      if (res_on) alpha = -r_dec * sw;
+      for (int i = tid; i < ksa; i += TL_THREADS) sel_l[i] = i < p.Ks ? p.sel[i] : 0;
+      // pad columns of the compact table are zero (the residual's are too)
+      const int pad = ksa - p.Ks;
+      for (int i = tid; i < TL_N * pad; i += TL_THREADS)
+        *reinterpret_cast<_Float16 *>(bres + ((i / pad) * ksp + p.Ks + i % pad) * 2) = (_Float16)0.0f;
+    }
     const int wm = w & 1, wn = w >> 1;
     const bool wide = nrows > 128;
     const int fa0 = wide ? 4 * wm : 2 * wm;
@@ -996,17 +1035,38 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
           for (int t = 0; t < 16; ++t) acc[i][j][t] = 0.0f;
       TlRaw R0, R1;
 #pragma unroll
-      for (int t = 0; t < TL_NS - 1; ++t) issue(t, t);
-      wait_vm<(TL_NS - 2) * 5>();
+      for (int t = 0; t < NS - 1; ++t) issue(t, t);
+      wait_vm<(NS - 2) * 5>();
       __syncthreads();
       if constexpr (MTV > 0) tl_read<MTV>(R0, lds, fa0, fb0, fbs, lane);
+      int sp = 0;                              // first selected channel not yet copied
       auto body = [&](const TlRaw &Rc, TlRaw &Rn, int s) __attribute__((always_inline)) {
         auto mid = [&]() __attribute__((always_inline)) {
-          wait_vm<(TL_NS - 3) * 5>();
+          wait_vm<(NS - 3) * 5>();
           __syncthreads();
-          issue(s + TL_NS - 1, (s + TL_NS - 1) % TL_NS);
+          issue(s + NS - 1, (s + NS - 1) % NS);
           if constexpr (MTV > 0)
-            tl_read<MTV>(Rn, lds + ((s + 1) % TL_NS) * TL_STAGE, fa0, fb0, fbs, lane);
+            tl_read<MTV>(Rn, lds + ((s + 1) % NS) * TL_STAGE, fa0, fb0, fbs, lane);
+          if constexpr (RAC) {
+            // selected channels of stage s (slot s % NS holds it until the
+            // next barrier): decoded weight values into the compact table
+            const unsigned char *sl = lds + (s % NS) * TL_STAGE;
+            int se = sp;
+            while (se < p.Ks && (int)uni((uint32_t)sel_l[se]) < TL_K * (s + 1)) ++se;
+            const int tb = tid & 127, f = tb >> 5, r = tb & 31;
+            for (int k = sp + (tid >> 7); k < se; k += 2) {
+              const int el = sel_l[k] - TL_K * s;
+              float v = 0.0f;
+              if (el >= 0 && el < TL_K) {       // sel ascending: always
+                const uint32_t byte = sl[TL_BCODE + ((f * 64 + (el >> 5) * 32 + r) * 16) + ((el & 31) >> 1)];
+                const uint32_t code = (el & 1) ? byte >> 4 : byte & 15u;
+                v = e2m1_value(code) * e4m3_to_f32(sl[TL_BSCL + tb * 4 + (el >> 4)]);
+                if (code & 8u) v = -v;
+              }
+              *reinterpret_cast<_Float16 *>(bres + (tb * ksp + k) * 2) = (_Float16)v;
+            }
+            sp = se;
+          }
         };
         if constexpr (MTV > 0) tl_stage<MTV>(Rc, acc, lane, mid);
         else mid();
@@ -1016,6 +1076,48 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
         body(R1, R0, s + 1);
       }
       wait_vm<0>();
+      if constexpr (RAC) {
+        if (res_on) {
+          __syncthreads();                     // the compact table is complete
+          if constexpr (MTV > 0) {
+            const int h = lane >> 5;
+            const uint16_t *ar[MTV];
+#pragma unroll
+            for (int i = 0; i < MTV; ++i) {
+              const int rr = 32 * (fa0 + i) + (lane & 31);
+              const int rc = rr < nrows ? rr : 0;
+              const int64_t tk = GATHER ? (int64_t)p.row_token[row0 + rc] : (int64_t)(row0 + rc);
+              ar[i] = p.r_sel + tk * ksa + 8 * h;
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+              for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int q = 0; q < 16; ++q) acc[i][j][q] *= inv_c;
+            f16x8 an[MTV];
+#pragma unroll
+            for (int i = 0; i < MTV; ++i) an[i] = *reinterpret_cast<const f16x8 *>(ar[i]);
+            for (int c = 0; c < ksa; c += 16) {
+              f16x8 ac[MTV], bfr[2];
+#pragma unroll
+              for (int i = 0; i < MTV; ++i) {
+                ac[i] = an[i];
+                if (c + 16 < ksa) an[i] = *reinterpret_cast<const f16x8 *>(ar[i] + c + 16);
+              }
+#pragma unroll
+              for (int j = 0; j < 2; ++j) {
+                const int fb = fb0 + j * fbs;
+                bfr[j] = *reinterpret_cast<const f16x8 *>(bres + ((32 * fb + (lane & 31)) * ksp + c + 8 * h) * 2);
+              }
+#pragma unroll
+              for (int i = 0; i < MTV; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(ac[i], bfr[j], acc[i][j]);
+            }
+          }
+        }
+      }
       // ---- epilogue: tensor scales, SwiGLU or plain, bf16 pairs of
       // adjacent columns swapped between neighbouring lanes so that every
       // store writes 4 bytes
@@ -1119,16 +1221,19 @@ void launch_skinny(const GemmArgs &p, const SkPlan &pl, hipStream_t s) {
 // host-side plan of the prefill kernel
 struct TlPlan {
   bool ok;
-  int ntn, grid;
+  int ntn, grid, lds;
 };
 
-inline TlPlan tile_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac) {
+// rac: the residual is fused (needs its compact form, rq_sel)
+inline TlPlan tile_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac, int Ks) {
   TlPlan pl{};
-  if (rac || K < 4 * TL_K || K % (2 * TL_K) != 0 || N % TL_N != 0 || E > TL_EMAX) return pl;
+  if (K < 4 * TL_K || K % (2 * TL_K) != 0 || N % TL_N != 0 || E > TL_EMAX) return pl;
   // byte offsets inside one activation matrix or one expert's weights, and
   // output offsets, fit 32 bits
   if (N * K / 2 >= (1LL << 32) || (rows + 1) * K / 2 >= (1LL << 32)) return pl;
   if ((rows + TL_M) * N * 2 >= (1LL << 32)) return pl;
+  pl.lds = tl_lds_bytes(rac, rac ? (Ks + 15) / 16 * 16 : 0);
+  if (pl.lds > TL_LDS_MAX) return pl;
   pl.ntn = (int)(N / TL_N);
   int64_t g = ((rows + TL_M - 1) / TL_M + E) * pl.ntn;
   g = (g + 7) / 8 * 8;
@@ -1138,14 +1243,14 @@ inline TlPlan tile_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac) {
   return pl;
 }
 
-template <bool GATHER, int EPI>
+template <bool GATHER, bool RAC, int EPI>
 void launch_tile(const GemmArgs &p, const TlPlan &pl, hipStream_t s) {
-  auto kern = gemm_tile_kernel<GATHER, EPI>;
+  auto kern = gemm_tile_kernel<GATHER, RAC, EPI>;
   static const bool attr = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                                               TL_LDS) == hipSuccess;
+                                               TL_LDS_MAX) == hipSuccess;
   (void)attr;
-  hipLaunchKernelGGL(kern, dim3((unsigned)pl.grid), dim3(TL_THREADS), TL_LDS, s, p, pl.ntn);
+  hipLaunchKernelGGL(kern, dim3((unsigned)pl.grid), dim3(TL_THREADS), (size_t)pl.lds, s, p, pl.ntn);
 }
 
 template <bool GATHER, bool RAC>
@@ -1156,9 +1261,9 @@ void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, const SkPl
     else launch_skinny<GATHER, RAC, QD_EPI_NONE>(p, pl, s);
     return;
   }
-  if (!RAC && tp.ok) {
-    if (epi == QD_EPI_SWIGLU) launch_tile<GATHER, QD_EPI_SWIGLU>(p, tp, s);
-    else launch_tile<GATHER, QD_EPI_NONE>(p, tp, s);
+  if (tp.ok) {
+    if (epi == QD_EPI_SWIGLU) launch_tile<GATHER, RAC, QD_EPI_SWIGLU>(p, tp, s);
+    else launch_tile<GATHER, RAC, QD_EPI_NONE>(p, tp, s);
     return;
   }
   if (epi == QD_EPI_SWIGLU)
@@ -1169,12 +1274,18 @@ void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, const SkPl
 
 }  // namespace
 
+bool qdi::gemm_wants_rq_sel(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
+                            int32_t epilogue) {
+  if (Ks <= 0 || rows <= 0 || E < 1 || N <= 0 || K <= 0) return false;
+  return !skinny_plan(rows, E, N, K, Ks, epilogue).ok && tile_plan(rows, E, N, K, true, Ks).ok;
+}
+
 extern "C" int64_t moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int64_t K,
                                                     int32_t E, int32_t Ks, int32_t epilogue) {
   if (rows < 0 || N <= 0 || K <= 0 || E < 1 || Ks < 0) return 0;
   const SkPlan pl = skinny_plan(rows, E, N, K, Ks, epilogue);
   if (pl.ok) return pl.grid;
-  const TlPlan tp = tile_plan(rows, E, N, K, Ks > 0);
+  const TlPlan tp = tile_plan(rows, E, N, K, Ks > 0, Ks);
   if (tp.ok) return tp.grid;
   return grid_x(rows, E, true) * grid_y(N, epilogue);
 }
@@ -1182,8 +1293,9 @@ extern "C" int64_t moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int
 extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
                                            const int32_t *expert_offsets, int32_t E, int64_t rows,
                                            const qd_nvfp4 *w, const qd_nvfp4 *rq,
-                                           const int32_t *sel_idx, int32_t Ks, int32_t epilogue,
-                                           void *out, float *amax_partials, void *stream) {
+                                           const int32_t *sel_idx, int32_t Ks, const void *rq_sel,
+                                           int32_t epilogue, void *out, float *amax_partials,
+                                           void *stream) {
   if (!a || !w || !out) return QD_ERR_NULL;
   if (epilogue != QD_EPI_NONE && epilogue != QD_EPI_SWIGLU) return QD_ERR_DTYPE;
   if (E < 1 || rows < 0) return QD_ERR_SHAPE;
@@ -1197,6 +1309,7 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
   if (epilogue == QD_EPI_SWIGLU && (N % 32 != 0)) return QD_ERR_SHAPE;
   if (!expert_offsets && E != 1) return QD_ERR_SHAPE;
   if (!row_token && rows > a->rows) return QD_ERR_SHAPE;
+  if (Ks > 0 && !rq) return QD_ERR_NULL;
   const bool rac = rq != nullptr && Ks > 0;
   if (rac) {
     st = qdh::check_nvfp4(rq, 1, rq->rows, K);
@@ -1233,11 +1346,15 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
     p.r_gs = rq->gscale;
     p.sel = sel_idx;
     p.Ks = Ks;
+    p.r_sel = static_cast<const uint16_t *>(rq_sel);
+    p.ksa = (Ks + 15) / 16 * 16;
   }
   p.out = static_cast<uint16_t *>(out);
   p.amax_part = amax_partials;
   const SkPlan pl = skinny_plan(rows, E, N, K, rac ? Ks : 0, epilogue);
-  const TlPlan tp = tile_plan(rows, E, N, K, rac);
+  const TlPlan tp = tile_plan(rows, E, N, K, rac, Ks);
+  // the tiled kernel takes the residual in its compact form only
+  if (rac && !pl.ok && tp.ok && (!rq_sel || !qdh::aligned16(rq_sel))) return rq_sel ? QD_ERR_ALIGN : QD_ERR_NULL;
   dim3 grid((unsigned)gx, (unsigned)gy);
   hipStream_t s = qdh::S(stream);
   if (row_token) {

@@ -124,6 +124,7 @@ Layout make_layout(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I) {
   put(QD_VIEW_HQ_GSCALE, 8);
   L.q2_ws = blob((int64_t)nvfp4_quantize_act_workspace(R, I));
   put(QD_VIEW_Z, R * H * 2);
+  put(QD_VIEW_RQ_SEL, T * H * 2);       // the compact residual, K_s <= H columns
   L.total = o;
   return L;
 }
@@ -197,6 +198,9 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   float *ramax = (float *)P(QD_VIEW_RAMAX);
   int32_t *sel = (int32_t *)P(QD_VIEW_SEL);
   const bool rac = Ks > 0;
+  // the W13 kernel for many rows per expert takes the residual compacted
+  const bool want_sel = rac && qdi::gemm_wants_rq_sel(R, E, 2 * I, H, Ks, QD_EPI_SWIGLU);
+  void *rq_sel = want_sel ? P(QD_VIEW_RQ_SEL) : nullptr;
   hipStream_t s = qdh::S(stream);
   // routing scratch, amax partials of X and the channel bitmap (the same
   // carving the standalone calls use)
@@ -244,6 +248,12 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
     hipLaunchKernelGGL(layer_resq_kernel, dim3((unsigned)g), dim3(256), 0, s,
                        static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
                        ramax, bitmap, rq.codes, rq.scales, rq.gscale);
+    if (want_sel) {
+      st = qdh::check_launch();
+      if (st) return st;
+      st = rac_gather_selected(&rq, sel, Ks, rq_sel, stream);
+      if (st) return st;
+    }
   } else {
     hipLaunchKernelGGL(layer_scatter_kernel, dim3((unsigned)nr), dim3(256), 0, s, T, E, k, nr,
                        ids, counts, ranks, offs, row_token, inv_row);
@@ -254,7 +264,7 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   float *hamax = (float *)P(QD_VIEW_H_AMAX);
   mark(QD_STAGE_W13);
   st = moe_w4a4_grouped_gemm(&xq, row_token, offs, E, R, w13, rac ? &rq : nullptr,
-                             rac ? sel : nullptr, Ks, QD_EPI_SWIGLU, h, hamax, stream);
+                             rac ? sel : nullptr, Ks, rq_sel, QD_EPI_SWIGLU, h, hamax, stream);
   if (st) return st;
   qd_nvfp4 hq{(uint8_t *)P(QD_VIEW_HQ_CODES), (uint8_t *)P(QD_VIEW_HQ_SCALES),
               (float *)P(QD_VIEW_HQ_GSCALE), 1, R, I};
@@ -266,7 +276,8 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   if (st) return st;
   uint16_t *z = (uint16_t *)P(QD_VIEW_Z);
   mark(QD_STAGE_W2);
-  st = moe_w4a4_grouped_gemm(&hq, nullptr, offs, E, R, w2, nullptr, nullptr, 0, QD_EPI_NONE, z,
+  st = moe_w4a4_grouped_gemm(&hq, nullptr, offs, E, R, w2, nullptr, nullptr, 0, nullptr,
+                             QD_EPI_NONE, z,
                              nullptr, stream);
   if (st) return st;
   mark(QD_STAGE_COMBINE);

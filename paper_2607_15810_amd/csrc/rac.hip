@@ -281,6 +281,28 @@ __global__ __launch_bounds__(256) void rac_residual_gemm_kernel(
   if (n < N) out[r * N + n] = alpha * acc;
 }
 
+// the masked residual at the selected channels, compacted per row, as f16
+// without the tensor scale: e2m1(code) * e4m3(block scale) is exact in f16;
+// columns past Ks are zero
+__global__ __launch_bounds__(256) void rac_gather_selected_kernel(
+    const uint8_t *__restrict__ codes, const uint8_t *__restrict__ scales, int64_t K,
+    const int32_t *__restrict__ sel, int Ks, int width, int64_t rows, uint16_t *__restrict__ out) {
+  const int64_t n = rows * width;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const int64_t t = i / width;
+    const int j = (int)(i - t * width);
+    float v = 0.0f;
+    if (j < Ks) {
+      const int64_t c = sel[j];
+      const uint32_t byte = codes[t * (K >> 1) + (c >> 1)];
+      const uint32_t code = (c & 1) ? byte >> 4 : byte & 15u;
+      v = e2m1_value(code) * e4m3_to_f32(scales[t * (K >> 4) + (c >> 4)]);
+      if (code & 8u) v = -v;
+    }
+    out[i] = __builtin_bit_cast(uint16_t, (_Float16)v);
+  }
+}
+
 }  // namespace
 
 extern "C" size_t rac_select_channels_workspace(int64_t T, int64_t K) {
@@ -373,5 +395,27 @@ extern "C" qd_status rac_residual_gemm(const qd_nvfp4 *rq, const int32_t *sel_id
   hipLaunchKernelGGL(rac_residual_gemm_kernel, dim3((unsigned)rows, (unsigned)gy), dim3(256), 0, s,
                      rq->codes, rq->scales, rq->gscale, sel_idx, Ks, row_token, expert_offsets,
                      (int)w->groups, rows, w->codes, w->scales, w->gscale, w->rows, rq->cols, out);
+  return qdh::check_launch();
+}
+
+extern "C" int32_t rac_selected_width(int32_t Ks) { return Ks <= 0 ? 0 : (Ks + 15) / 16 * 16; }
+
+extern "C" qd_status rac_gather_selected(const qd_nvfp4 *rq, const int32_t *sel_idx, int32_t Ks,
+                                         void *out, void *stream) {
+  if (!rq || !out) return QD_ERR_NULL;
+  if (Ks < 0 || Ks > rq->cols) return QD_ERR_SHAPE;
+  if (Ks > 0 && !sel_idx) return QD_ERR_NULL;
+  qd_status st = qdh::check_nvfp4(rq, 1, rq->rows, rq->cols);
+  if (st) return st;
+  if (!qdh::aligned16(out)) return QD_ERR_ALIGN;
+  if (qdh::fault_injected()) return QD_ERR_HIP;
+  const int width = rac_selected_width(Ks);
+  const int64_t n = rq->rows * width;
+  if (n == 0) return QD_OK;
+  int64_t g = (n + 255) / 256;
+  if (g > 8192) g = 8192;
+  hipLaunchKernelGGL(rac_gather_selected_kernel, dim3((unsigned)g), dim3(256), 0, qdh::S(stream),
+                     rq->codes, rq->scales, rq->cols, sel_idx, Ks, width, rq->rows,
+                     static_cast<uint16_t *>(out));
   return qdh::check_launch();
 }

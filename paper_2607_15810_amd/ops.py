@@ -146,6 +146,16 @@ def select_channels(x, xq, Ks, scores=None, ramax=None):
     return sel[:Ks], rq, scores, ramax
 
 
+def gather_selected(rq, sel):
+    """The masked residual at the selected channels, compacted per row: f16
+    [rows][rac_selected_width(Ks)] (no tensor scale; zero past Ks)."""
+    Ks = int(sel.numel())
+    width = Q.lib().rac_selected_width(Ks)
+    out = torch.empty((rq.rows, max(width, 8)), dtype=torch.float16, device=rq.codes.device)
+    Q.call("rac_gather_selected", _nv(rq), _ptr(sel), Ks, out.data_ptr(), _stream())
+    return out[:, :width]
+
+
 def residual_gemm(rq, sel, w, rows, row_token=None, offsets=None):
     dev = rq.codes.device
     out = torch.empty((rows, w.rows), dtype=torch.float32, device=dev)
@@ -155,7 +165,9 @@ def residual_gemm(rq, sel, w, rows, row_token=None, offsets=None):
 
 
 def grouped_gemm(a, w, rows, row_token=None, offsets=None, rq=None, sel=None,
-                 epilogue=Q.QD_EPI_NONE, want_amax=False):
+                 epilogue=Q.QD_EPI_NONE, want_amax=False, rq_sel=None):
+    """rq_sel: the compact residual (gather_selected(rq, sel)); formed here
+    when the residual is given without it."""
     dev = a.codes.device
     E = w.groups
     N = w.rows
@@ -166,9 +178,11 @@ def grouped_gemm(a, w, rows, row_token=None, offsets=None, rq=None, sel=None,
     if want_amax:
         cnt = Q.lib().moe_w4a4_grouped_gemm_amax_count(rows, N, a.cols, E, Ks, epilogue)
         amax = torch.empty(max(cnt, 1), dtype=torch.float32, device=dev)
+    if Ks and rq_sel is None:
+        rq_sel = gather_selected(rq, sel)
     Q.call("moe_w4a4_grouped_gemm", _nv(a), _ptr(row_token), _ptr(offsets), E, rows, _nv(w),
-           _nv(rq) if Ks else None, _ptr(sel) if Ks else None, Ks, epilogue, out.data_ptr(),
-           _ptr(amax), _stream())
+           _nv(rq) if Ks else None, _ptr(sel) if Ks else None, Ks,
+           _ptr(rq_sel) if Ks else None, epilogue, out.data_ptr(), _ptr(amax), _stream())
     return out, amax
 
 
@@ -251,4 +265,5 @@ class MoELayer:
             hq_scales=self.view("hq_scales", u8, (R, I // 16)),
             hq_gscale=self.view("hq_gscale", f32, (2,)),
             z=self.view("z", torch.bfloat16, (R, H)),
+            rq_sel=self.view("rq_sel", torch.float16, (T, Q.lib().rac_selected_width(self.Ks))),
         )

@@ -29,7 +29,7 @@ STAGE_NAMES = ["route", "quant_x", "select", "w13", "quant_h", "w2", "combine"]
 
 VIEW_NAMES = ["topk_ids", "topk_w", "offsets", "row_token", "inv_row", "xq_codes",
               "xq_scales", "xq_gscale", "scores", "ramax", "sel", "rq_codes", "rq_scales",
-              "rq_gscale", "h", "h_amax", "hq_codes", "hq_scales", "hq_gscale", "z"]
+              "rq_gscale", "h", "h_amax", "hq_codes", "hq_scales", "hq_gscale", "z", "rq_sel"]
 
 
 class NVFP4(ctypes.Structure):
@@ -58,12 +58,14 @@ SIGNATURES = {
     "rac_select_channels_workspace": (c_size_t, [c_int64, c_int64]),
     "rac_select_channels": (c_int, [c_void_p, PN, c_int32, c_void_p, c_void_p, c_int32,
                                     c_void_p, PN, c_void_p, c_size_t, c_void_p]),
+    "rac_selected_width": (c_int32, [c_int32]),
+    "rac_gather_selected": (c_int, [PN, c_void_p, c_int32, c_void_p, c_void_p]),
     "rac_residual_gemm": (c_int, [PN, c_void_p, c_int32, c_void_p, c_void_p, c_int64, PN,
                                   c_void_p, c_void_p]),
     "moe_w4a4_grouped_gemm_amax_count": (c_int64, [c_int64, c_int64, c_int64, c_int32, c_int32,
                                                    c_int32]),
     "moe_w4a4_grouped_gemm": (c_int, [PN, c_void_p, c_void_p, c_int32, c_int64, PN, PN,
-                                      c_void_p, c_int32, c_int32, c_void_p, c_void_p,
+                                      c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_void_p,
                                       c_void_p]),
     "moe_unpermute_combine": (c_int, [c_void_p, c_void_p, c_void_p, c_int64, c_int32, c_int64,
                                       c_void_p, c_void_p]),

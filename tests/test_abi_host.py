@@ -103,23 +103,47 @@ def test_route_validation(lib):
 def test_gemm_validation(lib):
     a = _nv(1, 16, 256, FAKE)
     w = _nv(4, 128, 256, FAKE)
+    # (a, row_token, offsets, E, rows, w, rq, sel, Ks, rq_sel, epilogue, out, amax, stream)
     r = lambda *x: Q.raw("moe_w4a4_grouped_gemm", *x)
-    assert r(ctypes.byref(a), None, FAKE, 4, 16, ctypes.byref(w), None, None, 0, 5, FAKE,
+    assert r(ctypes.byref(a), None, FAKE, 4, 16, ctypes.byref(w), None, None, 0, None, 5, FAKE,
              None, None) == Q.QD_ERR_DTYPE
-    assert r(ctypes.byref(a), None, None, 4, 16, ctypes.byref(w), None, None, 0, 0, FAKE,
+    assert r(ctypes.byref(a), None, None, 4, 16, ctypes.byref(w), None, None, 0, None, 0, FAKE,
              None, None) == Q.QD_ERR_SHAPE          # E > 1 needs offsets
     w_badk = _nv(4, 128, 128, FAKE)
-    assert r(ctypes.byref(a), None, FAKE, 4, 16, ctypes.byref(w_badk), None, None, 0, 0, FAKE,
-             None, None) == Q.QD_ERR_SHAPE
+    assert r(ctypes.byref(a), None, FAKE, 4, 16, ctypes.byref(w_badk), None, None, 0, None, 0,
+             FAKE, None, None) == Q.QD_ERR_SHAPE
     w_odd = _nv(4, 40, 256, FAKE)                  # SwiGLU needs N % 32 == 0
-    assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w_odd), None, None, 0, 1, FAKE,
-             None, None) == Q.QD_ERR_SHAPE
+    assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w_odd), None, None, 0, None, 1,
+             FAKE, None, None) == Q.QD_ERR_SHAPE
     rq = _nv(1, 16, 256, FAKE)
-    assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w), ctypes.byref(rq), None, 4, 0,
-             FAKE, None, None) == Q.QD_ERR_NULL     # residual without channel list
-    assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w), None, None, 0, 0, FAKE + 8,
-             None, None) == Q.QD_ERR_ALIGN
+    assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w), ctypes.byref(rq), None, 4,
+             None, 0, FAKE, None, None) == Q.QD_ERR_NULL     # residual without channel list
+    assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w), None, FAKE, 4, None, 0,
+             FAKE, None, None) == Q.QD_ERR_NULL     # K_s > 0 without the residual
+    assert r(ctypes.byref(a), FAKE, FAKE, 4, 16, ctypes.byref(w), None, None, 0, None, 0,
+             FAKE + 8, None, None) == Q.QD_ERR_ALIGN
+    # many rows per expert: the tiled kernel needs the compact residual
+    a_big = _nv(1, 4096, 256, FAKE)
+    rq_big = _nv(1, 4096, 256, FAKE)
+    w_big = _nv(4, 256, 256, FAKE)
+    assert r(ctypes.byref(a_big), FAKE, FAKE, 4, 8192, ctypes.byref(w_big), ctypes.byref(rq_big),
+             FAKE, 8, None, 1, FAKE, None, None) == Q.QD_ERR_NULL
+    assert r(ctypes.byref(a_big), FAKE, FAKE, 4, 8192, ctypes.byref(w_big), ctypes.byref(rq_big),
+             FAKE, 8, FAKE + 8, 1, FAKE, None, None) == Q.QD_ERR_ALIGN
     assert lib.moe_w4a4_grouped_gemm_amax_count(64, 256, 256, 4, 8, 1) > 0
+    # the layer sizes its partial buffer with the same count the kernel writes
+    assert lib.moe_w4a4_grouped_gemm_amax_count(8192, 256, 256, 4, 8, 1) % 8 == 0
+
+
+def test_gather_selected_validation(lib):
+    rq = _nv(1, 8, 64, FAKE)
+    r = lambda *x: Q.raw("rac_gather_selected", *x)
+    assert lib.rac_selected_width(0) == 0 and lib.rac_selected_width(1) == 16
+    assert lib.rac_selected_width(64) == 64 and lib.rac_selected_width(65) == 80
+    assert r(ctypes.byref(rq), FAKE, 65, FAKE, None) == Q.QD_ERR_SHAPE     # K_s > K
+    assert r(ctypes.byref(rq), None, 4, FAKE, None) == Q.QD_ERR_NULL
+    assert r(ctypes.byref(rq), FAKE, 4, FAKE + 8, None) == Q.QD_ERR_ALIGN
+    assert r(ctypes.byref(rq), None, 0, FAKE, None) == Q.QD_OK            # nothing to gather
 
 
 def test_select_and_combine_validation(lib):

@@ -55,6 +55,12 @@ SMALL = [
     # tile kernel (several n-tiles, partial m-tiles, skewed routing)
     ("tile", 256, 256, 4, 2, 128, 0, {}),
     ("tile_ragged_zipf", 300, 512, 8, 2, 256, 0, dict(routing="zipf")),
+    # the tile kernel with the residual fused in compact form: K_s padded to
+    # 16, skewed routing with edge-case activations, and K_s = K
+    ("tile_rac", 256, 256, 4, 2, 128, 8, {}),
+    ("tile_rac_zipf_edges", 300, 512, 8, 2, 128, 40,
+     dict(routing="zipf", acts="student_t3", edge_cases=True, outlier_frac=0.0)),
+    ("tile_rac_all", 256, 256, 4, 2, 64, 256, {}),
     # many rows per expert: the tiled (prefill) kernel instead of the skinny one
     ("many_rows", 256, 256, 4, 2, 64, 8, {}),
     ("many_rows_ktail", 300, 384, 4, 2, 96, 12, {}),
@@ -104,6 +110,12 @@ def test_layer_stagewise_small(case):
     sel, rq, _, _ = ops.select_channels(x, xq, Ks, scores, ramax)
     assert np.array_equal(sel.cpu().numpy(), act["sel"])
     assert_nvfp4_equal(rq, act["rq"], "rq")
+    # the compact residual: exact unscaled values at the selected channels
+    rq_sel = ops.gather_selected(rq, sel).float().cpu().numpy()
+    ref_un = OQ.dequantize_unscaled_f64(act["rq"]["codes"], act["rq"]["scales"])
+    assert rq_sel.shape == (T, (Ks + 15) // 16 * 16)
+    assert np.array_equal(rq_sel[:, :Ks].astype(np.float64), ref_un[:, act["sel"]])
+    assert not rq_sel[:, Ks:].any()
     # the unfused score pass gives the same statistics
     sel2, rq2, sc2, ra2 = ops.select_channels(x, xq, Ks)
     assert np.array_equal(sc2.cpu().numpy(), scores.cpu().numpy())
