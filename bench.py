@@ -49,6 +49,8 @@ def parse():
     ap.add_argument("--workload", default="moe_decode_t256_h2048")
     ap.add_argument("--copies", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-comparisons", action="store_true",
+                    help="skip the FP8 W8A8 layer and the K_s = 0 / 50%% rows")
     ap.add_argument("--cpu-experts", type=int, default=0,
                     help="experts in the oracle sample (0: automatic)")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -294,7 +296,7 @@ def main():
     # the W13 launch runs the decode kernel when the rows per expert are few
     skinny = Q.lib().moe_w4a4_grouped_gemm_amax_count(
         wl.T * wl.k, 2 * wl.I, wl.H, wl.E, wl.Ks, Q.QD_EPI_SWIGLU) <= 1024
-    kname = ("gemm_skinny_kernel" if skinny else "gemm_w4a4_kernel") + \
+    kname = ("gemm_skinny_kernel" if skinny else "gemm_tile_kernel") + \
         " (W13 + fused RAC residual + SwiGLU)"
     traffic = measured_traffic(args.workload)
     if decode:
@@ -338,10 +340,62 @@ def main():
         "roofline": roof,
     }
     print(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
+    if not args.no_comparisons:
+        out["comparisons"] = comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws)
     if not args.no_cpu_baseline:
         ne = args.cpu_experts or (4 if wl.H <= 2048 else 2)
         out["cpu_baseline"] = cpu_baseline(inp, ne)
     print(json.dumps(out))
+
+
+def time_steps(fns, steps, warmup):
+    """Average ms per call of fns[i % len(fns)]() over `steps` calls after
+    `warmup`, bracketed by synchronisations (HIP events on torch's stream)."""
+    import torch
+    for i in range(warmup):
+        fns[i % len(fns)]()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        fns[i % len(fns)]()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
+    """The measurement rows beside the headline: the FP8 W8A8 layer (same
+    routing and shapes, per-token / per-channel E4M3, no residual), the plain
+    W4A4 layer (K_s = 0) and RAC at K_s = 50% of the channels."""
+    import torch
+    from paper_2607_15810_amd import ops
+    dev = "cuda"
+    res = {}
+    steps, warm = max(args.steps, 10), max(args.warmup, 3)
+    y = torch.empty((wl.T, wl.H), dtype=torch.bfloat16, device=dev)
+    # FP8 W8A8 layer, as many weight copies as the headline rotates
+    w13c, w13d = ops.fp8_quantize_rows(inp.w13.to(dev))
+    w2c, w2d = ops.fp8_quantize_rows(inp.w2.to(dev))
+    f8 = [(w13c, w13d, w2c, w2d)] + [tuple(t.clone() for t in (w13c, w13d, w2c, w2d))
+                                     for _ in range(len(banks) - 1)]
+    lay8 = [ops.FP8MoELayer(*b, wl.T, wl.k) for b in f8]
+    ms8 = time_steps([lambda c=c: lay8[c](xs[c], lgs[c], y) for c in range(len(f8))], steps, warm)
+    res["fp8_w8a8"] = dict(ms_per_step=round(ms8, 5), value=round(wl.T / (ms8 * 1e-3), 1),
+                           unit="tokens/s", nvfp4_rac_speedup=round(ms8 / ms_step, 3),
+                           weight_bytes_per_param=1.0)
+    del lay8, f8, w13c, w13d, w2c, w2d
+    # the NVFP4 layer without RAC and with K_s = H / 2 (the paper's k = 50%)
+    for name, ks in (("w4a4_ks0", 0), ("rac_ks_half", wl.H // 2)):
+        lays = [ops.MoELayer(b13, b2, wl.T, wl.k, ks, ws=ws) for b13, b2 in banks]
+        ms = time_steps([lambda c=c: lays[c](xs[c], lgs[c], y) for c in range(len(lays))],
+                        steps, warm)
+        res[name] = dict(ms_per_step=round(ms, 5), value=round(wl.T / (ms * 1e-3), 1),
+                         unit="tokens/s", rac_channels=ks,
+                         time_vs_headline=round(ms / ms_step, 3))
+    torch.cuda.synchronize()
+    return res
 
 
 if __name__ == "__main__":

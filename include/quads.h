@@ -240,6 +240,50 @@ qd_status moe_unpermute_combine(const void *z, const int32_t *inv_row, const flo
                                 int64_t T, int32_t k, int64_t H, void *y, void *stream);
 
 /* ---------------------------------------------------------------------
+ * FP8 W8A8 comparison layer (Sec. 2.2 "FP8" paragraph: the FP8 rollout the
+ * paper compares against), same routing, SwiGLU and combine, no residual.
+ *
+ * fp8_quantize_rows -- E4M3 codes with one f32 scale per row: for a row with
+ * amax m > 0, enc = 448 / m, dec = 1 / enc (f32);
+ * code = E4M3_RNE(min(|x * enc|, 448)) with the sign in bit 7; a zero row
+ * takes dec = 1.  Weights [E][N][K] are E*N rows (one scale per output
+ * channel), activations one scale per token.
+ *   x     : bf16 (QD_DTYPE_BF16) or f32 [rows][cols].
+ *   codes : u8 [rows][cols];  dec: f32 [rows].
+ * ------------------------------------------------------------------- */
+qd_status fp8_quantize_rows(const void *x, int32_t dtype, int64_t rows, int64_t cols,
+                            uint8_t *codes, float *dec, void *stream);
+
+/* ---------------------------------------------------------------------
+ * moe_fp8_grouped_gemm -- per expert e and grouped row r:
+ *   v[r][n] = a_dec[src(r)] * w_dec[e][n] * sum_k a[src(r)][k] * w[e][n][k]
+ * (E4M3 products exact, f32 accumulation), epilogue as in
+ * moe_w4a4_grouped_gemm (QD_EPI_NONE: bf16 [rows][N]; QD_EPI_SWIGLU: N = 2I,
+ * bf16 [rows][I]).
+ *   a_codes, a_dec  : u8 [a_rows][K], f32 [a_rows];  row_token / offsets as
+ *                     in moe_w4a4_grouped_gemm.
+ *   w_codes, w_dec  : u8 [E][N][K], f32 [E][N].
+ * Sizes: K % 64 == 0, K >= 256; N % 256 == 0 (few rows per expert) or
+ * N % 128 == 0 (many); otherwise QD_ERR_UNSUPPORTED.  16-byte aligned codes
+ * and output.
+ * ------------------------------------------------------------------- */
+qd_status moe_fp8_grouped_gemm(const uint8_t *a_codes, const float *a_dec, int64_t a_rows,
+                               const int32_t *row_token, const int32_t *expert_offsets,
+                               int32_t E, int64_t rows, const uint8_t *w_codes,
+                               const float *w_dec, int64_t N, int64_t K, int32_t epilogue,
+                               void *out, void *stream);
+
+/* qd_fp8_moe_layer_forward -- route, quantise X per token, W13 with SwiGLU,
+ * quantise h per row, W2, combine: y bf16 [T][H].  w13: [E][2I][H] codes and
+ * [E][2I] scales; w2: [E][H][I] and [E][H] (from fp8_quantize_rows). */
+size_t    qd_fp8_moe_layer_workspace(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I);
+qd_status qd_fp8_moe_layer_forward(const void *x, const float *logits, int64_t T, int64_t H,
+                                   int32_t E, int32_t k, int64_t I, int32_t renorm,
+                                   const uint8_t *w13_codes, const float *w13_dec,
+                                   const uint8_t *w2_codes, const float *w2_dec, void *y,
+                                   void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------
  * qd_moe_layer_forward -- the whole rollout-side layer in one call: route,
  * quantise X with fused RAC scores, select, W13 GEMM with fused residual
  * and SwiGLU, quantise h, W2 GEMM, combine.  Same results as the seven

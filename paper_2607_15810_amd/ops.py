@@ -267,3 +267,54 @@ class MoELayer:
             z=self.view("z", torch.bfloat16, (R, H)),
             rq_sel=self.view("rq_sel", torch.float16, (T, Q.lib().rac_selected_width(self.Ks))),
         )
+
+
+# ---------------------------------------------------------------- FP8 W8A8 comparison layer
+
+def fp8_quantize_rows(x):
+    """E4M3 codes with one f32 scale per row of x ([rows][cols] bf16 or f32;
+    a weight bank [E][N][K] is E*N rows).  Returns (codes u8, dec f32)."""
+    _require_cuda(x)
+    x = x.contiguous()
+    cols = x.shape[-1]
+    rows = x.numel() // cols if cols else 0
+    codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    dec = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device)
+    dt = Q.QD_DTYPE_BF16 if x.dtype == torch.bfloat16 else Q.QD_DTYPE_F32
+    Q.call("fp8_quantize_rows", x.data_ptr(), dt, rows, cols, codes.data_ptr(), dec.data_ptr(),
+           _stream())
+    return codes, dec
+
+
+def fp8_grouped_gemm(a_codes, a_dec, w_codes, w_dec, rows, row_token=None, offsets=None,
+                     epilogue=Q.QD_EPI_NONE):
+    E, N, K = w_codes.shape
+    ncol = N // 2 if epilogue == Q.QD_EPI_SWIGLU else N
+    out = torch.empty((rows, ncol), dtype=torch.bfloat16, device=a_codes.device)
+    Q.call("moe_fp8_grouped_gemm", a_codes.data_ptr(), a_dec.data_ptr(), a_codes.shape[0],
+           _ptr(row_token), _ptr(offsets), E, rows, w_codes.data_ptr(), w_dec.data_ptr(), N, K,
+           epilogue, out.data_ptr(), _stream())
+    return out
+
+
+class FP8MoELayer:
+    """The FP8 W8A8 layer through qd_fp8_moe_layer_forward (the comparison
+    baseline: same routing, SwiGLU and combine, no residual)."""
+
+    def __init__(self, w13_codes, w13_dec, w2_codes, w2_dec, T, k, renorm=True):
+        self.w13 = (w13_codes, w13_dec)
+        self.w2 = (w2_codes, w2_dec)
+        self.E, N13, self.H = w13_codes.shape
+        self.I = N13 // 2
+        self.T, self.k, self.renorm = T, k, renorm
+        n = Q.lib().qd_fp8_moe_layer_workspace(T, self.H, self.E, k, self.I)
+        self.ws = _ws(n, w13_codes.device)
+
+    def __call__(self, x, logits, y=None):
+        if y is None:
+            y = torch.empty((self.T, self.H), dtype=torch.bfloat16, device=x.device)
+        Q.call("qd_fp8_moe_layer_forward", x.data_ptr(), logits.data_ptr(), self.T, self.H,
+               self.E, self.k, self.I, int(self.renorm), self.w13[0].data_ptr(),
+               self.w13[1].data_ptr(), self.w2[0].data_ptr(), self.w2[1].data_ptr(),
+               y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), _stream())
+        return y
