@@ -340,6 +340,18 @@ def main():
         "roofline": roof,
     }
     print(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
+    # the same steps replayed from HIP graphs (one captured layer call per
+    # weight copy): what a serving loop that captures its decode step sees
+    graphs = []
+    for c in range(copies):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            layers[c](xs[c], lgs[c], y)
+        graphs.append(g)
+    ms_graph = time_steps([g.replay for g in graphs], args.steps, args.warmup)
+    out["hip_graph"] = dict(ms_per_step=round(ms_graph, 5),
+                            value=round(wl.T / (ms_graph * 1e-3), 1), unit="tokens/s")
+    del graphs
     if not args.no_comparisons:
         out["comparisons"] = comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws)
     if not args.no_cpu_baseline:

@@ -428,3 +428,31 @@ def test_full_size_sampled(name):
     assert rel <= 1e-3, f"free-running rel-L2 {rel:.3e}"
     untouched = ~np.isin(perm["inv_row"], rows).any(axis=1)
     assert np.all(yg[untouched] == 0.0)
+
+
+def test_layer_graph_replay():
+    """The whole layer captured in a HIP graph: every replay, with eager work
+    and synchronisations in between, reproduces the eager output bit for bit
+    (the library records no memset nodes; flags and offsets are cleared by
+    kernels)."""
+    for case in (SMALL[0], next(c for c in SMALL if c[0] == "tile_rac")):
+        name, T, H, E, k, I, Ks, _ = case
+        inp = _run_small(case)
+        x = inp.x.to(DEV)
+        logits = inp.logits.to(DEV)
+        w13 = ops.quantize_weight(inp.w13.to(DEV))
+        w2 = ops.quantize_weight(inp.w2.to(DEV))
+        lay = ops.MoELayer(w13, w2, T, k, Ks)
+        y_eager = lay(x, logits).clone()
+        torch.cuda.synchronize()
+        y = torch.empty_like(y_eager)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            lay(x, logits, y)
+        for rep in range(3):
+            y.zero_()
+            lay(x, logits)                 # eager work on the same workspace in between
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(y.view(torch.int16), y_eager.view(torch.int16)), (name, rep)
