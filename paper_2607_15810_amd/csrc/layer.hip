@@ -77,6 +77,17 @@ __global__ __launch_bounds__(256) void layer_resq_kernel(
                      rscales, rgs);
 }
 
+// the residual at the selected channels, compacted per token (what the
+// prefill W13 kernel consumes), with the residual's tensor scale
+__global__ __launch_bounds__(256) void layer_compact_kernel(
+    const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
+    const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
+    const float *__restrict__ ramax, const int32_t *__restrict__ sel, int Ks, int width,
+    uint16_t *__restrict__ out, float *__restrict__ rgs) {
+  qdc::rac_compact_body(blockIdx.x, gridDim.x, x, xcodes, xscales, xgs, T, K, ramax, sel, Ks,
+                        width, out, rgs);
+}
+
 struct Layout {
   int64_t off[QD_VIEW_COUNT];
   int64_t route_ws, q1_ws, sel_ws, q2_ws, total;
@@ -241,18 +252,26 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
     else
       hipLaunchKernelGGL(layer_pre3_kernel<64>, g3, dim3(256), 0, s, T, E, k, nr, ids, counts,
                          ranks, offs, row_token, inv_row, scores, (int)H, Ks, sel, bitmap);
-    const int64_t total = T * (H / 16);
-    int64_t g = (total + 255) / 256;
-    if (g > 4096) g = 4096;
-    if (g < 1) g = 1;
-    hipLaunchKernelGGL(layer_resq_kernel, dim3((unsigned)g), dim3(256), 0, s,
-                       static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
-                       ramax, bitmap, rq.codes, rq.scales, rq.gscale);
     if (want_sel) {
-      st = qdh::check_launch();
-      if (st) return st;
-      st = rac_gather_selected(&rq, sel, Ks, rq_sel, stream);
-      if (st) return st;
+      // the prefill W13 kernel takes the residual at S only: computed
+      // directly for the blocks that hold a selected channel (the full
+      // masked residual is not materialised)
+      const int width = rac_selected_width(Ks);
+      const int64_t total = T * width;
+      int64_t g = (total + 255) / 256;
+      if (g > 8192) g = 8192;
+      if (g < 1) g = 1;
+      hipLaunchKernelGGL(layer_compact_kernel, dim3((unsigned)g), dim3(256), 0, s,
+                         static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
+                         ramax, sel, Ks, width, static_cast<uint16_t *>(rq_sel), rq.gscale);
+    } else {
+      const int64_t total = T * (H / 16);
+      int64_t g = (total + 255) / 256;
+      if (g > 4096) g = 4096;
+      if (g < 1) g = 1;
+      hipLaunchKernelGGL(layer_resq_kernel, dim3((unsigned)g), dim3(256), 0, s,
+                         static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
+                         ramax, bitmap, rq.codes, rq.scales, rq.gscale);
     }
   } else {
     hipLaunchKernelGGL(layer_scatter_kernel, dim3((unsigned)nr), dim3(256), 0, s, T, E, k, nr,

@@ -254,4 +254,48 @@ __device__ __forceinline__ void rac_resq_body(
   }
 }
 
+// The masked residual at the selected channels only, compacted per token:
+// out[t][j] = e2m1 * e4m3 value (no tensor scale, exact in f16) of channel
+// sel[j] in the residual quantised over all channels (the same block
+// arithmetic as rac_resq_body, evaluated for the blocks that hold a selected
+// channel), 0 for Ks <= j < width.  Also writes the residual's tensor scale.
+// Work item i of T * width; workgroup bid of nblk.
+__device__ __forceinline__ void rac_compact_body(
+    int bid, int nblk, const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
+    const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
+    const float *__restrict__ ramax, const int32_t *__restrict__ sel, int Ks, int width,
+    uint16_t *__restrict__ out, float *__restrict__ rgs) {
+  const float amax_r = ramax[0];
+  float s_enc, s_dec;
+  tensor_scale(amax_r, s_enc, s_dec);
+  const bool zero_tensor = !(amax_r >= kZeroAmax);
+  if (bid == 0 && threadIdx.x == 0) {
+    rgs[0] = s_enc;
+    rgs[1] = s_dec;
+  }
+  const float xs_dec = xgs[1];
+  const int64_t nbc = K >> 4;
+  const int64_t total = T * width;
+  const int64_t stride = (int64_t)nblk * blockDim.x;
+  for (int64_t i = (int64_t)bid * blockDim.x + threadIdx.x; i < total; i += stride) {
+    const int64_t t = i / width;
+    const int j = (int)(i - t * width);
+    float v = 0.0f;
+    if (j < Ks) {
+      const int c = sel[j];
+      const int64_t b = t * nbc + (c >> 4);
+      float xv[16], r[16];
+      load_bf16x16(x + b * 16, xv);
+      block_residual(xv, reinterpret_cast<const uint2 *>(xcodes)[b], xscales[b], xs_dec, r);
+      uint32_t lo, hi;
+      const uint32_t sb = quantize_block(r, s_enc, zero_tensor, lo, hi);
+      const int e = c & 15;
+      const uint32_t code = ((e < 8 ? lo : hi) >> (4 * (e & 7))) & 15u;
+      v = e2m1_value(code) * e4m3_to_f32(sb);
+      if (code & 8u) v = -v;
+    }
+    out[i] = __builtin_bit_cast(uint16_t, (_Float16)v);
+  }
+}
+
 }  // namespace qdc

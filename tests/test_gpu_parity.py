@@ -367,8 +367,19 @@ def test_full_size_sampled(name):
     assert np.array_equal(v["scores"].cpu().numpy().view(np.uint64), act["scores"])
     assert v["ramax"].item() == np.max(np.abs(act["r"]))
     assert np.array_equal(v["sel"].cpu().numpy(), act["sel"])
-    assert_nvfp4_equal(dict(packed=v["rq_codes"].cpu().numpy(), scales=v["rq_scales"].cpu().numpy(),
-                            gscale=v["rq_gscale"].cpu().numpy()), act["rq"], "rq")
+    # the masked residual: in full (decode kernel) or at S only, compacted
+    # (prefill kernel), with its tensor scale either way
+    assert v["rq_gscale"].cpu().numpy().view(np.uint32).tolist() == \
+        np.array([act["rq"]["s_enc"], act["rq"]["s_dec"]], np.float32).view(np.uint32).tolist()
+    if Q.lib().moe_w4a4_grouped_gemm_amax_count(R, 2 * I, H, E, Ks, Q.QD_EPI_SWIGLU) <= 1024:
+        assert_nvfp4_equal(dict(packed=v["rq_codes"].cpu().numpy(),
+                                scales=v["rq_scales"].cpu().numpy(),
+                                gscale=v["rq_gscale"].cpu().numpy()), act["rq"], "rq")
+    else:
+        ref_un = OQ.dequantize_unscaled_f64(act["rq"]["codes"], act["rq"]["scales"])
+        got = v["rq_sel"].float().cpu().numpy()
+        assert np.array_equal(got[:, :Ks].astype(np.float64), ref_un[:, act["sel"]])
+        assert not got[:, Ks:].any()
 
     # A6 on the sampled rows; every other row of h is exactly zero
     rows = np.concatenate([np.arange(offs_np[e], offs_np[e + 1]) for e in S])
