@@ -72,6 +72,17 @@ __device__ int block_exclusive_scan(int v, int *sh /* 1024 + 32 ints */, int &to
 constexpr int kSelThreads = 256;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kSelMaxK = 16384;
+constexpr int kSelBuckets = 2304;        // 11-bit keys (0..2048), 9 per thread
+constexpr int kSelCand = 512;            // candidates ranked directly
+
+// Monotone 11-bit key of a score: 0 for 0, else 1 + 32 e + m with e the
+// position of the leading one and m the five bits below it.
+__device__ __forceinline__ int sel_key(uint64_t v) {
+  if (v == 0ull) return 0;
+  const int e = 63 - __clzll((long long)v);
+  const uint32_t m = e >= 5 ? (uint32_t)(v >> (e - 5)) & 31u : (uint32_t)(v << (5 - e)) & 31u;
+  return 1 + 32 * e + (int)m;
+}
 
 template <int PER>
 __device__ __forceinline__ void rac_select_body(const uint64_t *__restrict__ scores, int K, int Ks,
@@ -81,11 +92,17 @@ __device__ __forceinline__ void rac_select_body(const uint64_t *__restrict__ sco
   __shared__ uint32_t gt[16384 / 32], eq[16384 / 32];
   __shared__ int sh[1024 + 32];
   __shared__ uint64_t s_max[kSelWaves];
+  __shared__ int hist[kSelBuckets];
+  __shared__ uint64_t cand_s[kSelCand];
+  __shared__ int cand_i[kSelCand];
+  __shared__ int s_cut[4];                  // bucket, count above it, candidates
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int nw = (K + 31) / 32;
   uint64_t sv[PER];
   bool live[PER];
   uint64_t mx = 0ull;
+  for (int i = tid; i < kSelBuckets; i += kSelThreads) hist[i] = 0;
+  if (tid == 0) s_cut[2] = 0;
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int j = tid + kSelThreads * i;
@@ -96,6 +113,68 @@ __device__ __forceinline__ void rac_select_body(const uint64_t *__restrict__ sco
   for (int w = tid; w < nw; w += kSelThreads) {
     gt[w] = 0u;
     eq[w] = 0u;
+  }
+  // ---- fast path: histogram of 11-bit keys, the bucket b* holding the
+  // K_s-th largest score, and a direct ranking of b*'s channels (by score
+  // desc, index asc); taken if b* holds at most kSelCand channels
+  bool fast = false;
+  if (Ks > 0) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+      if (live[i]) atomicAdd(&hist[sel_key(sv[i])], 1);
+    __syncthreads();
+    // thread t sums keys [kSelBuckets - 9 (t + 1), kSelBuckets - 9 t), top down
+    const int hi = kSelBuckets - 9 * tid;
+    int c = 0;
+#pragma unroll
+    for (int q = 1; q <= 9; ++q) c += hist[hi - q];
+    int tot;
+    int above = block_exclusive_scan(c, sh, tot);
+    if (above < Ks && above + c >= Ks) {
+      for (int q = 1; q <= 9; ++q) {
+        const int h = hist[hi - q];
+        if (above + h >= Ks) {
+          s_cut[0] = hi - q;
+          s_cut[1] = above;
+          break;
+        }
+        above += h;
+      }
+    }
+    __syncthreads();
+    const int bstar = s_cut[0];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (live[i] && sel_key(sv[i]) == bstar) {
+        const int slot = atomicAdd(&s_cut[2], 1);
+        if (slot < kSelCand) {
+          cand_s[slot] = sv[i];
+          cand_i[slot] = tid + kSelThreads * i;
+        }
+      }
+    }
+    __syncthreads();
+    const int nc = s_cut[2];
+    fast = nc <= kSelCand;
+    if (fast) {
+      const int need = Ks - s_cut[1];          // channels to take from b*
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int j = tid + kSelThreads * i;
+        if (live[i] && sel_key(sv[i]) > bstar) atomicOr(&gt[j >> 5], 1u << (j & 31));
+      }
+      for (int q = tid; q < nc; q += kSelThreads) {
+        const uint64_t v = cand_s[q];
+        const int jq = cand_i[q];
+        int r = 0;
+        for (int o = 0; o < nc; ++o) {
+          const uint64_t u = cand_s[o];
+          r += (u > v) || (u == v && cand_i[o] < jq);
+        }
+        if (r < need) atomicOr(&gt[jq >> 5], 1u << (jq & 31));
+      }
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -110,7 +189,7 @@ __device__ __forceinline__ void rac_select_body(const uint64_t *__restrict__ sco
   // theta = the K_s-th largest score; every wave tracks (prefix, remaining)
   uint64_t pre = 0ull, msk = 0ull;
   int rem = Ks;
-  if (Ks > 0 && mx != 0ull) {
+  if (!fast && Ks > 0 && mx != 0ull) {
     const int top = (63 - __clzll((long long)mx)) >> 2;
     for (int d = top, par = 0; d >= 0; --d, par ^= 1) {
       // per-lane digit counts packed as 16-bit fields: digit q lives in
@@ -158,8 +237,8 @@ __device__ __forceinline__ void rac_select_body(const uint64_t *__restrict__ sco
     }
   }
   const uint64_t theta = pre;
-  const int take_eq = Ks > 0 ? rem : 0;    // channels equal to theta to keep
-  if (Ks > 0) {
+  const int take_eq = (Ks > 0 && !fast) ? rem : 0;   // channels equal to theta to keep
+  if (Ks > 0 && !fast) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int j = tid + kSelThreads * i;

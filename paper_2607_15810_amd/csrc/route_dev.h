@@ -29,11 +29,65 @@ __device__ __forceinline__ bool better(float v1, int e1, float v2, int e2) {
   return v1 > v2 || (v1 == v2 && e1 < e2);
 }
 
-// One wavefront per token, four tokens per workgroup (workgroup index bid).
+// Top-k for E <= 256 experts, one wavefront per token, four tokens per
+// workgroup: the token's logits go to LDS and every lane ranks its experts
+// against all E of them (rank = how many experts come first in (value desc,
+// index asc)); an expert of rank r < k is slot r.  No serial rounds.
+constexpr int kRankMaxE = 256;
+__device__ __forceinline__ void route_topk_rank_body(int bid, const float *__restrict__ logits,
+                                                     int64_t T, int E, int k, int renorm,
+                                                     int32_t *__restrict__ ids,
+                                                     float *__restrict__ wts) {
+  __shared__ __align__(16) float lv[4][kRankMaxE];
+  __shared__ float slot_v[4][kMaxK];
+  __shared__ int slot_e[4][kMaxK];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int64_t t = (int64_t)bid * 4 + wid;
+  const bool ok = t < T;
+  for (int e = lane; e < E; e += 64) lv[wid][e] = ok ? logits[t * E + e] : 0.0f;
+  __syncthreads();
+  for (int e = lane; e < E; e += 64) {
+    const float v = lv[wid][e];
+    int r = 0;
+#pragma unroll 8
+    for (int i = 0; i < E; i += 4) {
+      const float4 u = *reinterpret_cast<const float4 *>(&lv[wid][i]);
+      r += (u.x > v || (u.x == v && i < e)) + (u.y > v || (u.y == v && i + 1 < e)) +
+           (u.z > v || (u.z == v && i + 2 < e)) + (u.w > v || (u.w == v && i + 3 < e));
+    }
+    if (r < k) {
+      slot_v[wid][r] = v;
+      slot_e[wid][r] = e;
+    }
+  }
+  __syncthreads();
+  if (!ok) return;
+  const float top_v = slot_v[wid][0];
+  float denom = 0.0f;
+  if (renorm) {
+    for (int s = 0; s < k; ++s) denom += expf(slot_v[wid][s] - top_v);   // slot order 0..k-1
+  } else {                 // full softmax denominator over all E experts
+    float part = 0.0f;
+    for (int e = lane; e < E; e += 64) part += expf(lv[wid][e] - top_v);
+    for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
+    denom = part;
+  }
+  if (lane < k) {
+    ids[t * k + lane] = slot_e[wid][lane];
+    wts[t * k + lane] = expf(slot_v[wid][lane] - top_v) / denom;
+  }
+}
+
+// One wavefront per token, four tokens per workgroup (workgroup index bid):
+// k rounds of a wave-wide arg-max (any E up to kMaxE).
 __device__ __forceinline__ void route_topk_body(int bid, const float *__restrict__ logits,
                                                 int64_t T, int E, int k, int renorm,
                                                 int32_t *__restrict__ ids,
                                                 float *__restrict__ wts) {
+  if (E <= kRankMaxE && (E & 3) == 0) {
+    route_topk_rank_body(bid, logits, T, E, k, renorm, ids, wts);
+    return;
+  }
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int64_t t = (int64_t)bid * 4 + wid;
   if (t >= T) return;
