@@ -221,7 +221,7 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
                                                qdh::align_up((size_t)nr * E * 4));
   float *part = reinterpret_cast<float *>(b + L.q1_ws);
   uint32_t *bitmap = reinterpret_cast<uint32_t *>(b + L.sel_ws);
-  const int ntopk = (int)((T + 3) / 4);
+  const int ntopk = qdr::topk_groups(T, E);
   const int64_t n16 = T * H / 16;
   const int ga = qdq::amax_grid(n16);
   int gx, gy;

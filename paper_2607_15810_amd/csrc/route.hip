@@ -62,7 +62,7 @@ extern "C" qd_status moe_route_permute(const float *logits, int64_t T, int32_t E
   int32_t *counts = static_cast<int32_t *>(ws);
   int32_t *ranks = reinterpret_cast<int32_t *>(static_cast<char *>(ws) +
                                                qdh::align_up((size_t)nblk * E * 4));
-  hipLaunchKernelGGL(route_topk_kernel, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, s, logits,
+  hipLaunchKernelGGL(route_topk_kernel, dim3((unsigned)qdr::topk_groups(T, E)), dim3(256), 0, s, logits,
                      T, E, k, renorm, topk_ids, topk_w);
   hipLaunchKernelGGL(route_rank_kernel, dim3(nblk), dim3(256), 0, s, T, E, k, topk_ids, counts,
                      ranks);

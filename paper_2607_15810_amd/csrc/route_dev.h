@@ -5,8 +5,10 @@
 //
 // Three workgroup bodies (launched alone by route.hip, or fused with the
 // activation quantiser and the channel selection by the layer):
-//   route_topk_body      one wavefront per token: k rounds of a wave-wide
-//                        arg-max, then the softmax weights.
+//   route_topk_body      E <= 256: one workgroup per token, every expert's
+//                        rank counted in parallel, rank r < k is slot r;
+//                        larger E: one wavefront per token, k rounds of a
+//                        wave-wide arg-max.  Then the softmax weights.
 //   route_rank_body      per block of 256 tokens: expert bitmasks in LDS give
 //                        every (token, slot) its rank among the block's tokens
 //                        of the same expert, and per-block expert counts.
@@ -29,62 +31,99 @@ __device__ __forceinline__ bool better(float v1, int e1, float v2, int e2) {
   return v1 > v2 || (v1 == v2 && e1 < e2);
 }
 
-// Top-k for E <= 256 experts, one wavefront per token, four tokens per
-// workgroup: the token's logits go to LDS and every lane ranks its experts
-// against all E of them (rank = how many experts come first in (value desc,
-// index asc)); an expert of rank r < k is slot r.  No serial rounds.
+// Top-k for E <= 256 experts, one workgroup per token: lane l of every wave
+// holds experts l, l + 64, ...; wave w broadcasts experts l + 64 j with
+// l in [16 w, 16 w + 16) in turn from their lanes and counts, for each of its
+// lane's experts, how many of those come first in (value desc, index asc);
+// the four partial counts summed in LDS give each expert's rank, and rank
+// r < k is slot r.  No serial reduction rounds.
 constexpr int kRankMaxE = 256;
 __device__ __forceinline__ void route_topk_rank_body(int bid, const float *__restrict__ logits,
                                                      int64_t T, int E, int k, int renorm,
                                                      int32_t *__restrict__ ids,
                                                      float *__restrict__ wts) {
-  __shared__ __align__(16) float lv[4][kRankMaxE];
-  __shared__ float slot_v[4][kMaxK];
-  __shared__ int slot_e[4][kMaxK];
+  __shared__ int rk[kRankMaxE];
+  __shared__ float slot_v[kMaxK];
+  __shared__ int slot_e[kMaxK];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int64_t t = (int64_t)bid * 4 + wid;
-  const bool ok = t < T;
-  for (int e = lane; e < E; e += 64) lv[wid][e] = ok ? logits[t * E + e] : 0.0f;
-  __syncthreads();
-  for (int e = lane; e < E; e += 64) {
-    const float v = lv[wid][e];
-    int r = 0;
-#pragma unroll 8
-    for (int i = 0; i < E; i += 4) {
-      const float4 u = *reinterpret_cast<const float4 *>(&lv[wid][i]);
-      r += (u.x > v || (u.x == v && i < e)) + (u.y > v || (u.y == v && i + 1 < e)) +
-           (u.z > v || (u.z == v && i + 2 < e)) + (u.w > v || (u.w == v && i + 3 < e));
-    }
-    if (r < k) {
-      slot_v[wid][r] = v;
-      slot_e[wid][r] = e;
+  const int64_t t = bid;
+  if (t >= T) return;                           // whole workgroup
+  const int per = (E + 63) >> 6;                // <= 4, uniform
+  for (int e = threadIdx.x; e < E; e += blockDim.x) rk[e] = 0;
+  float v[4];
+  int r[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + 64 * j;
+    v[j] = (j < per && e < E) ? logits[t * E + e] : 0.0f;
+    r[j] = 0;
+  }
+#pragma unroll
+  for (int j2 = 0; j2 < 4; ++j2) {
+    if (j2 >= per) break;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int i = 16 * wid + q;
+      const int e2 = i + 64 * j2;
+      const float u = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[j2]), i));
+      const bool v2 = e2 < E;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int e = lane + 64 * j;
+        r[j] += (v2 && (u > v[j] || (u == v[j] && e2 < e))) ? 1 : 0;
+      }
     }
   }
   __syncthreads();
-  if (!ok) return;
-  const float top_v = slot_v[wid][0];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + 64 * j;
+    if (j < per && e < E) atomicAdd(&rk[e], r[j]);
+  }
+  __syncthreads();
+  if (wid == 0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = lane + 64 * j;
+      if (j < per && e < E && rk[e] < k) {
+        slot_v[rk[e]] = v[j];
+        slot_e[rk[e]] = e;
+      }
+    }
+  }
+  __syncthreads();
+  if (wid != 0) return;
+  const float top_v = slot_v[0];
   float denom = 0.0f;
   if (renorm) {
-    for (int s = 0; s < k; ++s) denom += expf(slot_v[wid][s] - top_v);   // slot order 0..k-1
+    for (int s = 0; s < k; ++s) denom += expf(slot_v[s] - top_v);   // slot order 0..k-1
   } else {                 // full softmax denominator over all E experts
     float part = 0.0f;
-    for (int e = lane; e < E; e += 64) part += expf(lv[wid][e] - top_v);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (j < per && lane + 64 * j < E) part += expf(v[j] - top_v);
     for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
     denom = part;
   }
   if (lane < k) {
-    ids[t * k + lane] = slot_e[wid][lane];
-    wts[t * k + lane] = expf(slot_v[wid][lane] - top_v) / denom;
+    ids[t * k + lane] = slot_e[lane];
+    wts[t * k + lane] = expf(slot_v[lane] - top_v) / denom;
   }
 }
 
-// One wavefront per token, four tokens per workgroup (workgroup index bid):
-// k rounds of a wave-wide arg-max (any E up to kMaxE).
+// workgroups the top-k step needs for T tokens and E experts
+inline int topk_groups(int64_t T, int E) {
+  return (int)(E <= kRankMaxE ? T : (T + 3) / 4);
+}
+
+// E <= 256: the rank body above.  Otherwise one wavefront per token, four
+// tokens per workgroup (workgroup index bid): k rounds of a wave-wide arg-max
+// (any E up to kMaxE).
 __device__ __forceinline__ void route_topk_body(int bid, const float *__restrict__ logits,
                                                 int64_t T, int E, int k, int renorm,
                                                 int32_t *__restrict__ ids,
                                                 float *__restrict__ wts) {
-  if (E <= kRankMaxE && (E & 3) == 0) {
+  if (E <= kRankMaxE) {
     route_topk_rank_body(bid, logits, T, E, k, renorm, ids, wts);
     return;
   }
