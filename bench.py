@@ -231,7 +231,8 @@ def main():
 
     def clone_bank(b):
         return ops.NVFP4Tensor(b.codes.clone(), b.scales.clone(), b.gscale.clone(), b.groups,
-                               b.rows, b.cols)
+                               b.rows, b.cols,
+                               b.scales_frag.clone() if b.scales_frag is not None else None)
 
     copies = max(1, args.copies)
     banks = [(w13_0, w2_0)] + [(clone_bank(w13_0), clone_bank(w2_0)) for _ in range(copies - 1)]

@@ -57,19 +57,24 @@ typedef int qd_status;
 
 /*
  * An NVFP4 tensor: `groups` matrices of [rows][cols].  The struct itself is
- * host memory; the three arrays are device memory owned by the caller.
+ * host memory; the arrays are device memory owned by the caller.
  *   codes  : uint8 [groups][rows][cols/2]; element 2i of a row in bits 3:0,
  *            element 2i+1 in bits 7:4; a code is sign<<3 | E2M1 magnitude
  *            index (magnitudes 0, .5, 1, 1.5, 2, 3, 4, 6).
  *   scales : uint8 [groups][rows][cols/16]; E4M3FN bit patterns, sign 0.
  *   gscale : float [groups][2] = {s_enc, s_dec}, the FP32 tensor scale pair.
  * Element value: e2m1(code) * e4m3(scale) * s_dec.
+ *   scales_frag : optional second copy of the scales of a weight tensor,
+ *            laid out for the grouped GEMM's kernel for few rows per expert
+ *            (see nvfp4_pack_frag_scales); NULL everywhere else.
  */
 typedef struct {
   uint8_t *codes;
   uint8_t *scales;
   float   *gscale;
   int64_t  groups, rows, cols;
+  uint8_t *scales_frag;   /* optional, weights only: NULL, or the same scales
+                             in fragment order (nvfp4_pack_frag_scales) */
 } qd_nvfp4;
 
 const char *qd_status_string(qd_status s);
@@ -205,7 +210,8 @@ qd_status rac_residual_gemm(const qd_nvfp4 *rq, const int32_t *sel_idx, int32_t 
  *   row_token       : int32 [rows] gather map (NULL: row r reads a row r).
  *   expert_offsets  : int32 [E+1] row ranges per expert (NULL: E must be 1).
  *   rows            : number of grouped rows (T*k for the MoE layer).
- *   w               : E groups of [N][K].
+ *   w               : E groups of [N][K]; w->scales_frag (optional) is
+ *                     read by the kernel for few rows per expert.
  *   rq, sel_idx, Ks : the masked residual (NULL / 0: plain W4A4; Ks > 0
  *                     needs rq).
  *   rq_sel          : rac_gather_selected(rq, sel_idx, Ks) (f16, 16-byte
@@ -229,6 +235,25 @@ qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
                                 const int32_t *sel_idx, int32_t Ks, const void *rq_sel,
                                 int32_t epilogue, void *out, float *amax_partials,
                                 void *stream);
+
+/* ---------------------------------------------------------------------
+ * nvfp4_pack_frag_scales -- a load-time re-layout of a weight tensor's
+ * scales for the W4A4 expert GEMM of Sec. 3.3 on decode-shaped batches.
+ * That kernel streams each 16-row block of weights over K in chunks of 256
+ * elements; in the standard layout the 16 scale bytes a row needs per chunk
+ * lie 16 bytes apart in every row's scale line, in this one the 256 bytes of
+ * a block and chunk are contiguous, in the order the kernel's lanes take
+ * them.  Values are not touched.
+ *   w   : weights, groups E of [rows][cols]; rows % 16 == 0,
+ *         cols % 256 == 0 (otherwise QD_ERR_SHAPE).
+ *   out : uint8 [E][rows/16][cols/256][4][16][4] (16-byte aligned,
+ *         nvfp4_frag_scales_bytes(E, rows, cols) bytes), where
+ *         out[e][f][c][g][l][b] = scales[e][16 f + l][16 c + 4 g + b].
+ * Set w->scales_frag = out afterwards; moe_w4a4_grouped_gemm and
+ * qd_moe_layer_forward then read it instead of w->scales where it pays.
+ * ------------------------------------------------------------------- */
+int64_t   nvfp4_frag_scales_bytes(int64_t groups, int64_t rows, int64_t cols);
+qd_status nvfp4_pack_frag_scales(const qd_nvfp4 *w, uint8_t *out, void *stream);
 
 /* ---------------------------------------------------------------------
  * moe_unpermute_combine -- weighted sum of the k expert outputs per token:

@@ -35,6 +35,7 @@ struct GemmArgs {
   int64_t rows;
   const uint8_t *w_codes;
   const uint8_t *w_scales;
+  const uint8_t *w_sfrag;  // optional: the weight scales in fragment order
   const float *w_gs;
   int N;
   int K;
@@ -275,22 +276,30 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs p) {
 //    units are ordered expert-major, so a workgroup mostly stays on one
 //    expert.
 //  * Eight waves, 32 weight rows each.  A wave streams its rows through a
-//    private LDS ring of NS stages with direct global->LDS loads: in-flight
+//    private two-stage LDS ring with direct global->LDS loads: in-flight
 //    weights cost no registers.  One stage is 256 K-elements of 32 rows
-//    (4 KB of codes, 512 B of scales).
-//  * The 32 activation rows of the pass (with RAC also their masked
-//    residual rows) go through a four-slot LDS ring filled the same way
-//    and shared by the waves; each wave decodes the fragments it needs.
-//  * Loads are issued in one fixed order per iteration: the activations,
-//    then the weights of the stage three ahead, spread over the k-steps.
-//    Loads complete in issue order, so one explicit "vmcnt <= 16" at the
-//    top of each iteration proves that both have landed for the stage in
-//    hand while the next two stages stay in flight.  Loads past the last
-//    stage repeat the last stage's addresses into slots that are never
-//    read again.
-//  * Operands are decoded exactly to f16 in registers (see the top of this
-//    file) and multiplied on MFMA, with straight-line code for each number
-//    of valid 16-row m-tiles.
+//    (4 KB of codes, 512 B of scales; the scales from the fragment-ordered
+//    copy when the caller provides it, one contiguous 256-byte piece per
+//    fragment and stage).
+//  * Activations are decoded once per workgroup, not once per wave: waves
+//    0..3 each load one quarter of a stage's 32 activation rows (lane group
+//    g's 64 elements of every row, with their scale dword) into a private
+//    raw slot, decode it exactly to f16 one stage ahead and write it into a
+//    shared two-slot f16 panel, laid out as the MFMA's A fragments; every
+//    wave then reads its fragments from the panel.  With RAC, waves 4..7
+//    load the masked residual rows into a four-slot ring shared by the waves,
+//    which decode them at the k-steps that hold a selected channel.
+//  * Loads are issued in one fixed order per iteration: the activations of
+//    the stage three ahead, then the weights of the stage two ahead, spread
+//    over the k-steps.  Loads complete in issue order, so one explicit wait
+//    at the top of iteration s (at most one iteration's loads outstanding)
+//    proves that the wave's weights of stage s and its activations of stage
+//    s + 1 have landed; the barrier after it publishes the panel of stage s
+//    and everyone's residual rows.  Loads past the last stage repeat the
+//    last stage's addresses into slots that are never read again.
+//  * Weight operands are decoded exactly to f16 in registers (see the top of
+//    this file) and multiplied on MFMA, with straight-line code for each
+//    number of valid 16-row m-tiles.
 //  * RAC: the masked residual is zero outside the selected channels S, so
 //    its contraction with the weights runs over the same decoded weight
 //    fragments, restricted to the k-steps that contain a channel of S (a
@@ -304,30 +313,35 @@ constexpr int SK_WAVES = 8;
 constexpr int SK_THREADS = 64 * SK_WAVES;
 constexpr int SK_ROWS = 32 * SK_WAVES;   // weight rows per unit
 constexpr int SK_PR = 32;                // activation rows per pass
+constexpr int SK_NS = 2;                 // weight ring depth
 constexpr int SK_BSTAGE = 4608;          // bytes per wave and weight stage
-constexpr int SK_ASRC = SK_PR * 144;     // raw activation stage of one source
-constexpr int SK_NA = 4;                 // activation slots
+constexpr int SK_ASRC = SK_PR * 144;     // raw residual stage (codes + scales)
+constexpr int SK_NR = 4;                 // residual slots
+constexpr int SK_NX = 3;                 // raw activation slots per decoding wave
+constexpr int SK_XRAW = 1280;            // one decoding wave's raw stage: 1 KB codes, 256 B scales
+constexpr int SK_PANEL = SK_PR * 256 * 2;   // one f16 panel stage
 constexpr int SK_KMAX = 65536;
 constexpr int SK_EMAX = 512;             // experts (offsets and their scan kept in LDS)
 constexpr int SK_LDS_MAX = 160 * 1024;
 constexpr int SK_GRID = 256;             // one workgroup per CU
 
 struct SkLayout {
-  int b, a, junk, offs, pu, sw, smask, red, total;
+  int b, pan, xraw, rraw, junk, offs, pu, sw, smask, red, total;
 };
 
-// nsrc = 1 (activations) or 2 (activations and masked residual)
-__host__ __device__ inline SkLayout sk_layout(int K, int E, int nsrc, int ns) {
+__host__ __device__ inline SkLayout sk_layout(int K, int E, bool rac) {
   SkLayout L{};
   int o = 0;
   auto take = [&](int bytes) { int at = o; o += (bytes + 15) & ~15; return at; };
-  L.b = take(SK_WAVES * ns * SK_BSTAGE);
-  L.a = take(SK_NA * nsrc * SK_ASRC);
+  L.b = take(SK_WAVES * SK_NS * SK_BSTAGE);
+  L.pan = take(2 * SK_PANEL);
+  L.xraw = take(4 * SK_NX * SK_XRAW);
+  L.rraw = take(rac ? SK_NR * SK_ASRC : 0);
   L.junk = take(1024);
   L.offs = take((E + 1) * 4);
   L.pu = take((E + 1) * 4);
   L.sw = take(E * 4);
-  L.smask = take(nsrc > 1 ? (K >> 8) * 4 : 0);
+  L.smask = take(rac ? (K >> 8) * 4 : 0);
   L.red = take(16 * 4);
   L.total = o;
   return L;
@@ -385,54 +399,45 @@ struct BReg {
   u32x4 c00, c01, c10, c11;
   uint32_t s0, s1;
 };
-// Raw activation (and residual) data of one stage for MTV m-tiles, read
-// from the LDS slot in the same batch as the weights.
+// Raw masked-residual data of one stage for MTV m-tiles: the lane's 16 code
+// bytes per chunk and m-tile, and its scale dword.
 template <int MTV>
-struct ARaw {
-  uint4 x[2][MTV];      // [chunk][m-tile]: the lane's 16 code bytes
-  uint32_t xs[MTV];     // the lane's scale dword
-  uint4 r[2][MTV];      // the same for the residual
+struct RRaw {
+  uint4 r[2][MTV];
   uint32_t rs[MTV];
 };
-template <bool RAC, int MTV>
-__device__ __forceinline__ void load_araw(ARaw<MTV> &a, const unsigned char *asl, bool res,
-                                          int lane) {
+template <int MTV>
+__device__ __forceinline__ void load_rraw(RRaw<MTV> &a, const unsigned char *rsl, int lane) {
   const int lr = lane & 15, g = lane >> 4;
 #pragma unroll
   for (int i = 0; i < MTV; ++i) {
     const int rr = i * 16 + lr;
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2)
-      a.x[c2][i] = *reinterpret_cast<const uint4 *>(asl + ((c2 * 4 + g) * SK_PR + rr) * 16);
-    a.xs[i] = *reinterpret_cast<const uint32_t *>(asl + 4096 + (g * SK_PR + rr) * 4);
-    if (RAC && res) {
-      const unsigned char *rsl = asl + SK_ASRC;
-#pragma unroll
-      for (int c2 = 0; c2 < 2; ++c2)
-        a.r[c2][i] = *reinterpret_cast<const uint4 *>(rsl + ((c2 * 4 + g) * SK_PR + rr) * 16);
-      a.rs[i] = *reinterpret_cast<const uint32_t *>(rsl + 4096 + (g * SK_PR + rr) * 4);
-    }
+      a.r[c2][i] = *reinterpret_cast<const uint4 *>(rsl + ((c2 * 4 + g) * SK_PR + rr) * 16);
+    a.rs[i] = *reinterpret_cast<const uint32_t *>(rsl + 4096 + (g * SK_PR + rr) * 4);
   }
 }
 
-// One stage's MFMA work for MTV valid m-tiles, all operands decoded to f16
-// from registers.  hook(k) runs before k-step k (0..7): the caller issues
-// its loads for later stages there, spread over the stage.
+// One stage's MFMA work for MTV valid m-tiles.  pan points at the lane's A
+// fragment of k-step 0, m-tile 0 in the stage's f16 panel (k-step (c, s) is
+// 2048 (4c + s) bytes further, m-tile i 256 i).  hook(k) runs before k-step
+// k (0..7): the caller issues its loads for later stages there and decodes
+// the next panel.
 template <bool RAC, int MTV, typename Hook>
-__device__ __forceinline__ void sk_stage(const BReg &b, const ARaw<MTV> &a, uint32_t sm,
-                                         f32x4 (&acc)[2][2], f32x4 (&accr)[2][2], Hook &&hook) {
+__device__ __forceinline__ void sk_stage(const BReg &b, const unsigned char *pan,
+                                         const RRaw<MTV> &a, uint32_t sm, f32x4 (&acc)[2][2],
+                                         f32x4 (&accr)[2][2], Hook &&hook) {
 #pragma unroll
   for (int c2 = 0; c2 < 2; ++c2) {
     const u32x4 bv0 = c2 ? b.c01 : b.c00;
     const u32x4 bv1 = c2 ? b.c11 : b.c10;
     const f16x2 sp0 = scale_pair_of(b.s0, c2), sp1 = scale_pair_of(b.s1, c2);
-    f16x2 ap[MTV], rp[MTV];
+    f16x2 rp[MTV];
     const bool rchunk = RAC && ((sm >> (4 * c2)) & 15u) != 0u;
 #pragma unroll
-    for (int i = 0; i < MTV; ++i) {
-      ap[i] = scale_pair_of(a.xs[i], c2);
+    for (int i = 0; i < MTV; ++i)
       if (rchunk) rp[i] = scale_pair_of(a.rs[i], c2);
-    }
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       hook(c2 * 4 + s);
@@ -440,7 +445,8 @@ __device__ __forceinline__ void sk_stage(const BReg &b, const ARaw<MTV> &a, uint
       const f16x8 bf1 = decode8_sel(bv1[s], sp1, s >= 2);
 #pragma unroll
       for (int i = 0; i < MTV; ++i) {
-        const f16x8 af = decode8_sel(word_of(a.x[c2][i], s), ap[i], s >= 2);
+        const f16x8 af =
+            *reinterpret_cast<const f16x8 *>(pan + (c2 * 4 + s) * 2048 + i * 256);
         acc[i][0] = mfma16(af, bf0, acc[i][0]);
         acc[i][1] = mfma16(af, bf1, acc[i][1]);
       }
@@ -456,16 +462,30 @@ __device__ __forceinline__ void sk_stage(const BReg &b, const ARaw<MTV> &a, uint
   }
 }
 
-template <bool GATHER, bool RAC, int EPI, int NS>
+// A decoding wave (lane group g = wave index) turns its raw slot -- lane
+// (row l % 32, chunk l / 32): 16 code bytes at 16 l, the row's scale dword
+// at 1024 + 4 (l % 32) -- into its part of an f16 panel stage, where the A
+// fragment of k-step (c, s), lane group g, row r sits at
+// 2048 (4c + s) + 512 g + 16 r.
+__device__ __forceinline__ void sk_decode_panel(const unsigned char *xr, unsigned char *pw,
+                                                int lane) {
+  const uint4 cw = *reinterpret_cast<const uint4 *>(xr + lane * 16);
+  const uint32_t sdw = *reinterpret_cast<const uint32_t *>(xr + 1024 + (lane & 31) * 4);
+  const f16x2 sp = scale_pair_of(sdw, lane >> 5);
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    *reinterpret_cast<f16x8 *>(pw + s * 2048) = decode8_sel(word_of(cw, s), sp, s >= 2);
+}
+
+template <bool GATHER, bool RAC, int EPI>
 __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int nblk) {
-  constexpr int NSRC = RAC ? 2 : 1;
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, g = lane >> 4;
   const int K = p.K, N = p.N, E = p.E;
   const int64_t kb2 = K >> 1, kb16 = K >> 4;
-  const SkLayout L = sk_layout(K, E, NSRC, NS);
+  const SkLayout L = sk_layout(K, E, RAC);
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   int32_t *offs = reinterpret_cast<int32_t *>(lds + L.offs);
   int32_t *pu = reinterpret_cast<int32_t *>(lds + L.pu);
@@ -529,36 +549,58 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     // ---- issue cursors and their per-lane addresses
     SkCur ca = cc, cb = cc;
     const uint8_t *bc0, *bc1, *bs0, *bs1;
+    // weight scales: the standard layout (16 bytes per row and stage, in
+    // every row's scale line) or the fragment-ordered copy (256 contiguous
+    // bytes per 16-row fragment and stage, one dword per lane in lane order)
+    const int sstep = p.w_sfrag ? 256 : 16;
     auto bind_b = [&](const SkCur &c) {
       int64_t r0, r1;
+      // the wave's two 16-row fragments (all rows of a fragment are valid
+      // or none, N and I being multiples of 16; invalid ones read row 0)
+      int64_t f0, f1;
       if (EPI == QD_EPI_SWIGLU) {
         const int I = N >> 1;
         const int pr_ = c.nb * (SK_ROWS / 2) + w * 16 + lr;
         r0 = pr_ < I ? pr_ : 0;
         r1 = pr_ < I ? pr_ + I : 0;
+        const int fr = c.nb * (SK_ROWS / 32) + w;
+        f0 = 16 * fr < I ? fr : 0;
+        f1 = 16 * fr < I ? fr + (I >> 4) : 0;
       } else {
         const int r = c.nb * SK_ROWS + w * 32 + lr;
         r0 = r < N ? r : 0;
         r1 = r + 16 < N ? r + 16 : 0;
+        const int fr = c.nb * (SK_ROWS / 16) + 2 * w;
+        f0 = 16 * fr < N ? fr : 0;
+        f1 = 16 * (fr + 1) < N ? fr + 1 : 0;
       }
       r0 += (int64_t)c.e * N;
       r1 += (int64_t)c.e * N;
       bc0 = p.w_codes + r0 * kb2 + g * 32;
       bc1 = p.w_codes + r1 * kb2 + g * 32;
-      bs0 = p.w_scales + r0 * kb16 + g * 4;
-      bs1 = p.w_scales + r1 * kb16 + g * 4;
+      if (p.w_sfrag) {
+        const int64_t nf = N >> 4;
+        bs0 = p.w_sfrag + (((int64_t)c.e * nf + f0) * niter) * 256 + lane * 4;
+        bs1 = p.w_sfrag + (((int64_t)c.e * nf + f1) * niter) * 256 + lane * 4;
+      } else {
+        bs0 = p.w_scales + r0 * kb16 + g * 4;
+        bs1 = p.w_scales + r1 * kb16 + g * 4;
+      }
     };
-    // activations: a raw slot holds per source [codes: column block b =
-    // 4 * chunk + lane group, 32 rows x 16 B each][scales: lane group,
-    // 32 rows x 4 B].  Waves 0..3 load the codes of x (two column blocks
-    // each), waves 4..7 those of the residual; waves 0, 1 load the scales
-    // of x, waves 2, 3 those of the residual; spare loads go to a junk area.
+    // activations.  Waves 0..3 (decoders, lane group g = w) load lane
+    // (row l % 32, chunk l / 32)'s 16 code bytes and the row's scale dword
+    // of x into their private raw slot.  With RAC waves 4..7 load the
+    // masked residual into the shared ring: codes by column block b = 4 *
+    // chunk + lane group, 32 rows x 16 B each (two blocks per wave), scales
+    // by lane group, 32 rows x 4 B (waves 4, 5; waves 6, 7 load theirs into
+    // a junk area).  Without RAC waves 4..7 load no activations.
+    const bool dec = w < 4;
+    const bool has_a = dec || RAC;
     const int a_row = lane & 31;
     const int a_blk = 2 * (w & 3) + (lane >> 5);
-    const int a_cb = (a_blk & 3) * 32 + (a_blk >> 2) * 16;
-    const int a_sb = (2 * (w & 1) + (lane >> 5)) * 4;
-    const bool c_res = w >= 4, s_res = (w & 2) != 0;
-    const bool c_live = RAC || !c_res, s_live = w < (RAC ? 4 : 2);
+    const int64_t a_cb = dec ? 32 * w + 16 * (lane >> 5) : (a_blk & 3) * 32 + (a_blk >> 2) * 16;
+    const int64_t a_sb = dec ? 4 * w : (2 * (w & 1) + (lane >> 5)) * 4;
+    const bool s_live = dec || w < 6;
     const uint8_t *ac, *as;
     int a_e = -1, a_p = -1;
     auto bind_a = [&](const SkCur &c) {
@@ -568,27 +610,34 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
       int64_t r = (int64_t)c.ob + (int64_t)c.p * SK_PR + a_row;
       r = min(r, (int64_t)c.ob + c.rows - 1);
       const int64_t src = GATHER ? (int64_t)p.row_token[r] : r;
-      ac = (RAC && c_res ? p.r_codes : p.a_codes) + src * kb2 + a_cb;
-      as = (RAC && s_res ? p.r_scales : p.a_scales) + src * kb16 + a_sb;
+      ac = (dec ? p.a_codes : p.r_codes) + src * kb2 + a_cb;
+      as = (dec ? p.a_scales : p.r_scales) + src * kb16 + a_sb;
     };
-    const uint32_t bring = lds0 + L.b + w * NS * SK_BSTAGE;
+    const uint32_t bring = lds0 + L.b + w * SK_NS * SK_BSTAGE;
     const uint32_t junk = lds0 + L.junk;
+    // LDS destinations of the activation loads of stage sg
+    auto a_cdst = [&](int sg) -> uint32_t {
+      return dec ? lds0 + L.xraw + (w * SK_NX + sg % SK_NX) * SK_XRAW
+                 : lds0 + L.rraw + (sg % SK_NR) * SK_ASRC + (w & 3) * 1024;
+    };
+    auto a_sdst = [&](int sg) -> uint32_t {
+      return dec ? lds0 + L.xraw + (w * SK_NX + sg % SK_NX) * SK_XRAW + 1024
+                 : (s_live ? lds0 + L.rraw + (sg % SK_NR) * SK_ASRC + 4096 + (w & 1) * 256
+                           : junk);
+    };
+    auto issue_a = [&](int sg) {
+      dma16(ac + ca.it * 128, uni(a_cdst(sg)));
+      dma4(as + ca.it * 16, uni(a_sdst(sg)));
+    };
     auto issue_b = [&](int sg) {
-      const uint32_t slot = uni(bring + (sg % NS) * SK_BSTAGE);
+      const uint32_t slot = uni(bring + (sg % SK_NS) * SK_BSTAGE);
       const int off = cb.it * 128;
       dma16(bc0 + off, slot);
       dma16(bc0 + off + 16, slot + 1024);
       dma16(bc1 + off, slot + 2048);
       dma16(bc1 + off + 16, slot + 3072);
-      dma4(bs0 + cb.it * 16, slot + 4096);
-      dma4(bs1 + cb.it * 16, slot + 4096 + 256);
-    };
-    auto issue_a = [&](int sg) {
-      const uint32_t slot = lds0 + L.a + (sg % SK_NA) * (NSRC * SK_ASRC);
-      const uint32_t cdst = slot + (c_res ? SK_ASRC : 0) + (w & 3) * 1024;
-      const uint32_t sdst = slot + (s_res ? SK_ASRC : 0) + 4096 + (w & 1) * 256;
-      dma16(ac + ca.it * 128, uni(c_live ? cdst : junk));
-      dma4(as + ca.it * 16, uni(s_live ? sdst : junk));
+      dma4(bs0 + cb.it * sstep, slot + 4096);
+      dma4(bs1 + cb.it * sstep, slot + 4096 + 256);
     };
     auto adv_b = [&]() {
       const int e = cb.e, nb = cb.nb;
@@ -597,16 +646,35 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     auto adv_a = [&]() {
       if (S.next(ca)) bind_a(ca);
     };
+    // the panel slot of stage sg, seen from this lane as a decoder (write)
+    // and as a reader (its A fragment of k-step 0, m-tile 0)
+    auto pan_w = [&](int sg) {
+      return lds + L.pan + (sg & 1) * SK_PANEL + (lane >> 5) * 8192 + w * 512 + (lane & 31) * 16;
+    };
+    auto pan_r = [&](int sg) {
+      return lds + L.pan + (sg & 1) * SK_PANEL + g * 512 + lr * 16;
+    };
 
-    // ---- prologue: the steady-state issue order for the virtual
-    // iterations -3 .. -1 (activations, then weights, of stage i + 3)
+    // ---- prologue: activations of stages 0, 1, 2 and weights of stages
+    // 0, 1 in the steady-state order (A0 | A1 B0 | A2 B1), then the panel of
+    // stage 0
     bind_b(cb);
     bind_a(ca);
-    for (int i = 0; i < 3; ++i) {
-      issue_a(i);
+    if (has_a) {
+      issue_a(0);
       adv_a();
+    }
+    for (int i = 0; i < 2; ++i) {
+      if (has_a) {
+        issue_a(i + 1);
+        adv_a();
+      }
       issue_b(i);
       adv_b();
+    }
+    if (dec) {
+      wait_vm<16>();         // this wave's activations of stage 0
+      sk_decode_panel(lds + L.xraw + (w * SK_NX) * SK_XRAW, pan_w(0), lane);
     }
 
     f32x4 acc[2][2], accr[2][2];   // [m-tile][fragment]
@@ -621,11 +689,11 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     for (int sg = 0;; ++sg) {
       const int nrow = min(SK_PR, cc.rows - cc.p * SK_PR);
       const int mtv = nrow > 16 ? 2 : 1;
-      // after the weights of stage sg come the loads of stages sg + 1 and
-      // sg + 2: 2 x 8
-      wait_vm<16>();
-      __syncthreads();       // every wave's activations of stage sg have landed
-      const unsigned char *bsl = lds + L.b + (w * NS + sg % NS) * SK_BSTAGE;
+      // outstanding past this point: at most the last iteration's loads
+      // (activations of stage sg + 2, weights of stage sg + 1)
+      if (has_a) wait_vm<8>(); else wait_vm<6>();
+      __syncthreads();       // the panel of stage sg and all residual rows of sg have landed
+      const unsigned char *bsl = lds + L.b + (w * SK_NS + sg % SK_NS) * SK_BSTAGE;
       BReg b;
       b.c00 = *reinterpret_cast<const u32x4 *>(bsl + 0 * 1024 + lane * 16);
       b.c01 = *reinterpret_cast<const u32x4 *>(bsl + 1 * 1024 + lane * 16);
@@ -634,23 +702,22 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
       b.s0 = *reinterpret_cast<const uint32_t *>(bsl + 4096 + lane * 4);
       b.s1 = *reinterpret_cast<const uint32_t *>(bsl + 4096 + 256 + lane * 4);
       const uint32_t sm = RAC ? smask[cc.it] : 0u;
-      const unsigned char *asl = lds + L.a + (sg % SK_NA) * (NSRC * SK_ASRC);
-      // loads of stage sg + 3, one before each k-step: the activations into
-      // the slot every wave has finished with, then the weights into the
-      // slot just read
+      const unsigned char *rsl = lds + L.rraw + (sg % SK_NR) * SK_ASRC;
+      // before k-step 0 and 1: the activations of stage sg + 3; before k-step
+      // 2: the decode of stage sg + 1's panel; before k-steps 2..7: the
+      // weights of stage sg + 2 into the slot just read
       auto hook = [&](int k) {
         if (k < 2) {
-          const uint32_t slot = lds0 + L.a + ((sg + 3) % SK_NA) * (NSRC * SK_ASRC);
-          if (k == 0) {
-            const uint32_t cdst = slot + (c_res ? SK_ASRC : 0) + (w & 3) * 1024;
-            dma16(ac + ca.it * 128, uni(c_live ? cdst : junk));
-          } else {
-            const uint32_t sdst = slot + (s_res ? SK_ASRC : 0) + 4096 + (w & 1) * 256;
-            dma4(as + ca.it * 16, uni(s_live ? sdst : junk));
+          if (has_a) {
+            if (k == 0) dma16(ac + ca.it * 128, uni(a_cdst(sg + 3)));
+            else dma4(as + ca.it * 16, uni(a_sdst(sg + 3)));
           }
         } else {
-          const uint32_t slot = uni(bring + (sg % NS) * SK_BSTAGE);
-          const int off = cb.it * 128, soff = cb.it * 16;
+          if (k == 2 && dec)
+            sk_decode_panel(lds + L.xraw + (w * SK_NX + (sg + 1) % SK_NX) * SK_XRAW,
+                            pan_w(sg + 1), lane);
+          const uint32_t slot = uni(bring + (sg % SK_NS) * SK_BSTAGE);
+          const int off = cb.it * 128, soff = cb.it * sstep;
           if (k == 2) dma16(bc0 + off, slot);
           if (k == 3) dma16(bc0 + off + 16, slot + 1024);
           if (k == 4) dma16(bc1 + off, slot + 2048);
@@ -659,18 +726,19 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
           if (k == 7) dma4(bs1 + soff, slot + 4096 + 256);
         }
       };
+      const unsigned char *pr = pan_r(sg);
       if (mtv == 1) {
-        ARaw<1> a;
-        load_araw<RAC, 1>(a, asl, sm != 0u, lane);
+        RRaw<1> a;
+        if (RAC && sm != 0u) load_rraw<1>(a, rsl, lane);
         wait_lds();          // the weight slot may be refilled from here on
-        sk_stage<RAC, 1>(b, a, sm, acc, accr, hook);
+        sk_stage<RAC, 1>(b, pr, a, sm, acc, accr, hook);
       } else {
-        ARaw<2> a;
-        load_araw<RAC, 2>(a, asl, sm != 0u, lane);
+        RRaw<2> a;
+        if (RAC && sm != 0u) load_rraw<2>(a, rsl, lane);
         wait_lds();
-        sk_stage<RAC, 2>(b, a, sm, acc, accr, hook);
+        sk_stage<RAC, 2>(b, pr, a, sm, acc, accr, hook);
       }
-      adv_a();
+      if (has_a) adv_a();
       adv_b();
 
       if (cc.it == niter - 1) {
@@ -1145,7 +1213,6 @@ struct SkPlan {
   int nblk, grid;
   size_t lds;
 };
-constexpr int SK_NS = 3;                 // weight ring depth
 
 inline int64_t skinny_nblk(int64_t N, int epilogue) {
   return epilogue == QD_EPI_SWIGLU ? ((N / 2) + SK_ROWS / 2 - 1) / (SK_ROWS / 2)
@@ -1161,7 +1228,7 @@ inline SkPlan skinny_plan(int64_t rows, int E, int64_t N, int64_t K, int Ks, int
   const int64_t nblk = skinny_nblk(N, epilogue);
   pl.nblk = (int)nblk;
   pl.grid = (int)std::min<int64_t>(SK_GRID, (int64_t)E * nblk * 4);
-  pl.lds = (size_t)sk_layout((int)K, E, rac ? 2 : 1, SK_NS).total;
+  pl.lds = (size_t)sk_layout((int)K, E, rac).total;
   if (pl.lds > (size_t)SK_LDS_MAX) return pl;
   pl.ok = true;
   return pl;
@@ -1176,7 +1243,7 @@ inline int64_t grid_y(int64_t N, int epilogue) {
 
 template <bool GATHER, bool RAC, int EPI>
 void launch_skinny(const GemmArgs &p, const SkPlan &pl, hipStream_t s) {
-  auto kern = gemm_skinny_kernel<GATHER, RAC, EPI, SK_NS>;
+  auto kern = gemm_skinny_kernel<GATHER, RAC, EPI>;
   static const bool attr = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize,
                                                SK_LDS_MAX) == hipSuccess;
@@ -1256,6 +1323,44 @@ extern "C" int64_t moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int
   return grid_x(rows, E, true) * grid_y(N, epilogue);
 }
 
+// Fragment-ordered weight scales: one thread per output dword, i.e. per
+// (group e, 16-row fragment f, 256-column chunk c, lane l = 16 g + r); the
+// dword holds the scales of row 16 f + r, blocks 16 c + 4 g .. 16 c + 4 g + 3.
+__global__ __launch_bounds__(256) void pack_frag_scales_kernel(const uint8_t *__restrict__ sc,
+                                                               int64_t rows, int64_t cols,
+                                                               int64_t ndw,
+                                                               uint32_t *__restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= ndw) return;
+  const int l = (int)(i & 63);
+  const int64_t rec = i >> 6;
+  const int64_t nc = cols >> 8, nf = rows >> 4;
+  const int64_t c = rec % nc, f = (rec / nc) % nf, e = rec / (nc * nf);
+  const int64_t row = e * rows + 16 * f + (l & 15);
+  out[i] = *reinterpret_cast<const uint32_t *>(sc + row * (cols >> 4) + 16 * c + 4 * (l >> 4));
+}
+
+extern "C" int64_t nvfp4_frag_scales_bytes(int64_t groups, int64_t rows, int64_t cols) {
+  if (groups < 1 || rows < 0 || cols <= 0 || rows % 16 != 0 || cols % 256 != 0) return 0;
+  return groups * rows * (cols / 16);
+}
+
+extern "C" qd_status nvfp4_pack_frag_scales(const qd_nvfp4 *w, uint8_t *out, void *stream) {
+  if (!w || !out) return QD_ERR_NULL;
+  qd_status st = qdh::check_nvfp4(w, w->groups, w->rows, w->cols);
+  if (st) return st;
+  if (w->rows % 16 != 0 || w->cols % 256 != 0) return QD_ERR_SHAPE;
+  if (!qdh::aligned16(out)) return QD_ERR_ALIGN;
+  if (qdh::fault_injected()) return QD_ERR_HIP;
+  const int64_t ndw = w->groups * w->rows * (w->cols / 16) / 4;
+  if (ndw == 0) return QD_OK;
+  if ((ndw + 255) / 256 > 0x7fffffffLL) return QD_ERR_UNSUPPORTED;
+  hipLaunchKernelGGL(pack_frag_scales_kernel, dim3((unsigned)((ndw + 255) / 256)), dim3(256), 0,
+                     qdh::S(stream), w->scales, w->rows, w->cols, ndw,
+                     reinterpret_cast<uint32_t *>(out));
+  return qdh::check_launch();
+}
+
 extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
                                            const int32_t *expert_offsets, int32_t E, int64_t rows,
                                            const qd_nvfp4 *w, const qd_nvfp4 *rq,
@@ -1287,6 +1392,7 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
   if (Ks < 0) return QD_ERR_SHAPE;
   if (!qdh::aligned16(out) || (amax_partials && ((uintptr_t)amax_partials & 3u)))
     return QD_ERR_ALIGN;
+  if (w->scales_frag && !qdh::aligned16(w->scales_frag)) return QD_ERR_ALIGN;
   if (N > 0x7fffffff || K > 0x7fffffff) return QD_ERR_UNSUPPORTED;
   const int64_t gx = grid_x(rows, E, true), gy = grid_y(N, epilogue);
   if (gx > 0x7fffffffLL || gy > 65535) return QD_ERR_UNSUPPORTED;
@@ -1303,6 +1409,7 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
   p.rows = rows;
   p.w_codes = w->codes;
   p.w_scales = w->scales;
+  p.w_sfrag = w->scales_frag;
   p.w_gs = w->gscale;
   p.N = (int)N;
   p.K = (int)K;

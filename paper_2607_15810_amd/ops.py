@@ -6,6 +6,7 @@ pointers to libquads.so.  Nothing here computes any part of the layer.
 """
 
 from dataclasses import dataclass
+from typing import Optional
 
 import torch
 
@@ -36,13 +37,15 @@ def _ws(nbytes, device):
 
 @dataclass
 class NVFP4Tensor:
-    """codes uint8 [G][R][C/2], scales uint8 [G][R][C/16], gscale f32 [G][2]."""
+    """codes uint8 [G][R][C/2], scales uint8 [G][R][C/16], gscale f32 [G][2];
+    scales_frag: None, or the scales in fragment order (weights only)."""
     codes: torch.Tensor
     scales: torch.Tensor
     gscale: torch.Tensor
     groups: int
     rows: int
     cols: int
+    scales_frag: Optional[torch.Tensor] = None
 
     @staticmethod
     def empty(groups, rows, cols, device):
@@ -54,7 +57,8 @@ class NVFP4Tensor:
 
     def struct(self):
         return Q.NVFP4(self.codes.data_ptr(), self.scales.data_ptr(), self.gscale.data_ptr(),
-                       self.groups, self.rows, self.cols)
+                       self.groups, self.rows, self.cols,
+                       self.scales_frag.data_ptr() if self.scales_frag is not None else None)
 
     def ref(self):
         import ctypes
@@ -90,8 +94,10 @@ def quantize_act(x, amax_partials=None, rac=False):
     return out, scores, ramax
 
 
-def quantize_weight(w):
-    """Q_W of a bf16 bank [groups][rows][cols], one tensor scale per group."""
+def quantize_weight(w, frag_scales=True):
+    """Q_W of a bf16 bank [groups][rows][cols], one tensor scale per group.
+    With frag_scales (and rows % 16 == 0, cols % 256 == 0) the result also
+    carries the fragment-ordered copy of its scales (pack_frag_scales)."""
     _require_cuda(w)
     w = w.contiguous()
     if w.dim() == 2:
@@ -101,6 +107,21 @@ def quantize_weight(w):
     ws = _ws(Q.lib().nvfp4_quantize_weight_workspace(G, R, C), w.device)
     Q.call("nvfp4_quantize_weight", w.data_ptr(), G, R, C, _nv(out), ws.data_ptr(), ws.numel(),
            _stream())
+    if frag_scales and Q.lib().nvfp4_frag_scales_bytes(G, R, C) > 0:
+        out.scales_frag = pack_frag_scales(out)
+    return out
+
+
+def pack_frag_scales(t):
+    """The scales of weight tensor t re-laid out in fragment order: uint8
+    [G][R/16][C/256][256] (nvfp4_pack_frag_scales)."""
+    n = Q.lib().nvfp4_frag_scales_bytes(t.groups, t.rows, t.cols)
+    if n <= 0:
+        raise ValueError("fragment-ordered scales need rows % 16 == 0 and cols % 256 == 0")
+    out = torch.empty((t.groups, t.rows // 16, t.cols // 256, 256), dtype=torch.uint8,
+                      device=t.codes.device)
+    plain = NVFP4Tensor(t.codes, t.scales, t.gscale, t.groups, t.rows, t.cols)
+    Q.call("nvfp4_pack_frag_scales", _nv(plain), out.data_ptr(), _stream())
     return out
 
 

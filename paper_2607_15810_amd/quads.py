@@ -33,9 +33,10 @@ VIEW_NAMES = ["topk_ids", "topk_w", "offsets", "row_token", "inv_row", "xq_codes
 
 
 class NVFP4(ctypes.Structure):
-    """qd_nvfp4: three device pointers and the shape."""
+    """qd_nvfp4: device pointers, the shape, the optional fragment-ordered scales."""
     _fields_ = [("codes", c_void_p), ("scales", c_void_p), ("gscale", c_void_p),
-                ("groups", c_int64), ("rows", c_int64), ("cols", c_int64)]
+                ("groups", c_int64), ("rows", c_int64), ("cols", c_int64),
+                ("scales_frag", c_void_p)]
 
 
 PN = POINTER(NVFP4)
@@ -64,6 +65,8 @@ SIGNATURES = {
                                   c_void_p, c_void_p]),
     "moe_w4a4_grouped_gemm_amax_count": (c_int64, [c_int64, c_int64, c_int64, c_int32, c_int32,
                                                    c_int32]),
+    "nvfp4_frag_scales_bytes": (c_int64, [c_int64, c_int64, c_int64]),
+    "nvfp4_pack_frag_scales": (c_int, [PN, c_void_p, c_void_p]),
     "moe_w4a4_grouped_gemm": (c_int, [PN, c_void_p, c_void_p, c_int32, c_int64, PN, PN,
                                       c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_void_p,
                                       c_void_p]),

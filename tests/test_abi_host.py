@@ -189,3 +189,27 @@ def test_injected_launch_failure():
                          cwd=ROOT, timeout=120)
     assert out.returncode == 0, out.stderr
     assert int(out.stdout.strip().splitlines()[-1]) == Q.QD_ERR_HIP
+
+
+def test_frag_scales_validation(lib):
+    assert lib.nvfp4_frag_scales_bytes(2, 32, 512) == 2 * 32 * 32
+    assert lib.nvfp4_frag_scales_bytes(2, 40, 512) == 0        # rows % 16
+    assert lib.nvfp4_frag_scales_bytes(2, 32, 384) == 0        # cols % 256
+    assert lib.nvfp4_frag_scales_bytes(0, 32, 512) == 0
+    r = lib.nvfp4_pack_frag_scales
+    assert r(None, FAKE, None) == Q.QD_ERR_NULL
+    assert r(ctypes.byref(_nv(2, 32, 512, FAKE)), None, None) == Q.QD_ERR_NULL
+    assert r(ctypes.byref(_nv(2, 40, 512, FAKE)), FAKE, None) == Q.QD_ERR_SHAPE
+    assert r(ctypes.byref(_nv(2, 32, 384, FAKE)), FAKE, None) == Q.QD_ERR_SHAPE
+    assert r(ctypes.byref(_nv(2, 32, 512, FAKE)), FAKE + 4, None) == Q.QD_ERR_ALIGN
+
+
+def test_gemm_rejects_misaligned_frag_scales(lib):
+    a = _nv(1, 16, 256, FAKE)
+    w = _nv(4, 128, 256, FAKE)
+    w.scales_frag = FAKE + 8
+    offs = FAKE
+    st = lib.moe_w4a4_grouped_gemm(ctypes.byref(a), None, offs, 4, 16, ctypes.byref(w), None,
+                                   None, 0, None, 0, FAKE, None, None)
+    assert st == Q.QD_ERR_ALIGN
+
