@@ -548,43 +548,51 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     const float r_dec = RAC ? p.r_gs[1] : 0.0f;
     // ---- issue cursors and their per-lane addresses
     SkCur ca = cc, cb = cc;
-    const uint8_t *bc0, *bc1, *bs0, *bs1;
+    // weight codes: dma i of a stage brings full 128-byte row chunks, lane
+    // l row 8 i + l / 8 of the wave's 32 (rows 16..31: the second fragment)
+    // and 16-byte piece (l % 8) ^ (l / 8), so the pieces of a row land
+    // XOR-swizzled and the fragment reads below are free of bank conflicts
+    const uint8_t *bcq[4], *bs0, *bs1;
+    const int bq_piece = (lane & 7) ^ (lane >> 3);
     // weight scales: the standard layout (16 bytes per row and stage, in
     // every row's scale line) or the fragment-ordered copy (256 contiguous
     // bytes per 16-row fragment and stage, one dword per lane in lane order)
     const int sstep = p.w_sfrag ? 256 : 16;
     auto bind_b = [&](const SkCur &c) {
-      int64_t r0, r1;
       // the wave's two 16-row fragments (all rows of a fragment are valid
       // or none, N and I being multiples of 16; invalid ones read row 0)
-      int64_t f0, f1;
+      int64_t r0, r1, f0, f1;
+      const int lq = lane >> 3;               // fragment row of dma 0 (dma 1: + 8)
       if (EPI == QD_EPI_SWIGLU) {
         const int I = N >> 1;
-        const int pr_ = c.nb * (SK_ROWS / 2) + w * 16 + lr;
-        r0 = pr_ < I ? pr_ : 0;
-        r1 = pr_ < I ? pr_ + I : 0;
         const int fr = c.nb * (SK_ROWS / 32) + w;
-        f0 = 16 * fr < I ? fr : 0;
-        f1 = 16 * fr < I ? fr + (I >> 4) : 0;
+        const bool ok = 16 * fr < I;
+        r0 = ok ? 16 * fr : 0;
+        r1 = ok ? 16 * fr + I : 0;
+        f0 = ok ? fr : 0;
+        f1 = ok ? fr + (I >> 4) : 0;
       } else {
-        const int r = c.nb * SK_ROWS + w * 32 + lr;
-        r0 = r < N ? r : 0;
-        r1 = r + 16 < N ? r + 16 : 0;
         const int fr = c.nb * (SK_ROWS / 16) + 2 * w;
-        f0 = 16 * fr < N ? fr : 0;
-        f1 = 16 * (fr + 1) < N ? fr + 1 : 0;
+        const bool ok0 = 16 * fr < N, ok1 = 16 * (fr + 1) < N;
+        r0 = ok0 ? 16 * fr : 0;
+        r1 = ok1 ? 16 * (fr + 1) : 0;
+        f0 = ok0 ? fr : 0;
+        f1 = ok1 ? fr + 1 : 0;
       }
       r0 += (int64_t)c.e * N;
       r1 += (int64_t)c.e * N;
-      bc0 = p.w_codes + r0 * kb2 + g * 32;
-      bc1 = p.w_codes + r1 * kb2 + g * 32;
+      // an invalid fragment reads rows 0..15 of the expert (any valid rows)
+      bcq[0] = p.w_codes + (r0 + lq) * kb2 + 16 * bq_piece;
+      bcq[1] = p.w_codes + (r0 + lq + 8) * kb2 + 16 * bq_piece;
+      bcq[2] = p.w_codes + (r1 + lq) * kb2 + 16 * bq_piece;
+      bcq[3] = p.w_codes + (r1 + lq + 8) * kb2 + 16 * bq_piece;
       if (p.w_sfrag) {
         const int64_t nf = N >> 4;
         bs0 = p.w_sfrag + (((int64_t)c.e * nf + f0) * niter) * 256 + lane * 4;
         bs1 = p.w_sfrag + (((int64_t)c.e * nf + f1) * niter) * 256 + lane * 4;
       } else {
-        bs0 = p.w_scales + r0 * kb16 + g * 4;
-        bs1 = p.w_scales + r1 * kb16 + g * 4;
+        bs0 = p.w_scales + (r0 + lr) * kb16 + g * 4;
+        bs1 = p.w_scales + (r1 + lr) * kb16 + g * 4;
       }
     };
     // activations.  Waves 0..3 (decoders, lane group g = w) load lane
@@ -615,6 +623,8 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     };
     const uint32_t bring = lds0 + L.b + w * SK_NS * SK_BSTAGE;
     const uint32_t junk = lds0 + L.junk;
+    const int b_off0 = 128 * lr + 16 * ((2 * g) ^ (lr & 7));
+    const int b_off1 = 128 * lr + 16 * ((2 * g + 1) ^ (lr & 7));
     // LDS destinations of the activation loads of stage sg
     auto a_cdst = [&](int sg) -> uint32_t {
       return dec ? lds0 + L.xraw + (w * SK_NX + sg % SK_NX) * SK_XRAW
@@ -632,10 +642,10 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     auto issue_b = [&](int sg) {
       const uint32_t slot = uni(bring + (sg % SK_NS) * SK_BSTAGE);
       const int off = cb.it * 128;
-      dma16(bc0 + off, slot);
-      dma16(bc0 + off + 16, slot + 1024);
-      dma16(bc1 + off, slot + 2048);
-      dma16(bc1 + off + 16, slot + 3072);
+      dma16(bcq[0] + off, slot);
+      dma16(bcq[1] + off, slot + 1024);
+      dma16(bcq[2] + off, slot + 2048);
+      dma16(bcq[3] + off, slot + 3072);
       dma4(bs0 + cb.it * sstep, slot + 4096);
       dma4(bs1 + cb.it * sstep, slot + 4096 + 256);
     };
@@ -694,11 +704,14 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
       if (has_a) wait_vm<8>(); else wait_vm<6>();
       __syncthreads();       // the panel of stage sg and all residual rows of sg have landed
       const unsigned char *bsl = lds + L.b + (w * SK_NS + sg % SK_NS) * SK_BSTAGE;
+      // row r of the stage (r < 16: first fragment) holds piece q at
+      // 128 r + 16 (q ^ (r % 8)); this lane needs pieces 2g, 2g + 1 of rows
+      // lr and 16 + lr
       BReg b;
-      b.c00 = *reinterpret_cast<const u32x4 *>(bsl + 0 * 1024 + lane * 16);
-      b.c01 = *reinterpret_cast<const u32x4 *>(bsl + 1 * 1024 + lane * 16);
-      b.c10 = *reinterpret_cast<const u32x4 *>(bsl + 2 * 1024 + lane * 16);
-      b.c11 = *reinterpret_cast<const u32x4 *>(bsl + 3 * 1024 + lane * 16);
+      b.c00 = *reinterpret_cast<const u32x4 *>(bsl + b_off0);
+      b.c01 = *reinterpret_cast<const u32x4 *>(bsl + b_off1);
+      b.c10 = *reinterpret_cast<const u32x4 *>(bsl + 2048 + b_off0);
+      b.c11 = *reinterpret_cast<const u32x4 *>(bsl + 2048 + b_off1);
       b.s0 = *reinterpret_cast<const uint32_t *>(bsl + 4096 + lane * 4);
       b.s1 = *reinterpret_cast<const uint32_t *>(bsl + 4096 + 256 + lane * 4);
       const uint32_t sm = RAC ? smask[cc.it] : 0u;
@@ -718,10 +731,10 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
                             pan_w(sg + 1), lane);
           const uint32_t slot = uni(bring + (sg % SK_NS) * SK_BSTAGE);
           const int off = cb.it * 128, soff = cb.it * sstep;
-          if (k == 2) dma16(bc0 + off, slot);
-          if (k == 3) dma16(bc0 + off + 16, slot + 1024);
-          if (k == 4) dma16(bc1 + off, slot + 2048);
-          if (k == 5) dma16(bc1 + off + 16, slot + 3072);
+          if (k == 2) dma16(bcq[0] + off, slot);
+          if (k == 3) dma16(bcq[1] + off, slot + 1024);
+          if (k == 4) dma16(bcq[2] + off, slot + 2048);
+          if (k == 5) dma16(bcq[3] + off, slot + 3072);
           if (k == 6) dma4(bs0 + soff, slot + 4096);
           if (k == 7) dma4(bs1 + soff, slot + 4096 + 256);
         }
