@@ -286,17 +286,16 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs p) {
 //    g's 64 elements of every row, with their scale dword) into a private
 //    raw slot, decode it exactly to f16 one stage ahead and write it into a
 //    shared two-slot f16 panel, laid out as the MFMA's A fragments; every
-//    wave then reads its fragments from the panel.  With RAC, waves 4..7
-//    load the masked residual rows into a four-slot ring shared by the waves,
-//    which decode them at the k-steps that hold a selected channel.
-//  * Loads are issued in one fixed order per iteration: the activations of
-//    the stage three ahead, then the weights of the stage two ahead, spread
-//    over the k-steps.  Loads complete in issue order, so one explicit wait
-//    at the top of iteration s (at most one iteration's loads outstanding)
-//    proves that the wave's weights of stage s and its activations of stage
-//    s + 1 have landed; the barrier after it publishes the panel of stage s
-//    and everyone's residual rows.  Loads past the last stage repeat the
-//    last stage's addresses into slots that are never read again.
+//    wave then reads its fragments from the panel.  With RAC, waves 4..7 do
+//    the same for the masked residual rows into a second panel.
+//  * Loads are issued in one fixed order per iteration, spread over the
+//    k-steps: the activations, then the weights, of the stage two ahead.
+//    Loads complete in issue order, so one explicit wait at the top of
+//    iteration s (at most the last iteration's weights outstanding) proves
+//    that the wave's weights of stage s and its activations of stage s + 1
+//    have landed; the barrier after it publishes the panels of stage s.
+//    Loads past the last stage repeat the last stage's addresses into slots
+//    that are never read again.
 //  * Weight operands are decoded exactly to f16 in registers (see the top of
 //    this file) and multiplied on MFMA, with straight-line code for each
 //    number of valid 16-row m-tiles.
@@ -315,9 +314,7 @@ constexpr int SK_ROWS = 32 * SK_WAVES;   // weight rows per unit
 constexpr int SK_PR = 32;                // activation rows per pass
 constexpr int SK_NS = 2;                 // weight ring depth
 constexpr int SK_BSTAGE = 4608;          // bytes per wave and weight stage
-constexpr int SK_ASRC = SK_PR * 144;     // raw residual stage (codes + scales)
-constexpr int SK_NR = 4;                 // residual slots
-constexpr int SK_NX = 3;                 // raw activation slots per decoding wave
+constexpr int SK_NX = 2;                 // raw activation slots per decoding wave
 constexpr int SK_XRAW = 1280;            // one decoding wave's raw stage: 1 KB codes, 256 B scales
 constexpr int SK_PANEL = SK_PR * 256 * 2;   // one f16 panel stage
 constexpr int SK_KMAX = 65536;
@@ -326,18 +323,17 @@ constexpr int SK_LDS_MAX = 160 * 1024;
 constexpr int SK_GRID = 256;             // one workgroup per CU
 
 struct SkLayout {
-  int b, pan, xraw, rraw, junk, offs, pu, sw, smask, red, total;
+  int b, pan, xraw, offs, pu, sw, smask, red, total;
 };
 
+// panels: [source x, residual][slot 0, 1]; raw slots: [decoding wave][slot]
 __host__ __device__ inline SkLayout sk_layout(int K, int E, bool rac) {
   SkLayout L{};
   int o = 0;
   auto take = [&](int bytes) { int at = o; o += (bytes + 15) & ~15; return at; };
   L.b = take(SK_WAVES * SK_NS * SK_BSTAGE);
-  L.pan = take(2 * SK_PANEL);
-  L.xraw = take(4 * SK_NX * SK_XRAW);
-  L.rraw = take(rac ? SK_NR * SK_ASRC : 0);
-  L.junk = take(1024);
+  L.pan = take((rac ? 4 : 2) * SK_PANEL);
+  L.xraw = take((rac ? 8 : 4) * SK_NX * SK_XRAW);
   L.offs = take((E + 1) * 4);
   L.pu = take((E + 1) * 4);
   L.sw = take(E * 4);
@@ -399,45 +395,20 @@ struct BReg {
   u32x4 c00, c01, c10, c11;
   uint32_t s0, s1;
 };
-// Raw masked-residual data of one stage for MTV m-tiles: the lane's 16 code
-// bytes per chunk and m-tile, and its scale dword.
-template <int MTV>
-struct RRaw {
-  uint4 r[2][MTV];
-  uint32_t rs[MTV];
-};
-template <int MTV>
-__device__ __forceinline__ void load_rraw(RRaw<MTV> &a, const unsigned char *rsl, int lane) {
-  const int lr = lane & 15, g = lane >> 4;
-#pragma unroll
-  for (int i = 0; i < MTV; ++i) {
-    const int rr = i * 16 + lr;
-#pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2)
-      a.r[c2][i] = *reinterpret_cast<const uint4 *>(rsl + ((c2 * 4 + g) * SK_PR + rr) * 16);
-    a.rs[i] = *reinterpret_cast<const uint32_t *>(rsl + 4096 + (g * SK_PR + rr) * 4);
-  }
-}
-
-// One stage's MFMA work for MTV valid m-tiles.  pan points at the lane's A
-// fragment of k-step 0, m-tile 0 in the stage's f16 panel (k-step (c, s) is
-// 2048 (4c + s) bytes further, m-tile i 256 i).  hook(k) runs before k-step
-// k (0..7): the caller issues its loads for later stages there and decodes
-// the next panel.
+// One stage's MFMA work for MTV valid m-tiles.  pan / rpan point at the
+// lane's A fragment of k-step 0, m-tile 0 in the stage's f16 panels of x
+// and of the masked residual (k-step (c, s) is 2048 (4c + s) bytes further,
+// m-tile i 256 i).  hook(k) runs before k-step k (0..7): the caller issues
+// its loads for later stages there and decodes the next panels.
 template <bool RAC, int MTV, typename Hook>
 __device__ __forceinline__ void sk_stage(const BReg &b, const unsigned char *pan,
-                                         const RRaw<MTV> &a, uint32_t sm, f32x4 (&acc)[2][2],
-                                         f32x4 (&accr)[2][2], Hook &&hook) {
+                                         const unsigned char *rpan, uint32_t sm,
+                                         f32x4 (&acc)[2][2], f32x4 (&accr)[2][2], Hook &&hook) {
 #pragma unroll
   for (int c2 = 0; c2 < 2; ++c2) {
     const u32x4 bv0 = c2 ? b.c01 : b.c00;
     const u32x4 bv1 = c2 ? b.c11 : b.c10;
     const f16x2 sp0 = scale_pair_of(b.s0, c2), sp1 = scale_pair_of(b.s1, c2);
-    f16x2 rp[MTV];
-    const bool rchunk = RAC && ((sm >> (4 * c2)) & 15u) != 0u;
-#pragma unroll
-    for (int i = 0; i < MTV; ++i)
-      if (rchunk) rp[i] = scale_pair_of(a.rs[i], c2);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       hook(c2 * 4 + s);
@@ -453,7 +424,8 @@ __device__ __forceinline__ void sk_stage(const BReg &b, const unsigned char *pan
       if (RAC && ((sm >> (4 * c2 + s)) & 1u)) {
 #pragma unroll
         for (int i = 0; i < MTV; ++i) {
-          const f16x8 rf = decode8_sel(word_of(a.r[c2][i], s), rp[i], s >= 2);
+          const f16x8 rf =
+              *reinterpret_cast<const f16x8 *>(rpan + (c2 * 4 + s) * 2048 + i * 256);
           accr[i][0] = mfma16(rf, bf0, accr[i][0]);
           accr[i][1] = mfma16(rf, bf1, accr[i][1]);
         }
@@ -462,7 +434,7 @@ __device__ __forceinline__ void sk_stage(const BReg &b, const unsigned char *pan
   }
 }
 
-// A decoding wave (lane group g = wave index) turns its raw slot -- lane
+// A decoding wave (lane group g = wave index % 4) turns its raw slot -- lane
 // (row l % 32, chunk l / 32): 16 code bytes at 16 l, the row's scale dword
 // at 1024 + 4 (l % 32) -- into its part of an f16 panel stage, where the A
 // fragment of k-step (c, s), lane group g, row r sits at
@@ -595,20 +567,16 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
         bs1 = p.w_scales + (r1 + lr) * kb16 + g * 4;
       }
     };
-    // activations.  Waves 0..3 (decoders, lane group g = w) load lane
-    // (row l % 32, chunk l / 32)'s 16 code bytes and the row's scale dword
-    // of x into their private raw slot.  With RAC waves 4..7 load the
-    // masked residual into the shared ring: codes by column block b = 4 *
-    // chunk + lane group, 32 rows x 16 B each (two blocks per wave), scales
-    // by lane group, 32 rows x 4 B (waves 4, 5; waves 6, 7 load theirs into
-    // a junk area).  Without RAC waves 4..7 load no activations.
-    const bool dec = w < 4;
-    const bool has_a = dec || RAC;
+    // activations.  Decoding wave w (waves 0..3: x; with RAC waves 4..7:
+    // the masked residual; lane group gd = w % 4) loads lane (row l % 32,
+    // chunk l / 32)'s 16 code bytes and the row's scale dword into its
+    // private raw slot.  Without RAC waves 4..7 load no activations.
+    const bool xdec = w < 4;
+    const bool has_a = xdec || RAC;
+    const int gd = w & 3;
     const int a_row = lane & 31;
-    const int a_blk = 2 * (w & 3) + (lane >> 5);
-    const int64_t a_cb = dec ? 32 * w + 16 * (lane >> 5) : (a_blk & 3) * 32 + (a_blk >> 2) * 16;
-    const int64_t a_sb = dec ? 4 * w : (2 * (w & 1) + (lane >> 5)) * 4;
-    const bool s_live = dec || w < 6;
+    const int64_t a_cb = 32 * gd + 16 * (lane >> 5);
+    const int64_t a_sb = 4 * gd;
     const uint8_t *ac, *as;
     int a_e = -1, a_p = -1;
     auto bind_a = [&](const SkCur &c) {
@@ -618,26 +586,19 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
       int64_t r = (int64_t)c.ob + (int64_t)c.p * SK_PR + a_row;
       r = min(r, (int64_t)c.ob + c.rows - 1);
       const int64_t src = GATHER ? (int64_t)p.row_token[r] : r;
-      ac = (dec ? p.a_codes : p.r_codes) + src * kb2 + a_cb;
-      as = (dec ? p.a_scales : p.r_scales) + src * kb16 + a_sb;
+      ac = (xdec ? p.a_codes : p.r_codes) + src * kb2 + a_cb;
+      as = (xdec ? p.a_scales : p.r_scales) + src * kb16 + a_sb;
     };
     const uint32_t bring = lds0 + L.b + w * SK_NS * SK_BSTAGE;
-    const uint32_t junk = lds0 + L.junk;
     const int b_off0 = 128 * lr + 16 * ((2 * g) ^ (lr & 7));
     const int b_off1 = 128 * lr + 16 * ((2 * g + 1) ^ (lr & 7));
-    // LDS destinations of the activation loads of stage sg
-    auto a_cdst = [&](int sg) -> uint32_t {
-      return dec ? lds0 + L.xraw + (w * SK_NX + sg % SK_NX) * SK_XRAW
-                 : lds0 + L.rraw + (sg % SK_NR) * SK_ASRC + (w & 3) * 1024;
-    };
-    auto a_sdst = [&](int sg) -> uint32_t {
-      return dec ? lds0 + L.xraw + (w * SK_NX + sg % SK_NX) * SK_XRAW + 1024
-                 : (s_live ? lds0 + L.rraw + (sg % SK_NR) * SK_ASRC + 4096 + (w & 1) * 256
-                           : junk);
+    // the raw slot of stage sg (codes; the scale dwords 1024 further)
+    auto a_raw = [&](int sg) -> uint32_t {
+      return lds0 + L.xraw + (w * SK_NX + sg % SK_NX) * SK_XRAW;
     };
     auto issue_a = [&](int sg) {
-      dma16(ac + ca.it * 128, uni(a_cdst(sg)));
-      dma4(as + ca.it * 16, uni(a_sdst(sg)));
+      dma16(ac + ca.it * 128, uni(a_raw(sg)));
+      dma4(as + ca.it * 16, uni(a_raw(sg) + 1024));
     };
     auto issue_b = [&](int sg) {
       const uint32_t slot = uni(bring + (sg % SK_NS) * SK_BSTAGE);
@@ -656,34 +617,33 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     auto adv_a = [&]() {
       if (S.next(ca)) bind_a(ca);
     };
-    // the panel slot of stage sg, seen from this lane as a decoder (write)
-    // and as a reader (its A fragment of k-step 0, m-tile 0)
+    // the panel slot of stage sg (source x: 0, residual: 1), seen from this
+    // lane as a decoder (write) and as a reader (its A fragment of k-step 0,
+    // m-tile 0)
     auto pan_w = [&](int sg) {
-      return lds + L.pan + (sg & 1) * SK_PANEL + (lane >> 5) * 8192 + w * 512 + (lane & 31) * 16;
+      return lds + L.pan + ((w >> 2) * 2 + (sg & 1)) * SK_PANEL + (lane >> 5) * 8192 + gd * 512 +
+             (lane & 31) * 16;
     };
-    auto pan_r = [&](int sg) {
-      return lds + L.pan + (sg & 1) * SK_PANEL + g * 512 + lr * 16;
+    auto pan_r = [&](int src, int sg) {
+      return lds + L.pan + (src * 2 + (sg & 1)) * SK_PANEL + g * 512 + lr * 16;
     };
 
-    // ---- prologue: activations of stages 0, 1, 2 and weights of stages
-    // 0, 1 in the steady-state order (A0 | A1 B0 | A2 B1), then the panel of
-    // stage 0
+    // ---- prologue: the steady-state issue order for stages 0 and 1
+    // (A0 | A1 B0 | B1), then the panel of stage 0
     bind_b(cb);
     bind_a(ca);
     if (has_a) {
       issue_a(0);
       adv_a();
+      issue_a(1);
+      adv_a();
     }
     for (int i = 0; i < 2; ++i) {
-      if (has_a) {
-        issue_a(i + 1);
-        adv_a();
-      }
       issue_b(i);
       adv_b();
     }
-    if (dec) {
-      wait_vm<16>();         // this wave's activations of stage 0
+    if (has_a) {
+      wait_vm<14>();         // this wave's activations of stage 0
       sk_decode_panel(lds + L.xraw + (w * SK_NX) * SK_XRAW, pan_w(0), lane);
     }
 
@@ -699,10 +659,9 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     for (int sg = 0;; ++sg) {
       const int nrow = min(SK_PR, cc.rows - cc.p * SK_PR);
       const int mtv = nrow > 16 ? 2 : 1;
-      // outstanding past this point: at most the last iteration's loads
-      // (activations of stage sg + 2, weights of stage sg + 1)
-      if (has_a) wait_vm<8>(); else wait_vm<6>();
-      __syncthreads();       // the panel of stage sg and all residual rows of sg have landed
+      // outstanding past this point: at most the weights of stage sg + 1
+      wait_vm<6>();
+      __syncthreads();       // the panels of stage sg are complete
       const unsigned char *bsl = lds + L.b + (w * SK_NS + sg % SK_NS) * SK_BSTAGE;
       // row r of the stage (r < 16: first fragment) holds piece q at
       // 128 r + 16 (q ^ (r % 8)); this lane needs pieces 2g, 2g + 1 of rows
@@ -715,18 +674,18 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
       b.s0 = *reinterpret_cast<const uint32_t *>(bsl + 4096 + lane * 4);
       b.s1 = *reinterpret_cast<const uint32_t *>(bsl + 4096 + 256 + lane * 4);
       const uint32_t sm = RAC ? smask[cc.it] : 0u;
-      const unsigned char *rsl = lds + L.rraw + (sg % SK_NR) * SK_ASRC;
-      // before k-step 0 and 1: the activations of stage sg + 3; before k-step
-      // 2: the decode of stage sg + 1's panel; before k-steps 2..7: the
-      // weights of stage sg + 2 into the slot just read
+      // before k-step 0 and 1: the activations of stage sg + 2 (into the
+      // raw slot decoded in the last iteration); before k-step 2: the decode
+      // of stage sg + 1's panels; before k-steps 2..7: the weights of stage
+      // sg + 2 into the slot just read
       auto hook = [&](int k) {
         if (k < 2) {
           if (has_a) {
-            if (k == 0) dma16(ac + ca.it * 128, uni(a_cdst(sg + 3)));
-            else dma4(as + ca.it * 16, uni(a_sdst(sg + 3)));
+            if (k == 0) dma16(ac + ca.it * 128, uni(a_raw(sg + 2)));
+            else dma4(as + ca.it * 16, uni(a_raw(sg + 2) + 1024));
           }
         } else {
-          if (k == 2 && dec)
+          if (k == 2 && has_a)
             sk_decode_panel(lds + L.xraw + (w * SK_NX + (sg + 1) % SK_NX) * SK_XRAW,
                             pan_w(sg + 1), lane);
           const uint32_t slot = uni(bring + (sg % SK_NS) * SK_BSTAGE);
@@ -739,18 +698,13 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
           if (k == 7) dma4(bs1 + soff, slot + 4096 + 256);
         }
       };
-      const unsigned char *pr = pan_r(sg);
-      if (mtv == 1) {
-        RRaw<1> a;
-        if (RAC && sm != 0u) load_rraw<1>(a, rsl, lane);
-        wait_lds();          // the weight slot may be refilled from here on
-        sk_stage<RAC, 1>(b, pr, a, sm, acc, accr, hook);
-      } else {
-        RRaw<2> a;
-        if (RAC && sm != 0u) load_rraw<2>(a, rsl, lane);
-        wait_lds();
-        sk_stage<RAC, 2>(b, pr, a, sm, acc, accr, hook);
-      }
+      const unsigned char *pr = pan_r(0, sg);
+      const unsigned char *prr = pan_r(RAC ? 1 : 0, sg);
+      wait_lds();            // the weight slot may be refilled from here on
+      if (mtv == 1)
+        sk_stage<RAC, 1>(b, pr, prr, sm, acc, accr, hook);
+      else
+        sk_stage<RAC, 2>(b, pr, prr, sm, acc, accr, hook);
       if (has_a) adv_a();
       adv_b();
 
