@@ -805,6 +805,13 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
 //
 // Stage slot: A codes [8 fragments][64 lanes][16 B], B codes [4 fragments]
 // likewise, then A scale dwords [256 rows] and B scale dwords [128 rows].
+// Scale loads are the costly part of a stage (4 bytes per row, each in a
+// different scale line): the B scales come from the weights'
+// fragment-ordered copy when present (64 contiguous bytes per 16 rows), and
+// when LDS allows, the A scales of four stages at a time (16 contiguous
+// bytes per row, one load per 16-byte piece) go into a two-slot ring of their
+// own; the three stages between those loads issue a one-line dummy load in
+// their place so every stage issues the same number of loads.
 // Lane l of a fragment holds row l % 32, elements 32 (l / 32) .. +31 of the
 // stage; MFMA k-step s (0..3) takes elements 8s .. 8s+7 of each half, for A
 // and B alike.
@@ -826,6 +833,8 @@ __host__ __device__ constexpr int tl_ns(bool rac) { return rac ? 3 : 4; }   // r
 __host__ __device__ inline int tl_lds_bytes(bool rac, int ksa) {
   return tl_ns(rac) * TL_STAGE + (rac ? TL_N * (ksa + 8) * 2 + ksa * 4 : 0);
 }
+constexpr int TL_AGRP = 2 * TL_M * 16;   // the A-scale ring: 2 slots x 256 rows x 16 B
+constexpr int TL_LDS_2WG = TL_LDS_MAX / 2;   // two workgroups per CU
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -853,9 +862,10 @@ struct TlRaw {
   uint32_t as[4], bs[2];
 };
 
+// ascl / astr: the A scale dword of row r of this stage is at ascl + r * astr
 template <int MTV>
-__device__ __forceinline__ void tl_read(TlRaw &R, const unsigned char *sl, int fa0, int fb0,
-                                        int fbs, int lane) {
+__device__ __forceinline__ void tl_read(TlRaw &R, const unsigned char *sl, const unsigned char *ascl,
+                                        int astr, int fa0, int fb0, int fbs, int lane) {
   const int r = lane & 31;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
@@ -867,7 +877,7 @@ __device__ __forceinline__ void tl_read(TlRaw &R, const unsigned char *sl, int f
   for (int i = 0; i < MTV; ++i) {
     const int fa = fa0 + i;
     R.a[i] = *reinterpret_cast<const uint4 *>(sl + TL_ACODE + (fa * 64 + lane) * 16);
-    R.as[i] = *reinterpret_cast<const uint32_t *>(sl + TL_ASCL + (fa * 32 + r) * 4);
+    R.as[i] = *reinterpret_cast<const uint32_t *>(ascl + (fa * 32 + r) * astr);
   }
 }
 
@@ -904,7 +914,7 @@ __device__ __forceinline__ float swiglu_fast(float g, float u) {
 }
 
 template <bool GATHER, bool RAC, int EPI>
-__global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, int ntn) {
+__global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, int ntn, int grp) {
   constexpr int NS = tl_ns(RAC);
   extern __shared__ __align__(16) unsigned char lds[];
   __shared__ int sh_w[4];
@@ -978,23 +988,52 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
     const uint32_t oa1 = arow(64 * w + 32 + (lane & 31)) * (uint32_t)kb2 + hb;
     const uint32_t ob = (uint32_t)tile_wrow<EPI>(32 * w + (lane & 31), nt, N) * (uint32_t)kb2 + hb;
     const uint32_t oas = arow(64 * w + lane) * (uint32_t)kb16;
-    const uint32_t obs = (uint32_t)tile_wrow<EPI>(64 * (w & 1) + lane, nt, N) * (uint32_t)kb16;
+    const int bsr = tile_wrow<EPI>(64 * (w & 1) + lane, nt, N);
+    const bool sfrag = p.w_sfrag != nullptr;
+    // B scales: the standard layout (4 bytes of the row's line per stage) or
+    // the fragment-ordered copy (fragment f, chunk s / 4: 256 bytes, of
+    // which stage s takes the 64 at (s % 4) * 64, 4 per row)
+    const uint32_t obs = sfrag ? (uint32_t)(((bsr >> 4) * (K >> 8)) * 256 + (bsr & 15) * 4)
+                               : (uint32_t)bsr * (uint32_t)kb16;
     const uint8_t *wc = uni_ptr(p.w_codes + (int64_t)e * N * kb2);
-    const uint8_t *ws = uni_ptr(p.w_scales + (int64_t)e * N * kb16);
+    const uint8_t *ws = uni_ptr((sfrag ? p.w_sfrag : p.w_scales) + (int64_t)e * N * kb16);
+    const int bsstep = sfrag ? 64 : 4;
     const int nst = K / TL_K;
+    // the A-scale ring (grp): after the stage ring and the compact table
+    const uint32_t agrp = lds0 + (uint32_t)tl_lds_bytes(RAC, RAC ? p.ksa : 0);
+    const uint32_t oag = arow(64 * w + lane) * (uint32_t)kb16;
     // five loads per wave and stage (waves 0 / 2 and 1 / 3 load the same B
     // scale half: equal bytes to equal places)
     auto issue = [&](int s, int q) __attribute__((always_inline)) {
       s = min(s, nst - 1);
       const uint32_t sb = uni(lds0 + q * TL_STAGE);
       const uint8_t *ac = uni_ptr(p.a_codes + s * 32), *as_ = uni_ptr(p.a_scales + s * 4);
-      const uint8_t *bc = uni_ptr(wc + s * 32), *bs_ = uni_ptr(ws + s * 4);
+      const uint8_t *bc = uni_ptr(wc + s * 32), *bs_ = uni_ptr(ws + s * bsstep);
       dma16s(ac, oa0, sb + TL_ACODE + (2 * w) * 1024);
       dma16s(ac, oa1, sb + TL_ACODE + (2 * w + 1) * 1024);
       dma16s(bc, ob, sb + TL_BCODE + w * 1024);
-      dma4s(as_, oas, sb + TL_ASCL + w * 256);
+      if (grp) {
+        // stage 4G brings group G's A scales (rows 64 w .. 64 w + 63, 16 B
+        // each) into ring slot G % 2; other stages load one line (the group
+        // scales of the wave's first row: a different line per workgroup,
+        // never one line for the whole chip) into the unused A-scale area of
+        // their stage slot
+        if ((s & 3) == 0)
+          dma16s(uni_ptr(p.a_scales + (s >> 2) * 16), oag,
+                 uni(agrp + ((s >> 2) & 1) * (TL_AGRP / 2) + w * 1024));
+        else
+          dma16s(uni_ptr(p.a_scales + (s >> 2) * 16), uni(oag), sb + TL_ASCL);
+      } else {
+        dma4s(as_, oas, sb + TL_ASCL + w * 256);
+      }
       dma4s(bs_, obs, sb + TL_BSCL + (w & 1) * 256);
     };
+    // where tl_read finds stage s's A scales
+    auto a_src = [&](int s) __attribute__((always_inline)) -> const unsigned char * {
+      return grp ? lds + (agrp - lds0) + ((s >> 2) & 1) * (TL_AGRP / 2) + (s & 3) * 4
+                 : lds + (s % NS) * TL_STAGE + TL_ASCL;
+    };
+    const int astr = grp ? 16 : 4;
     const float a_dec = p.a_gs[1], sw = p.w_gs[2 * e + 1];
     float alpha = a_dec * sw;
     // RAC: acc -> acc * inv_c + accr, then alpha = -s_dec_r * s_dec_w.  A
@@ -1039,7 +1078,7 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
       for (int t = 0; t < NS - 1; ++t) issue(t, t);
       wait_vm<(NS - 2) * 5>();
       __syncthreads();
-      if constexpr (MTV > 0) tl_read<MTV>(R0, lds, fa0, fb0, fbs, lane);
+      if constexpr (MTV > 0) tl_read<MTV>(R0, lds, a_src(0), astr, fa0, fb0, fbs, lane);
       int sp = 0;                              // first selected channel not yet copied
       auto body = [&](const TlRaw &Rc, TlRaw &Rn, int s) __attribute__((always_inline)) {
         auto mid = [&]() __attribute__((always_inline)) {
@@ -1047,7 +1086,8 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
           __syncthreads();
           issue(s + NS - 1, (s + NS - 1) % NS);
           if constexpr (MTV > 0)
-            tl_read<MTV>(Rn, lds + ((s + 1) % NS) * TL_STAGE, fa0, fb0, fbs, lane);
+            tl_read<MTV>(Rn, lds + ((s + 1) % NS) * TL_STAGE, a_src(s + 1), astr, fa0, fb0, fbs,
+                         lane);
           if constexpr (RAC) {
             // selected channels of stage s (slot s % NS holds it until the
             // next barrier): decoded weight values into the compact table
@@ -1221,7 +1261,7 @@ void launch_skinny(const GemmArgs &p, const SkPlan &pl, hipStream_t s) {
 // host-side plan of the prefill kernel
 struct TlPlan {
   bool ok;
-  int ntn, grid, lds;
+  int ntn, grid, lds, grp;
 };
 
 // rac: the residual is fused (needs its compact form, rq_sel)
@@ -1234,6 +1274,13 @@ inline TlPlan tile_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac, int
   if ((rows + TL_M) * N * 2 >= (1LL << 32)) return pl;
   pl.lds = tl_lds_bytes(rac, rac ? (Ks + 15) / 16 * 16 : 0);
   if (pl.lds > TL_LDS_MAX) return pl;
+  // the A-scale ring where it keeps the workgroups per CU (groups of four
+  // stages: K a multiple of 256, so no group reads past a row's scales)
+  if (K % 256 == 0 && ((pl.lds <= TL_LDS_2WG && pl.lds + TL_AGRP <= TL_LDS_2WG) ||
+                       (pl.lds > TL_LDS_2WG && pl.lds + TL_AGRP <= TL_LDS_MAX))) {
+    pl.lds += TL_AGRP;
+    pl.grp = 1;
+  }
   pl.ntn = (int)(N / TL_N);
   int64_t g = ((rows + TL_M - 1) / TL_M + E) * pl.ntn;
   g = (g + 7) / 8 * 8;
@@ -1250,7 +1297,8 @@ void launch_tile(const GemmArgs &p, const TlPlan &pl, hipStream_t s) {
                                                hipFuncAttributeMaxDynamicSharedMemorySize,
                                                TL_LDS_MAX) == hipSuccess;
   (void)attr;
-  hipLaunchKernelGGL(kern, dim3((unsigned)pl.grid), dim3(TL_THREADS), (size_t)pl.lds, s, p, pl.ntn);
+  hipLaunchKernelGGL(kern, dim3((unsigned)pl.grid), dim3(TL_THREADS), (size_t)pl.lds, s, p, pl.ntn,
+                     pl.grp);
 }
 
 template <bool GATHER, bool RAC>

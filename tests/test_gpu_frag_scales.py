@@ -4,8 +4,8 @@ The copy is a pure re-layout, so the checks are exact: the packed bytes
 against a numpy transposition of the standard layout, and the grouped GEMM
 (decode-shaped batches, where the kernel reads the copy) bit for bit against
 the same call without it.  Shapes include weight-row counts that are not a
-multiple of the kernel's 256-row unit, where part of a unit's fragments lie
-past the last row.
+multiple of the decode kernel's 256-row unit, where part of a unit's
+fragments lie past the last row, and prefill shapes (the tile kernel).
 """
 
 import numpy as np
@@ -59,6 +59,9 @@ CASES = [
     ("swiglu_partial_unit_rac", 64, 512, 8, 2, 288, Q.QD_EPI_SWIGLU, 24),
     ("plain_partial_unit", 48, 512, 8, 4, 272, Q.QD_EPI_NONE, 0),
     ("swiglu_two_passes", 96, 256, 4, 2, 512, Q.QD_EPI_SWIGLU, 8),
+    # many rows per expert: the prefill tile kernel reads the copy too
+    ("tile_swiglu_rac", 512, 512, 4, 2, 256, Q.QD_EPI_SWIGLU, 16),
+    ("tile_plain", 400, 768, 4, 2, 384, Q.QD_EPI_NONE, 0),
 ]
 
 
