@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparisons", action="store_true",
                     help="skip the FP8 W8A8 layer and the K_s = 0 / 50%% rows")
+    ap.add_argument("--ks-sweep", action="store_true",
+                    help="add a K_s sweep (0, 12.5, 25, 50, 75, 100%% of the channels and the "
+                         "configured K_s): step time and compensated-activation error")
     ap.add_argument("--cpu-experts", type=int, default=0,
                     help="experts in the oracle sample (0: automatic)")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -355,6 +358,8 @@ def main():
     del graphs
     if not args.no_comparisons:
         out["comparisons"] = comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws)
+    if args.ks_sweep:
+        out["ks_sweep"] = ks_sweep(args, wl, banks, xs, lgs, ws)
     if not args.no_cpu_baseline:
         ne = args.cpu_experts or (4 if wl.H <= 2048 else 2)
         out["cpu_baseline"] = cpu_baseline(inp, ne)
@@ -409,6 +414,40 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
                          time_vs_headline=round(ms / ms_step, 3))
     torch.cuda.synchronize()
     return res
+
+
+def ks_sweep(args, wl, banks, xs, lgs, ws):
+    """Throughput against the number of compensated channels (the paper's
+    K_s sweep, Sec. 3.3 / its ablation on k): per K_s the layer's step time
+    and the relative error of the compensated activation,
+    ||x - (x_hat - r_hat_S)|| / ||x|| (x_hat, r_hat_S the dequantised NVFP4
+    activation and masked residual, all from the library's own calls)."""
+    import torch
+    from paper_2607_15810_amd import ops
+    dev = "cuda"
+    steps, warm = max(args.steps, 10), max(args.warmup, 3)
+    y = torch.empty((wl.T, wl.H), dtype=torch.bfloat16, device=dev)
+    x = xs[0]
+    xf = x.float()
+    nx = torch.linalg.vector_norm(xf).item()
+    xq, scores, ramax = ops.quantize_act(x, rac=True)
+    xhat = ops.dequantize(xq)[0]
+    points = sorted({0, wl.Ks} | {max(1, round(f * wl.H)) for f in (0.125, 0.25, 0.5, 0.75, 1.0)})
+    rows = []
+    for ks in points:
+        lays = [ops.MoELayer(b13, b2, wl.T, wl.k, ks, ws=ws) for b13, b2 in banks]
+        ms = time_steps([lambda c=c: lays[c](xs[c], lgs[c], y) for c in range(len(lays))],
+                        steps, warm)
+        comp = xhat
+        if ks:
+            _, rq, _, _ = ops.select_channels(x, xq, ks, scores, ramax)
+            comp = xhat - ops.dequantize(rq)[0]
+        err = torch.linalg.vector_norm(xf - comp).item() / max(nx, 1e-30)
+        rows.append(dict(rac_channels=ks, frac=round(ks / wl.H, 4), ms_per_step=round(ms, 5),
+                         value=round(wl.T / (ms * 1e-3), 1), act_rel_err=round(err, 6)))
+        del lays
+    torch.cuda.synchronize()
+    return rows
 
 
 if __name__ == "__main__":
