@@ -309,6 +309,52 @@ qd_status qd_fp8_moe_layer_forward(const void *x, const float *logits, int64_t T
                                    void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------
+ * MXFP4 W4A4 comparison layer: the OCP Microscaling FP4 format that CDNA4's
+ * scaled MFMA reads natively (E2M1 elements, one E8M0 power-of-two scale
+ * per 32 elements, no tensor scale), on the same routing, SwiGLU and combine
+ * as the NVFP4 layer and without residual.  It is not the paper's format:
+ * it measures what the exact NVFP4 semantics of Sec. 2.2 ("FP4" paragraph:
+ * E4M3 scale per 16 elements, FP32 tensor scale) cost on this hardware.
+ *
+ * mxfp4_quantize_rows -- per block of 32 consecutive elements of a row,
+ * with m = max |x|: s = floor(log2 m) - 2, clamped to [-127, 127] (-127 for
+ * m == 0); scale byte s + 127.  code = E2M1_RNE(|x| * 2^-s) with ties to
+ * even, saturating at 6, and the sign in bit 3.
+ *   x      : bf16 (QD_DTYPE_BF16) or f32 [rows][cols], cols % 32 == 0,
+ *            16-byte aligned.
+ *   codes  : u8 [rows][cols/2], element 2i in bits 3:0 (16-byte aligned).
+ *   scales : u8 [rows][cols/32].
+ * ------------------------------------------------------------------- */
+qd_status mxfp4_quantize_rows(const void *x, int32_t dtype, int64_t rows, int64_t cols,
+                              uint8_t *codes, uint8_t *scales, void *stream);
+
+/* ---------------------------------------------------------------------
+ * moe_mxfp4_grouped_gemm -- per expert e and grouped row r:
+ *   v[r][n] = sum_k a[src(r)][k] * w[e][n][k]   (MXFP4 values, f32 accumulation
+ *   on v_mfma_scale_f32_32x32x64_f8f6f4), epilogue as in moe_w4a4_grouped_gemm.
+ *   a_codes, a_scales : u8 [a_rows][K/2], u8 [a_rows][K/32] (4-byte aligned).
+ *   w_codes, w_scales : u8 [E][N][K/2], u8 [E][N][K/32].
+ *   row_token / offsets as in moe_w4a4_grouped_gemm.
+ * Sizes: K % 128 == 0, K >= 256; N % 256 == 0 (few rows per expert) or
+ * N % 128 == 0 (many); otherwise QD_ERR_UNSUPPORTED.
+ * ------------------------------------------------------------------- */
+qd_status moe_mxfp4_grouped_gemm(const uint8_t *a_codes, const uint8_t *a_scales, int64_t a_rows,
+                                 const int32_t *row_token, const int32_t *expert_offsets,
+                                 int32_t E, int64_t rows, const uint8_t *w_codes,
+                                 const uint8_t *w_scales, int64_t N, int64_t K, int32_t epilogue,
+                                 void *out, void *stream);
+
+/* qd_mxfp4_moe_layer_forward -- route, quantise X, W13 with SwiGLU, quantise h,
+ * W2, combine: y bf16 [T][H].  w13: [E][2I][H/2] codes and [E][2I][H/32]
+ * scales; w2: [E][H][I/2] and [E][H][I/32] (from mxfp4_quantize_rows). */
+size_t    qd_mxfp4_moe_layer_workspace(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I);
+qd_status qd_mxfp4_moe_layer_forward(const void *x, const float *logits, int64_t T, int64_t H,
+                                     int32_t E, int32_t k, int64_t I, int32_t renorm,
+                                     const uint8_t *w13_codes, const uint8_t *w13_scales,
+                                     const uint8_t *w2_codes, const uint8_t *w2_scales, void *y,
+                                     void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------
  * qd_moe_layer_forward -- the whole rollout-side layer in one call: route,
  * quantise X with fused RAC scores, select, W13 GEMM with fused residual
  * and SwiGLU, quantise h, W2 GEMM, combine.  Same results as the seven

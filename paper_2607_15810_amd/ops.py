@@ -339,3 +339,56 @@ class FP8MoELayer:
                self.w13[1].data_ptr(), self.w2[0].data_ptr(), self.w2[1].data_ptr(),
                y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), _stream())
         return y
+
+
+def mxfp4_quantize_rows(x):
+    """MXFP4 codes and E8M0 block scales of x ([..][cols] bf16 or f32,
+    cols % 32 == 0; a weight bank [E][N][K] is E*N rows).  Returns
+    (codes u8 [..][cols/2], scales u8 [..][cols/32])."""
+    _require_cuda(x)
+    x = x.contiguous()
+    cols = x.shape[-1]
+    rows = x.numel() // cols if cols else 0
+    codes = torch.empty(x.shape[:-1] + (cols // 2,), dtype=torch.uint8, device=x.device)
+    scales = torch.empty(x.shape[:-1] + (cols // 32,), dtype=torch.uint8, device=x.device)
+    dt = Q.QD_DTYPE_BF16 if x.dtype == torch.bfloat16 else Q.QD_DTYPE_F32
+    Q.call("mxfp4_quantize_rows", x.data_ptr(), dt, rows, cols, codes.data_ptr(),
+           scales.data_ptr(), _stream())
+    return codes, scales
+
+
+def mxfp4_grouped_gemm(a_codes, a_scales, w_codes, w_scales, rows, row_token=None, offsets=None,
+                       epilogue=Q.QD_EPI_NONE):
+    E, N, K2 = w_codes.shape
+    K = 2 * K2
+    ncol = N // 2 if epilogue == Q.QD_EPI_SWIGLU else N
+    out = torch.empty((rows, ncol), dtype=torch.bfloat16, device=a_codes.device)
+    Q.call("moe_mxfp4_grouped_gemm", a_codes.data_ptr(), a_scales.data_ptr(), a_codes.shape[0],
+           _ptr(row_token), _ptr(offsets), E, rows, w_codes.data_ptr(), w_scales.data_ptr(), N,
+           K, epilogue, out.data_ptr(), _stream())
+    return out
+
+
+class MXFP4MoELayer:
+    """The MXFP4 W4A4 comparison layer through qd_mxfp4_moe_layer_forward
+    (same routing, SwiGLU and combine, no residual)."""
+
+    def __init__(self, w13_codes, w13_scales, w2_codes, w2_scales, T, k, renorm=True):
+        self.w13 = (w13_codes, w13_scales)
+        self.w2 = (w2_codes, w2_scales)
+        self.E, N13, H2 = w13_codes.shape
+        self.H = 2 * H2
+        self.I = N13 // 2
+        self.T, self.k, self.renorm = T, k, renorm
+        n = Q.lib().qd_mxfp4_moe_layer_workspace(T, self.H, self.E, k, self.I)
+        self.ws = _ws(n, w13_codes.device)
+
+    def __call__(self, x, logits, y=None):
+        if y is None:
+            y = torch.empty((self.T, self.H), dtype=torch.bfloat16, device=x.device)
+        Q.call("qd_mxfp4_moe_layer_forward", x.data_ptr(), logits.data_ptr(), self.T, self.H,
+               self.E, self.k, self.I, int(self.renorm), self.w13[0].data_ptr(),
+               self.w13[1].data_ptr(), self.w2[0].data_ptr(), self.w2[1].data_ptr(),
+               y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), _stream())
+        return y
+

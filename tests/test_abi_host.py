@@ -213,3 +213,24 @@ def test_gemm_rejects_misaligned_frag_scales(lib):
                                    None, 0, None, 0, FAKE, None, None)
     assert st == Q.QD_ERR_ALIGN
 
+
+def test_mxfp4_validation(lib):
+    q = lib.mxfp4_quantize_rows
+    assert q(FAKE, 0, 4, 40, FAKE, FAKE, None) == Q.QD_ERR_SHAPE       # cols % 32
+    assert q(FAKE, 7, 4, 64, FAKE, FAKE, None) == Q.QD_ERR_DTYPE
+    assert q(None, 0, 4, 64, FAKE, FAKE, None) == Q.QD_ERR_NULL
+    assert q(FAKE + 2, 0, 4, 64, FAKE, FAKE, None) == Q.QD_ERR_ALIGN
+    assert q(None, 0, 0, 64, None, None, None) == Q.QD_OK              # empty: nothing to do
+    g = lib.moe_mxfp4_grouped_gemm
+    args = lambda K, N, ws=FAKE: (FAKE, FAKE, 64, None, FAKE, 4, 64, FAKE, ws, N, K, 0, FAKE, None)
+    assert g(*args(192, 256)) == Q.QD_ERR_UNSUPPORTED                  # K % 128
+    assert g(*args(256, 200)) == Q.QD_ERR_UNSUPPORTED                  # N % 128
+    assert g(*args(256, 256, FAKE + 2)) == Q.QD_ERR_ALIGN              # scales 4-byte aligned
+    assert g(None, FAKE, 64, None, FAKE, 4, 64, FAKE, FAKE, 256, 256, 0, FAKE, None) == Q.QD_ERR_NULL
+    assert g(FAKE, FAKE, 64, None, FAKE, 4, 64, FAKE, FAKE, 256, 256, 9, FAKE, None) == Q.QD_ERR_DTYPE
+    lw = lib.qd_mxfp4_moe_layer_workspace
+    assert lw(16, 256, 4, 2, 256) > 0
+    f = lib.qd_mxfp4_moe_layer_forward
+    assert f(FAKE, FAKE, 16, 256, 4, 2, 256, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16,
+             None) == Q.QD_ERR_WORKSPACE
+
