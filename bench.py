@@ -50,7 +50,7 @@ def parse():
     ap.add_argument("--copies", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparisons", action="store_true",
-                    help="skip the FP8 W8A8 layer and the K_s = 0 / 50%% rows")
+                    help="skip the FP8 / MXFP4 layers and the K_s = 0 / 50%% rows")
     ap.add_argument("--ks-sweep", action="store_true",
                     help="add a K_s sweep (0, 12.5, 25, 50, 75, 100%% of the channels and the "
                          "configured K_s): step time and compensated-activation error")
@@ -385,8 +385,9 @@ def time_steps(fns, steps, warmup):
 
 def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
     """The measurement rows beside the headline: the FP8 W8A8 layer (same
-    routing and shapes, per-token / per-channel E4M3, no residual), the plain
-    W4A4 layer (K_s = 0) and RAC at K_s = 50% of the channels."""
+    routing and shapes, per-token / per-channel E4M3, no residual), the
+    MXFP4 W4A4 layer (the hardware's native FP4 format, no residual), the
+    plain NVFP4 W4A4 layer (K_s = 0) and RAC at K_s = 50% of the channels."""
     import torch
     from paper_2607_15810_amd import ops
     dev = "cuda"
@@ -404,6 +405,18 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
                            unit="tokens/s", nvfp4_rac_speedup=round(ms8 / ms_step, 3),
                            weight_bytes_per_param=1.0)
     del lay8, f8, w13c, w13d, w2c, w2d
+    # MXFP4 W4A4 layer (E8M0 per 32 elements, the FP4 MFMA's own block
+    # scales; no tensor scale, no residual): what exact NVFP4 costs here
+    m13c, m13s = ops.mxfp4_quantize_rows(inp.w13.to(dev))
+    m2c, m2s = ops.mxfp4_quantize_rows(inp.w2.to(dev))
+    mx = [(m13c, m13s, m2c, m2s)] + [tuple(t.clone() for t in (m13c, m13s, m2c, m2s))
+                                     for _ in range(len(banks) - 1)]
+    laym = [ops.MXFP4MoELayer(*b, wl.T, wl.k) for b in mx]
+    msm = time_steps([lambda c=c: laym[c](xs[c], lgs[c], y) for c in range(len(mx))], steps, warm)
+    res["mxfp4_w4a4"] = dict(ms_per_step=round(msm, 5), value=round(wl.T / (msm * 1e-3), 1),
+                             unit="tokens/s", nvfp4_rac_speedup=round(msm / ms_step, 3),
+                             weight_bytes_per_param=0.53125)
+    del laym, mx, m13c, m13s, m2c, m2s
     # the NVFP4 layer without RAC and with K_s = H / 2 (the paper's k = 50%)
     for name, ks in (("w4a4_ks0", 0), ("rac_ks_half", wl.H // 2)):
         lays = [ops.MoELayer(b13, b2, wl.T, wl.k, ks, ws=ws) for b13, b2 in banks]
