@@ -24,6 +24,7 @@
 // K order inside every MFMA).
 #include "common.h"
 #include "lds_dma.h"
+#include "tile_sched.h"
 
 namespace {
 
@@ -133,56 +134,10 @@ __global__ __launch_bounds__(F8_THREADS, 2) void gemm_fp8_kernel(Fp8Args p, int 
   const int tid = threadIdx.x, lane = tid & 63, w = (int)uni((uint32_t)tid >> 6);
   const int K = p.K, N = p.N, E = p.E;
 
-  // ---- M-tiles per expert (exclusive scan, four experts per thread)
-  int cnt[4], tsum = 0;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int e = 4 * tid + q;
-    int c = 0;
-    if (p.offsets) c = e < E ? p.offsets[e + 1] - p.offsets[e] : 0;
-    else c = e == 0 ? (int)p.rows : 0;
-    cnt[q] = (max(c, 0) + TM - 1) / TM;
-    tsum += cnt[q];
-  }
-  int xs = tsum;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(xs, o, 64);
-    if (lane >= o) xs += y;
-  }
-  if (lane == 63) sh_w[w] = xs;
-  if (tid == 0) sh_t[0] = -1;
-  __syncthreads();
-  const int mt_total = sh_w[0] + sh_w[1] + sh_w[2] + sh_w[3];
-  const int b = blockIdx.x;
-  const int ntile = mt_total * ntn;
-  const int per = (ntile + 7) >> 3;
-  const int slot = b >> 3;
-  const int L = (b & 7) * per + slot;
-  const bool live = slot < per && L < ntile;
-  const int mt = live ? L / ntn : -1, nt = live ? L - (L / ntn) * ntn : 0;
-  {
-    int base = xs - tsum;
-    for (int ww = 0; ww < w; ++ww) base += sh_w[ww];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (mt >= base && mt < base + cnt[q]) {
-        const int e = 4 * tid + q;
-        const int o0 = p.offsets ? p.offsets[e] : 0;
-        const int o1 = p.offsets ? p.offsets[e + 1] : (int)p.rows;
-        const int r0 = o0 + (mt - base) * TM;
-        sh_t[0] = e;
-        sh_t[1] = r0;
-        sh_t[2] = min(TM, o1 - r0);
-      }
-      base += cnt[q];
-    }
-  }
-  __syncthreads();
-  const int e = (int)uni((uint32_t)sh_t[0]);
+  const qdt::Tile tl = qdt::find_tile<TM>(p.offsets, p.E, p.rows, ntn, sh_w, sh_t);
+  const int e = tl.e;
   if (e < 0) return;
-  const int row0 = (int)uni((uint32_t)sh_t[1]);
-  const int nrows = (int)uni((uint32_t)sh_t[2]);
+  const int row0 = tl.row0, nrows = tl.nrows, nt = tl.nt;
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   float *sa = reinterpret_cast<float *>(lds + NS * C::STAGE);     // [TM] activation row scales
   float *sw = sa + TM;                                            // [NT] weight row scales
@@ -363,8 +318,7 @@ inline F8Plan fp8_plan(int64_t rows, int E, int64_t N, int64_t K, int epilogue) 
     return pl;
   pl.ntn = (int)(N / nt);
   pl.lds = pl.tm == 256 ? F8Cfg<256>::LDS : F8Cfg<32>::LDS;
-  int64_t g = ((rows + pl.tm - 1) / pl.tm + E) * pl.ntn;
-  g = (g + 7) / 8 * 8;
+  const int64_t g = qdt::tile_grid(rows, E, pl.tm, pl.ntn);
   if (g > 0x7fffffffLL) return pl;
   pl.grid = (int)g;
   pl.ok = true;
