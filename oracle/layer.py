@@ -6,13 +6,19 @@ the paper; readings, parity unpinned by the paper):
   L4  per expert e, rows [off_e, off_{e+1}):  [g; u] = x~[row_token] W13_hat[e]^T
       (float64; W13[e] is [2I][H], gate rows [0, I), up rows [I, 2I));
       h = bf16_RNE(silu(g) * u), silu(g) = g / (1 + exp(-g)).
-  L5  h_hat = Q_A(h) (plain NVFP4, no RAC: RAC sits at the W13 activation
-      site, Sec. 3.3 "profiled W13 activation site");
+  L5  h_hat = Q_A(h) (plain NVFP4; the paper profiles RAC at the W13
+      activation site only, Sec. 3.3);
       z = bf16_RNE(h_hat W2_hat[e]^T) (float64 product, W2[e] is [H][I]; the
       expert outputs are held as bf16 between the down projection and the
       combine);
       y[t] = sum_s w[t, s] * z[inv_row[t, s]] (float64), s = 0..k-1; the
       layer output is bf16_RNE(y).
+  L6  Optional RAC at the W2 input as well (K_s2 > 0; an extension the
+      paper's method admits at any activation site, Sec. 3.3): h goes
+      through the same steps A3-A5 as X, with the R = T*k permuted rows of h
+      as the batch (one channel set shared by all experts), and
+      z = bf16_RNE((h_hat - M_S (.) Q_A(dh_q)) W2_hat[e]^T) as in
+      Eq. (residual-recon).
 
 Stage functions take the previous stage's values explicitly so the tests can
 teacher-force them with the GPU's own intermediates (bf16 h, z), and return
@@ -93,10 +99,15 @@ def swiglu(gu, I):
     return bf16_round_f64(silu(g) * u)
 
 
-def w2_stage(hq, offsets, w2, rows=None):
-    """A8: z = h_hat W2_hat[e]^T for the permuted rows."""
+def w2_stage(hq, offsets, w2, rows=None, rq=None):
+    """A8: z = h_hat W2_hat[e]^T for the permuted rows.  rq (L6): the masked
+    residual of h, subtracted from h_hat before the contraction; the abs-sum
+    then counts both terms."""
     hh = quant.dequantize_f64(hq["codes"], hq["scales"], hq["s_dec"])
-    return grouped_gemm(hh, None, offsets, w2, rows=rows)
+    if rq is None:
+        return grouped_gemm(hh, None, offsets, w2, rows=rows)
+    rh = quant.dequantize_f64(rq["codes"], rq["scales"], rq["s_dec"])
+    return grouped_gemm(hh - rh, None, offsets, w2, rows=rows, a_abs_src=np.abs(hh) + np.abs(rh))
 
 
 def combine(z, inv_row, w, tokens=None):
@@ -117,11 +128,12 @@ def combine(z, inv_row, w, tokens=None):
     return y, mag
 
 
-def moe_layer(x, logits, w13, w2, k, Ks, renorm=True):
+def moe_layer(x, logits, w13, w2, k, Ks, renorm=True, Ks2=0):
     """Free-running forward of the whole layer (A1-A9).
 
     x: float32 [T][H] (bf16-valued); logits float32 [T][E];
-    w13 / w2: quantised banks from quant.quantize_weight_bank.
+    w13 / w2: quantised banks from quant.quantize_weight_bank;
+    Ks2: channels of h compensated at the W2 input (L6; 0: none).
     Returns a dict of every intermediate.
     """
     x = np.asarray(x, dtype=np.float32)
@@ -134,10 +146,14 @@ def moe_layer(x, logits, w13, w2, k, Ks, renorm=True):
     act = rac.rac_activation(x, Ks)
     gu, gu_mag = w13_stage(act["xq"], act["rq"], perm["row_token"], perm["offsets"], w13)
     h = swiglu(gu, I)
-    hq = quant.quantize(h.astype(np.float32))
-    z, z_mag = w2_stage(hq, perm["offsets"], w2)
+    if Ks2 > 0:
+        act2 = rac.rac_activation(h.astype(np.float32), Ks2)
+        hq, rq2 = act2["xq"], act2["rq"]
+    else:
+        act2, hq, rq2 = None, quant.quantize(h.astype(np.float32)), None
+    z, z_mag = w2_stage(hq, perm["offsets"], w2, rq=rq2)
     zb = bf16_round_f64(z)
     y, y_mag = combine(zb, perm["inv_row"], wts)
     return dict(ids=ids, w=wts, **perm, act=act, gu=gu, gu_mag=gu_mag, h=h,
-                hq=hq, z=z, zb=zb, z_mag=z_mag, y=y, y_mag=y_mag,
+                hq=hq, act2=act2, z=z, zb=zb, z_mag=z_mag, y=y, y_mag=y_mag,
                 yb=bf16_round_f64(y))

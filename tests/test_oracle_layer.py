@@ -104,6 +104,51 @@ def test_layer_against_brute_force():
     assert np.allclose(out["y"], y, rtol=1e-12, atol=1e-15)
 
 
+def test_layer_w2_site_rac_brute_force():
+    """L6: RAC at the W2 input, checked per (token, slot) without the
+    permutation.  The statistics of h (amax, channel scores, the residual's
+    amax) are taken over all T*k rows, in any order, so the rows are stacked
+    in (token, slot) order here; each row's W2 input is then its own
+    reconstruction h_hat - r_S, and the residual must lower the error of z
+    against the unquantised h."""
+    T, H, E, k, I, Ks, Ks2 = 10, 64, 4, 2, 32, 6, 8
+    x, logits, w13, w2 = _case(4, T, H, E, k, I)
+    out = layer.moe_layer(x, logits, w13, w2, k, Ks, Ks2=Ks2)
+    plain = layer.moe_layer(x, logits, w13, w2, k, Ks)
+    act = rac.rac_activation(x, Ks)
+    xt = rac.reconstruct(act["xq"], act["rq"])
+    ids = route.topk(logits, k)
+    w = route.weights(logits, ids, True)
+    hrows = []
+    for t in range(T):
+        for s in range(k):
+            gu = layer.dequant_bank_f64(w13, ids[t, s]) @ xt[t]
+            g, u = gu[:I], gu[I:]
+            hrows.append(formats.bf16_round_f64(g / (1 + np.exp(-g)) * u))
+    hm = np.array(hrows)
+    act2 = rac.rac_activation(hm.astype(np.float32), Ks2)
+    assert np.array_equal(out["act2"]["sel"], act2["sel"])
+    ht = rac.reconstruct(act2["xq"], act2["rq"])
+    y = np.zeros((T, H))
+    err_rac = err_plain = 0.0
+    for t in range(T):
+        for s in range(k):
+            W = layer.dequant_bank_f64(w2, ids[t, s])
+            z = formats.bf16_round_f64(W @ ht[t * k + s])
+            y[t] += w[t, s] * z
+    assert np.allclose(out["y"], y, rtol=1e-12, atol=1e-15)
+    # z with the W2-site residual sits closer to h W2_hat^T than plain W4A4 z
+    exact = np.zeros_like(out["z"])
+    for r in range(T * k):
+        e = int(np.searchsorted(out["offsets"], r, side="right") - 1)
+        exact[r] = layer.dequant_bank_f64(w2, e) @ out["h"][r]
+    err_rac = np.linalg.norm(out["z"] - exact)
+    # the plain layer's h equals this one's (RAC at W2 changes nothing upstream)
+    assert np.array_equal(plain["h"], out["h"])
+    err_plain = np.linalg.norm(plain["z"] - exact)
+    assert err_rac < err_plain
+
+
 def test_fp8_rows_and_gemm():
     rng = np.random.default_rng(3)
     x = _bf16(rng.standard_normal((6, 32)) * 3)
