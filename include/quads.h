@@ -363,6 +363,13 @@ qd_status qd_mxfp4_moe_layer_forward(const void *x, const float *logits, int64_t
  *   x      : bf16 [T][H]; logits: f32 [T][E];
  *   w13    : E groups of [2I][H]; w2: E groups of [H][I];
  *   y      : bf16 [T][H];
+ *   Ks     : channels of X compensated at the W13 input (0 <= Ks <= H).
+ *   Ks2    : channels of h compensated at the W2 input (0 <= Ks2 <= I; 0
+ *            is the paper's configuration).  With Ks2 > 0, h is quantised
+ *            with its channel scores (a fresh amax pass over h), the top
+ *            Ks2 channels are selected over all T*k rows (one set for all
+ *            experts) and the W2 GEMM takes the masked residual as W13
+ *            does, Sec. 3.3, Eq. (residual-recon).
  *   ws     : at least qd_moe_layer_workspace(T, H, E, k, I) bytes; the
  *            intermediates live there (see qd_moe_layer_views).
  * Errors: QD_ERR_SHAPE as the calls above (E <= 1024, k <= 32);
@@ -370,7 +377,8 @@ qd_status qd_mxfp4_moe_layer_forward(const void *x, const float *logits, int64_t
  * ------------------------------------------------------------------- */
 size_t    qd_moe_layer_workspace(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I);
 qd_status qd_moe_layer_forward(const void *x, const float *logits, int64_t T, int64_t H,
-                               int32_t E, int32_t k, int64_t I, int32_t Ks, int32_t renorm,
+                               int32_t E, int32_t k, int64_t I, int32_t Ks, int32_t Ks2,
+                               int32_t renorm,
                                const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y,
                                void *ws, size_t ws_bytes, void *stream);
 
@@ -382,14 +390,17 @@ qd_status qd_moe_layer_forward(const void *x, const float *logits, int64_t T, in
  * With the shared launches the first three stages are: ROUTE = routing
  * top-k with the amax pass over X; QUANT_X = routing ranks with the X
  * quantiser; SELECT = routing scatter with the channel selection, then the
- * masked residual (scatter alone when Ks == 0).  events NULL: no recording.
+ * masked residual (scatter alone when Ks == 0).  With Ks2 > 0, QUANT_H
+ * also holds the W2-site selection and masked residual.  events NULL: no
+ * recording.
  */
 enum {
   QD_STAGE_ROUTE = 0, QD_STAGE_QUANT_X, QD_STAGE_SELECT, QD_STAGE_W13, QD_STAGE_QUANT_H,
   QD_STAGE_W2, QD_STAGE_COMBINE, QD_STAGE_COUNT
 };
 qd_status qd_moe_layer_forward_timed(const void *x, const float *logits, int64_t T, int64_t H,
-                                     int32_t E, int32_t k, int64_t I, int32_t Ks, int32_t renorm,
+                                     int32_t E, int32_t k, int64_t I, int32_t Ks, int32_t Ks2,
+                                     int32_t renorm,
                                      const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y,
                                      void *ws, size_t ws_bytes, void *const *events,
                                      void *stream);
@@ -404,7 +415,8 @@ enum {
   QD_VIEW_XQ_CODES, QD_VIEW_XQ_SCALES, QD_VIEW_XQ_GSCALE, QD_VIEW_SCORES, QD_VIEW_RAMAX,
   QD_VIEW_SEL, QD_VIEW_RQ_CODES, QD_VIEW_RQ_SCALES, QD_VIEW_RQ_GSCALE, QD_VIEW_H,
   QD_VIEW_H_AMAX, QD_VIEW_HQ_CODES, QD_VIEW_HQ_SCALES, QD_VIEW_HQ_GSCALE, QD_VIEW_Z,
-  QD_VIEW_RQ_SEL, QD_VIEW_COUNT
+  QD_VIEW_RQ_SEL, QD_VIEW_H_SCORES, QD_VIEW_H_RAMAX, QD_VIEW_SEL2, QD_VIEW_HR_CODES,
+  QD_VIEW_HR_SCALES, QD_VIEW_HR_GSCALE, QD_VIEW_HR_SEL, QD_VIEW_COUNT
 };
 qd_status qd_moe_layer_views(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I,
                              int64_t *off /* host, QD_VIEW_COUNT */);

@@ -90,7 +90,7 @@ __global__ __launch_bounds__(256) void layer_compact_kernel(
 
 struct Layout {
   int64_t off[QD_VIEW_COUNT];
-  int64_t route_ws, q1_ws, sel_ws, q2_ws, total;
+  int64_t route_ws, q1_ws, sel_ws, q2_ws, sel2_ws, total;
 };
 
 Layout make_layout(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I) {
@@ -136,6 +136,16 @@ Layout make_layout(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I) {
   L.q2_ws = blob((int64_t)nvfp4_quantize_act_workspace(R, I));
   put(QD_VIEW_Z, R * H * 2);
   put(QD_VIEW_RQ_SEL, T * H * 2);       // the compact residual, K_s <= H columns
+  // RAC at the W2 input (K_s2 > 0): statistics, selection and masked
+  // residual of h over the R permuted rows
+  put(QD_VIEW_H_SCORES, I * 8);
+  put(QD_VIEW_H_RAMAX, 4);
+  put(QD_VIEW_SEL2, I * 4);
+  L.sel2_ws = blob((int64_t)rac_select_channels_workspace(R, I));
+  put(QD_VIEW_HR_CODES, R * I / 2);
+  put(QD_VIEW_HR_SCALES, R * I / 16);
+  put(QD_VIEW_HR_GSCALE, 8);
+  put(QD_VIEW_HR_SEL, R * (int64_t)rac_selected_width((int32_t)I) * 2);
   L.total = o;
   return L;
 }
@@ -158,22 +168,22 @@ extern "C" qd_status qd_moe_layer_views(int64_t T, int64_t H, int32_t E, int32_t
 
 extern "C" qd_status qd_moe_layer_forward(const void *x, const float *logits, int64_t T,
                                           int64_t H, int32_t E, int32_t k, int64_t I,
-                                          int32_t Ks, int32_t renorm, const qd_nvfp4 *w13,
-                                          const qd_nvfp4 *w2, void *y, void *ws,
-                                          size_t ws_bytes, void *stream) {
-  return qd_moe_layer_forward_timed(x, logits, T, H, E, k, I, Ks, renorm, w13, w2, y, ws,
+                                          int32_t Ks, int32_t Ks2, int32_t renorm,
+                                          const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y,
+                                          void *ws, size_t ws_bytes, void *stream) {
+  return qd_moe_layer_forward_timed(x, logits, T, H, E, k, I, Ks, Ks2, renorm, w13, w2, y, ws,
                                     ws_bytes, nullptr, stream);
 }
 
 extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logits, int64_t T,
                                                 int64_t H, int32_t E, int32_t k, int64_t I,
-                                                int32_t Ks, int32_t renorm, const qd_nvfp4 *w13,
-                                                const qd_nvfp4 *w2, void *y, void *ws,
-                                                size_t ws_bytes, void *const *events,
-                                                void *stream) {
+                                                int32_t Ks, int32_t Ks2, int32_t renorm,
+                                                const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y,
+                                                void *ws, size_t ws_bytes,
+                                                void *const *events, void *stream) {
   if (!w13 || !w2) return QD_ERR_NULL;
   if (T < 0 || H <= 0 || H % 32 || I <= 0 || I % 32 || E < 1 || k < 1 || k > E) return QD_ERR_SHAPE;
-  if (Ks < 0 || Ks > H) return QD_ERR_SHAPE;
+  if (Ks < 0 || Ks > H || Ks2 < 0 || Ks2 > I) return QD_ERR_SHAPE;
   // routing limits (as moe_route_permute) and the fused channel selection
   if (E > qdr::kMaxE || k > qdr::kMaxK || T * (int64_t)k > 0x7fffffffLL) return QD_ERR_SHAPE;
   if (Ks > 0 && H > qdc::kSelMaxK) return QD_ERR_UNSUPPORTED;
@@ -288,16 +298,38 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   qd_nvfp4 hq{(uint8_t *)P(QD_VIEW_HQ_CODES), (uint8_t *)P(QD_VIEW_HQ_SCALES),
               (float *)P(QD_VIEW_HQ_GSCALE), 1, R, I};
   mark(QD_STAGE_QUANT_H);
-  st = nvfp4_quantize_act(h, QD_DTYPE_BF16, R, I, hamax,
-                          moe_w4a4_grouped_gemm_amax_count(R, 2 * I, H, E, Ks, QD_EPI_SWIGLU), &hq,
-                          nullptr, nullptr, b + L.q2_ws, nvfp4_quantize_act_workspace(R, I),
-                          stream);
-  if (st) return st;
+  const bool rac2 = Ks2 > 0;
+  qd_nvfp4 hr{(uint8_t *)P(QD_VIEW_HR_CODES), (uint8_t *)P(QD_VIEW_HR_SCALES),
+              (float *)P(QD_VIEW_HR_GSCALE), 1, R, I};
+  int32_t *sel2 = (int32_t *)P(QD_VIEW_SEL2);
+  void *hr_sel = nullptr;
+  if (!rac2) {
+    st = nvfp4_quantize_act(h, QD_DTYPE_BF16, R, I, hamax,
+                            moe_w4a4_grouped_gemm_amax_count(R, 2 * I, H, E, Ks, QD_EPI_SWIGLU),
+                            &hq, nullptr, nullptr, b + L.q2_ws,
+                            nvfp4_quantize_act_workspace(R, I), stream);
+    if (st) return st;
+  } else {
+    // the scored quantiser takes its own amax pass over h (which also
+    // clears the score accumulators), then the W2-site selection
+    uint64_t *hscores = (uint64_t *)P(QD_VIEW_H_SCORES);
+    float *hramax = (float *)P(QD_VIEW_H_RAMAX);
+    st = nvfp4_quantize_act(h, QD_DTYPE_BF16, R, I, nullptr, 0, &hq, hscores, hramax,
+                            b + L.q2_ws, nvfp4_quantize_act_workspace(R, I), stream);
+    if (st) return st;
+    st = rac_select_channels(h, &hq, Ks2, hscores, hramax, 1, sel2, &hr, b + L.sel2_ws,
+                             rac_select_channels_workspace(R, I), stream);
+    if (st) return st;
+    if (qdi::gemm_wants_rq_sel(R, E, H, I, Ks2, QD_EPI_NONE)) {
+      hr_sel = P(QD_VIEW_HR_SEL);
+      st = rac_gather_selected(&hr, sel2, Ks2, hr_sel, stream);
+      if (st) return st;
+    }
+  }
   uint16_t *z = (uint16_t *)P(QD_VIEW_Z);
   mark(QD_STAGE_W2);
-  st = moe_w4a4_grouped_gemm(&hq, nullptr, offs, E, R, w2, nullptr, nullptr, 0, nullptr,
-                             QD_EPI_NONE, z,
-                             nullptr, stream);
+  st = moe_w4a4_grouped_gemm(&hq, nullptr, offs, E, R, w2, rac2 ? &hr : nullptr,
+                             rac2 ? sel2 : nullptr, Ks2, hr_sel, QD_EPI_NONE, z, nullptr, stream);
   if (st) return st;
   mark(QD_STAGE_COMBINE);
   st = moe_unpermute_combine(z, inv_row, wts, T, k, H, y, stream);

@@ -220,12 +220,13 @@ class MoELayer:
     """The whole layer through qd_moe_layer_forward, with a reusable
     workspace; `views()` exposes the intermediates of the last call."""
 
-    def __init__(self, w13, w2, T, k, Ks, renorm=True, ws=None):
+    def __init__(self, w13, w2, T, k, Ks, renorm=True, ws=None, Ks2=0):
+        """Ks: channels compensated at the W13 input; Ks2: at the W2 input."""
         self.w13, self.w2 = w13, w2
         self.E = w13.groups
         self.I = w13.rows // 2
         self.H = w13.cols
-        self.T, self.k, self.Ks, self.renorm = T, k, Ks, renorm
+        self.T, self.k, self.Ks, self.Ks2, self.renorm = T, k, Ks, Ks2, renorm
         dev = w13.codes.device
         n = Q.lib().qd_moe_layer_workspace(T, self.H, self.E, k, self.I)
         self.ws = _ws(n, dev) if ws is None else ws
@@ -249,9 +250,9 @@ class MoELayer:
         if events is not None:
             evp = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
         Q.call("qd_moe_layer_forward_timed", x.data_ptr(), logits.data_ptr(), self.T, self.H,
-               self.E, self.k, self.I, self.Ks, int(self.renorm), ctypes.byref(self._s13),
-               ctypes.byref(self._s2), y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), evp,
-               _stream())
+               self.E, self.k, self.I, self.Ks, self.Ks2, int(self.renorm),
+               ctypes.byref(self._s13), ctypes.byref(self._s2), y.data_ptr(),
+               self.ws.data_ptr(), self.ws.numel(), evp, _stream())
         return y
 
     def view(self, name, dtype, shape):
@@ -287,6 +288,14 @@ class MoELayer:
             hq_gscale=self.view("hq_gscale", f32, (2,)),
             z=self.view("z", torch.bfloat16, (R, H)),
             rq_sel=self.view("rq_sel", torch.float16, (T, Q.lib().rac_selected_width(self.Ks))),
+            h_scores=self.view("h_scores", torch.int64, (I,)),
+            h_ramax=self.view("h_ramax", f32, (1,)),
+            sel2=self.view("sel2", i32, (self.Ks2,)),
+            hr_codes=self.view("hr_codes", u8, (R, I // 2)),
+            hr_scales=self.view("hr_scales", u8, (R, I // 16)),
+            hr_gscale=self.view("hr_gscale", f32, (2,)),
+            hr_sel=self.view("hr_sel", torch.float16,
+                             (R, Q.lib().rac_selected_width(self.Ks2))),
         )
 
 

@@ -29,7 +29,8 @@ STAGE_NAMES = ["route", "quant_x", "select", "w13", "quant_h", "w2", "combine"]
 
 VIEW_NAMES = ["topk_ids", "topk_w", "offsets", "row_token", "inv_row", "xq_codes",
               "xq_scales", "xq_gscale", "scores", "ramax", "sel", "rq_codes", "rq_scales",
-              "rq_gscale", "h", "h_amax", "hq_codes", "hq_scales", "hq_gscale", "z", "rq_sel"]
+              "rq_gscale", "h", "h_amax", "hq_codes", "hq_scales", "hq_gscale", "z", "rq_sel",
+              "h_scores", "h_ramax", "sel2", "hr_codes", "hr_scales", "hr_gscale", "hr_sel"]
 
 
 class NVFP4(ctypes.Structure):
@@ -93,11 +94,11 @@ SIGNATURES = {
                                            c_void_p]),
     "qd_moe_layer_workspace": (c_size_t, [c_int64, c_int64, c_int32, c_int32, c_int64]),
     "qd_moe_layer_forward": (c_int, [c_void_p, c_void_p, c_int64, c_int64, c_int32, c_int32,
-                                     c_int64, c_int32, c_int32, PN, PN, c_void_p, c_void_p,
-                                     c_size_t, c_void_p]),
+                                     c_int64, c_int32, c_int32, c_int32, PN, PN, c_void_p,
+                                     c_void_p, c_size_t, c_void_p]),
     "qd_moe_layer_forward_timed": (c_int, [c_void_p, c_void_p, c_int64, c_int64, c_int32,
-                                           c_int32, c_int64, c_int32, c_int32, PN, PN, c_void_p,
-                                           c_void_p, c_size_t, c_void_p, c_void_p]),
+                                           c_int32, c_int64, c_int32, c_int32, c_int32, PN, PN,
+                                           c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]),
     "qd_moe_layer_views": (c_int, [c_int64, c_int64, c_int32, c_int32, c_int64,
                                    POINTER(c_int64)]),
 }

@@ -170,6 +170,15 @@ def test_layer_workspace_and_views(lib):
     o = list(off)
     assert o == sorted(o) and len(set(o)) == len(o)
     assert all(v % 256 == 0 for v in o) and o[-1] < n
+    # channel counts outside [0, H] (W13 site) and [0, I] (W2 site)
+    F = 1 << 20
+    w13 = Q.NVFP4(F, F, F, 4, 128, 256)
+    w2 = Q.NVFP4(F, F, F, 4, 256, 64)
+    f = lambda Ks, Ks2: Q.raw("qd_moe_layer_forward", F, F, 16, 256, 4, 2, 64, Ks, Ks2, 1,
+                              ctypes.byref(w13), ctypes.byref(w2), F, F, 1 << 30, None)
+    assert f(257, 0) == Q.QD_ERR_SHAPE
+    assert f(8, 65) == Q.QD_ERR_SHAPE
+    assert f(8, -1) == Q.QD_ERR_SHAPE
 
 
 def test_injected_launch_failure():

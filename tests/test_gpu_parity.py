@@ -174,6 +174,72 @@ def test_layer_stagewise_small(case):
     assert rel <= 1e-3, f"free-running rel-L2 {rel:.3e}"
 
 
+W2RAC = [
+    # name, T, H, E, k, I, Ks, Ks2, kwargs: RAC at the W2 input as well
+    # (the decode kernel with K = I = 256, the tile kernel with the compact
+    # residual, every channel of h, and skewed routing with edge values)
+    ("w2rac_skinny", 64, 256, 8, 2, 256, 8, 16, {}),
+    ("w2rac_tile", 256, 256, 4, 2, 128, 8, 24, {}),
+    ("w2rac_all_ks0", 64, 256, 8, 2, 64, 0, 64, {}),
+    ("w2rac_zipf_edges", 300, 512, 8, 2, 128, 40, 20,
+     dict(routing="zipf", acts="student_t3", edge_cases=True, outlier_frac=0.0)),
+]
+
+
+@pytest.mark.parametrize("case", W2RAC, ids=[c[0] for c in W2RAC])
+def test_layer_w2_site_rac(case):
+    name, T, H, E, k, I, Ks, Ks2, kw = case
+    inp = synth.small_moe(name, T, H, E, k, I, Ks, seed=zlib.crc32(name.encode()) % 1000, **kw)
+    x = inp.x.to(DEV)
+    logits = inp.logits.to(DEV)
+    lg = inp.logits.numpy()
+    w13 = ops.quantize_weight(inp.w13.to(DEV))
+    w2 = ops.quantize_weight(inp.w2.to(DEV))
+    W13, W2 = oracle_bank(inp.w13), oracle_bank(inp.w2)
+    xf = np_bf16(inp.x)
+    full = OL.moe_layer(xf, lg, W13, W2, k, Ks, Ks2=Ks2)
+    R = T * k
+    offs = torch.from_numpy(full["offsets"].astype(np.int32)).to(DEV)
+    # A3-A5 at the W2 site on the oracle's h: bit-exact
+    h_or = full["h"].astype(np.float32)
+    act2 = full["act2"]
+    hq, sc, ra = ops.quantize_act(bf16_tensor(h_or), rac=True)
+    assert_nvfp4_equal(hq, act2["xq"], "hq")
+    assert np.array_equal(sc.cpu().numpy().view(np.uint64), act2["scores"])
+    assert ra.item() == np.max(np.abs(act2["r"]))
+    sel, hr, _, _ = ops.select_channels(bf16_tensor(h_or), hq, Ks2, sc, ra)
+    assert np.array_equal(sel.cpu().numpy(), act2["sel"])
+    assert_nvfp4_equal(hr, act2["rq"], "hr")
+    # A8 with the residual on the oracle's operands
+    sel_or = torch.from_numpy(act2["sel"].astype(np.int32)).to(DEV)
+    z, _ = ops.grouped_gemm(upload_nvfp4(act2["xq"]), w2, R, None, offs,
+                            upload_nvfp4(act2["rq"]), sel_or)
+    ref_z, mag_z = OL.w2_stage(act2["xq"], full["offsets"], W2, rq=act2["rq"])
+    check_close_bf16(np_bf16(z), ref_z, mag_z, "z (W2-site RAC)")
+    # the layer call equals the GPU op-by-op sequence from its own h
+    lay = ops.MoELayer(w13, w2, T, k, Ks, Ks2=Ks2)
+    y = lay(x, logits)
+    torch.cuda.synchronize()
+    v = lay.views()
+    hq_g, sc_g, ra_g = ops.quantize_act(v["h"], rac=True)
+    sel_g, hr_g, _, _ = ops.select_channels(v["h"], hq_g, Ks2, sc_g, ra_g)
+    assert torch.equal(v["hq_codes"], hq_g.codes[0])
+    assert torch.equal(v["h_scores"], sc_g)
+    assert torch.equal(v["sel2"], sel_g)
+    assert torch.equal(v["hr_codes"], hr_g.codes[0])
+    assert torch.equal(v["hr_scales"], hr_g.scales[0])
+    zg, _ = ops.grouped_gemm(hq_g, w2, R, None, v["offsets"], hr_g, sel_g)
+    yg = ops.unpermute_combine(zg, v["inv_row"], v["w"])
+    assert torch.equal(y.view(torch.int16), yg.view(torch.int16))
+    # free-running against the oracle's layer
+    yb = full["yb"]
+    rel = np.linalg.norm(np_bf16(y) - yb) / max(np.linalg.norm(yb), 1e-30)
+    assert rel <= 1e-3, f"free-running rel-L2 {rel:.3e}"
+    # and the W2-site residual is live: the output differs from K_s2 = 0
+    y0 = ops.MoELayer(w13, w2, T, k, Ks)(x, logits)
+    assert not torch.equal(y0, y)
+
+
 def test_dense_gemm_with_rac():
     """16 tokens x K=256 x N=128, 4 outlier channels x30, RAC on 8 channels."""
     inp = synth.generate("dense_t16_k256_n128")
