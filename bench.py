@@ -387,7 +387,8 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
     """The measurement rows beside the headline: the FP8 W8A8 layer (same
     routing and shapes, per-token / per-channel E4M3, no residual), the
     MXFP4 W4A4 layer (the hardware's native FP4 format, no residual), the
-    plain NVFP4 W4A4 layer (K_s = 0) and RAC at K_s = 50% of the channels."""
+    plain NVFP4 W4A4 layer (K_s = 0), RAC at K_s = 50% of the channels, and
+    RAC at both the W13 and the W2 inputs."""
     import torch
     from paper_2607_15810_amd import ops
     dev = "cuda"
@@ -417,14 +418,19 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
                              unit="tokens/s", nvfp4_rac_speedup=round(msm / ms_step, 3),
                              weight_bytes_per_param=0.53125)
     del laym, mx, m13c, m13s, m2c, m2s
-    # the NVFP4 layer without RAC and with K_s = H / 2 (the paper's k = 50%)
-    for name, ks in (("w4a4_ks0", 0), ("rac_ks_half", wl.H // 2)):
-        lays = [ops.MoELayer(b13, b2, wl.T, wl.k, ks, ws=ws) for b13, b2 in banks]
+    # the NVFP4 layer without RAC, with K_s = H / 2 (the paper's k = 50%),
+    # and with RAC at the W2 input too (the same fraction of I channels)
+    ks2 = max(1, round(wl.Ks * wl.I / wl.H)) if wl.Ks else 0
+    for name, ks, k2 in (("w4a4_ks0", 0, 0), ("rac_ks_half", wl.H // 2, 0),
+                         ("rac_w13_and_w2", wl.Ks, ks2)):
+        lays = [ops.MoELayer(b13, b2, wl.T, wl.k, ks, ws=ws, Ks2=k2) for b13, b2 in banks]
         ms = time_steps([lambda c=c: lays[c](xs[c], lgs[c], y) for c in range(len(lays))],
                         steps, warm)
         res[name] = dict(ms_per_step=round(ms, 5), value=round(wl.T / (ms * 1e-3), 1),
                          unit="tokens/s", rac_channels=ks,
                          time_vs_headline=round(ms / ms_step, 3))
+        if k2:
+            res[name]["rac_channels_w2"] = k2
     torch.cuda.synchronize()
     return res
 

@@ -68,11 +68,16 @@ __global__ __launch_bounds__(256) void layer_scatter_kernel(
                           inv_row);
 }
 
+// masked residual quantisation; with sel_emit, workgroup 0 also lists S
+// from the bitmap (after the selection by rank)
 __global__ __launch_bounds__(256) void layer_resq_kernel(
     const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
     const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
     const float *__restrict__ ramax, const uint32_t *__restrict__ bitmap,
-    uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales, float *__restrict__ rgs) {
+    uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales, float *__restrict__ rgs,
+    int32_t *__restrict__ sel_emit) {
+  __shared__ int sh[1024 + 32];
+  if (sel_emit && blockIdx.x == 0) qdc::rac_emit_sel(bitmap, (int)K, sel_emit, sh);
   qdc::rac_resq_body(blockIdx.x, gridDim.x, x, xcodes, xscales, xgs, T, K, ramax, bitmap, rcodes,
                      rscales, rgs);
 }
@@ -86,6 +91,20 @@ __global__ __launch_bounds__(256) void layer_compact_kernel(
     uint16_t *__restrict__ out, float *__restrict__ rgs) {
   qdc::rac_compact_body(blockIdx.x, gridDim.x, x, xcodes, xscales, xgs, T, K, ramax, sel, Ks,
                         width, out, rgs);
+}
+
+// routing scatter (nr workgroups) | RAC channel selection by rank
+// (ceil(K / 8) workgroups, each writing one byte of the bitmap)
+__global__ __launch_bounds__(256) void layer_pre3r_kernel(
+    int64_t T, int E, int k, int nr, const int32_t *__restrict__ ids,
+    const int32_t *__restrict__ counts, const int32_t *__restrict__ ranks,
+    int32_t *__restrict__ offsets, int32_t *__restrict__ row_token, int32_t *__restrict__ inv_row,
+    const uint64_t *__restrict__ scores, int K, int Ks, uint32_t *__restrict__ bitmap) {
+  const int b = blockIdx.x;
+  if (b < nr)
+    qdr::route_scatter_body(b, T, E, k, nr, ids, counts, ranks, offsets, row_token, inv_row);
+  else
+    qdc::rac_rank_select_body(b - nr, scores, K, Ks, bitmap);
 }
 
 struct Layout {
@@ -221,6 +240,11 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   const bool rac = Ks > 0;
   // the W13 kernel for many rows per expert takes the residual compacted
   const bool want_sel = rac && qdi::gemm_wants_rq_sel(R, E, 2 * I, H, Ks, QD_EPI_SWIGLU);
+  // otherwise, for H <= 4096, the selection by rank, with S listed from its
+  // bitmap by the masked-residual kernel (the compact residual reads S in
+  // every workgroup, so it keeps the one-workgroup selection, which lists
+  // S itself)
+  const bool rank_sel = rac && !want_sel && H <= qdc::kRankSelMaxK;
   void *rq_sel = want_sel ? P(QD_VIEW_RQ_SEL) : nullptr;
   hipStream_t s = qdh::S(stream);
   // routing scratch, amax partials of X and the channel bitmap (the same
@@ -253,7 +277,11 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   mark(QD_STAGE_SELECT);
   if (rac) {
     const dim3 g3((unsigned)(nr + 1));
-    if (H <= 2048)
+    if (rank_sel)
+      hipLaunchKernelGGL(layer_pre3r_kernel, dim3((unsigned)(nr + (H + 7) / 8)), dim3(256), 0,
+                         s, T, E, k, nr, ids, counts, ranks, offs, row_token, inv_row, scores,
+                         (int)H, Ks, bitmap);
+    else if (H <= 2048)
       hipLaunchKernelGGL(layer_pre3_kernel<8>, g3, dim3(256), 0, s, T, E, k, nr, ids, counts,
                          ranks, offs, row_token, inv_row, scores, (int)H, Ks, sel, bitmap);
     else if (H <= 4096)
@@ -281,7 +309,8 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
       if (g < 1) g = 1;
       hipLaunchKernelGGL(layer_resq_kernel, dim3((unsigned)g), dim3(256), 0, s,
                          static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
-                         ramax, bitmap, rq.codes, rq.scales, rq.gscale);
+                         ramax, bitmap, rq.codes, rq.scales, rq.gscale,
+                         rank_sel ? sel : nullptr);
     }
   } else {
     hipLaunchKernelGGL(layer_scatter_kernel, dim3((unsigned)nr), dim3(256), 0, s, T, E, k, nr,

@@ -289,6 +289,76 @@ __device__ __forceinline__ void rac_select_body(const uint64_t *__restrict__ sco
   }
 }
 
+// Selection by rank for K <= kRankSelMaxK, spread over ceil(K / 8)
+// workgroups (the layer's fused path).  Workgroup g ranks channels
+// 8 g .. 8 g + 7 against all K channels in (score desc, index asc) order:
+// rank(c) = #{j : s_j > s_c, or s_j == s_c and j < c}.  The ranks are a
+// permutation of 0..K-1, so the channels of rank < K_s are exactly the K_s
+// the threshold selection above takes (top K_s by score, ties to the lower
+// index).  Each workgroup stores its byte of the bitmap; the next kernel
+// on the stream lists S from the bitmap (rac_emit_sel).  32 threads share a
+// channel: thread (part p, channel o) counts over the channels j = p
+// (mod 32) of a copy of the scores in LDS, so the eight channels of a wave
+// read eight consecutive scores per step.
+constexpr int kRankSelMaxK = 4096;
+
+__device__ __forceinline__ void rac_rank_select_body(int g, const uint64_t *__restrict__ scores,
+                                                     int K, int Ks,
+                                                     uint32_t *__restrict__ bitmap) {
+  __shared__ uint64_t sk[kRankSelMaxK];
+  __shared__ int red[4][8];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  for (int i = tid; i < K; i += 256) sk[i] = scores[i];
+  __syncthreads();
+  const int own = tid & 7, part = tid >> 3;
+  const int c = 8 * g + own;
+  const uint64_t sc = c < K ? sk[c] : 0ull;
+  int r = 0;
+  int j = part;
+  for (; j + 32 * 7 < K; j += 32 * 8) {
+    uint64_t u[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) u[q] = sk[j + 32 * q];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int jq = j + 32 * q;
+      r += (int)((u[q] > sc) | ((u[q] == sc) & (jq < c)));
+    }
+  }
+  for (; j < K; j += 32) {
+    const uint64_t u = sk[j];
+    r += (int)((u > sc) | ((u == sc) & (j < c)));
+  }
+  // sum over the eight parts of the wave (lanes own + 8 i), then the waves
+  r += __shfl_xor(r, 8, 64);
+  r += __shfl_xor(r, 16, 64);
+  r += __shfl_xor(r, 32, 64);
+  if (lane < 8) red[wid][own] = r;
+  __syncthreads();
+  if (wid == 0) {
+    const int rank = lane < 8 ? red[0][own] + red[1][own] + red[2][own] + red[3][own] : 0;
+    const uint64_t b = __ballot(lane < 8 && c < K && rank < Ks);
+    if (lane == 0) reinterpret_cast<uint8_t *>(bitmap)[g] = (uint8_t)b;
+  }
+}
+
+// S in ascending order from the selection bitmap (K <= 8192: one word per
+// thread of a 256-thread workgroup), into `out` (global or LDS).  Every
+// thread of the workgroup calls it; sh: 1024 + 32 ints of LDS.
+__device__ __forceinline__ void rac_emit_sel(const uint32_t *__restrict__ bitmap, int K,
+                                             int32_t *out, int *sh) {
+  const int tid = threadIdx.x;
+  const int nw = (K + 31) >> 5;
+  uint32_t m = tid < nw ? bitmap[tid] : 0u;
+  if (tid == nw - 1 && (K & 31)) m &= (1u << (K & 31)) - 1u;
+  int tot;
+  int pos = block_exclusive_scan(__popc(m), sh, tot);
+  while (m) {
+    out[pos++] = tid * 32 + (__ffs(m) - 1);
+    m &= m - 1u;
+  }
+}
+
 // Masked residual quantisation: one thread per 16-element block of [T][K];
 // workgroup bid of nblk.
 __device__ __forceinline__ void rac_resq_body(

@@ -31,12 +31,23 @@ __device__ __forceinline__ bool better(float v1, int e1, float v2, int e2) {
   return v1 > v2 || (v1 == v2 && e1 < e2);
 }
 
+// Order-preserving 64-bit key of (value desc, index asc): a larger key takes
+// an earlier slot.  The float bits map to an unsigned order (negative values
+// flipped), -0 counts as +0 (they compare equal), and the low word holds the
+// complement of the expert index.  No real logit maps to key 0, which pads.
+__device__ __forceinline__ uint64_t topk_key(float v, int e) {
+  uint32_t b = __float_as_uint(v);
+  if (b == 0x80000000u) b = 0u;
+  const uint32_t o = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return ((uint64_t)o << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)e);
+}
+
 // Top-k for E <= 256 experts, one workgroup per token: lane l of every wave
-// holds experts l, l + 64, ...; wave w broadcasts experts l + 64 j with
-// l in [16 w, 16 w + 16) in turn from their lanes and counts, for each of its
-// lane's experts, how many of those come first in (value desc, index asc);
-// the four partial counts summed in LDS give each expert's rank, and rank
-// r < k is slot r.  No serial reduction rounds.
+// holds experts l, l + 64, ...; wave w broadcasts the keys of experts
+// l + 64 j with l in [16 w, 16 w + 16) in turn from their lanes and counts,
+// for each of its lane's experts, how many of those have a larger key; the
+// four partial counts summed in LDS give each expert's rank, and rank r < k
+// is slot r.  No serial reduction rounds.
 constexpr int kRankMaxE = 256;
 __device__ __forceinline__ void route_topk_rank_body(int bid, const float *__restrict__ logits,
                                                      int64_t T, int E, int k, int renorm,
@@ -51,27 +62,28 @@ __device__ __forceinline__ void route_topk_rank_body(int bid, const float *__res
   const int per = (E + 63) >> 6;                // <= 4, uniform
   for (int e = threadIdx.x; e < E; e += blockDim.x) rk[e] = 0;
   float v[4];
+  uint64_t key[4];
   int r[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + 64 * j;
-    v[j] = (j < per && e < E) ? logits[t * E + e] : 0.0f;
+    const bool ok = j < per && e < E;
+    v[j] = ok ? logits[t * E + e] : 0.0f;
+    key[j] = ok ? topk_key(v[j], e) : 0ull;
     r[j] = 0;
   }
+  const int wu = __builtin_amdgcn_readfirstlane(wid);
 #pragma unroll
   for (int j2 = 0; j2 < 4; ++j2) {
     if (j2 >= per) break;
+    const uint32_t kh = (uint32_t)(key[j2] >> 32), kl = (uint32_t)key[j2];
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
-      const int i = 16 * wid + q;
-      const int e2 = i + 64 * j2;
-      const float u = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[j2]), i));
-      const bool v2 = e2 < E;
+      const int i = 16 * wu + q;
+      const uint64_t u = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)kh, i) << 32) |
+                         (uint32_t)__builtin_amdgcn_readlane((int)kl, i);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int e = lane + 64 * j;
-        r[j] += (v2 && (u > v[j] || (u == v[j] && e2 < e))) ? 1 : 0;
-      }
+      for (int j = 0; j < 4; ++j) r[j] += u > key[j] ? 1 : 0;
     }
   }
   __syncthreads();
