@@ -62,6 +62,18 @@ __device__ __forceinline__ void amax_partial_body(int bid, int nblk, const void 
   if (threadIdx.x == 0) part[bid] = m;
 }
 
+// trunc(sq * 2^F) as uint64 for a finite float sq >= 0, exactly (what the
+// float64 product and truncation give): sq = m * 2^x with m the integer
+// significand, so the result is m shifted by x + F.
+__device__ __forceinline__ uint64_t fixed_point_term(float sq, int F) {
+  const uint32_t bits = __float_as_uint(sq);
+  const uint32_t be = bits >> 23;
+  const uint64_t m = be ? ((bits & 0x7FFFFFu) | 0x800000u) : (bits & 0x7FFFFFu);
+  const int sh = (be ? (int)be - 150 : -149) + F;
+  if (sh >= 0) return m << sh;
+  return sh > -64 ? m >> (-sh) : 0ull;
+}
+
 // Q_A over [rows][cols] on a (gx, gy) grid of workgroups; this is
 // workgroup (bx, by).  Thread (tx, ty) of a 16x16 workgroup owns column block
 // (bx*16 + tx) and rows ty, ty+16*gy, ...  With RAC the same pass forms
@@ -117,22 +129,23 @@ __device__ __forceinline__ void quantize_act_body(
           float xh = dequant_value(c, sbf, s_dec);
           float rr = xh - v[i];
           rmax = fmaxf(rmax, fabsf(rr));
-          float sq = rr * rr;
-          double d = ldexp((double)sq, F);
-          acc[i] += (uint64_t)d;       // truncation toward zero; d < 2^37
+          acc[i] += fixed_point_term(rr * rr, F);   // each term < 2^37
         }
       }
     }
   }
   if (RAC) {
     // reduce the per-thread sums over ty, then one atomic per channel
-    __shared__ uint64_t part[16][256];
+    // (channel 16 tx + i of row ty at 17 i + tx: consecutive tx are
+    // adjacent when written, and consecutive channels 17 apart when read)
+    __shared__ uint64_t part[16][16 * 17];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) part[ty][tx * 16 + i] = acc[i];
+    for (int i = 0; i < 16; ++i) part[ty][17 * i + tx] = acc[i];
     __syncthreads();
     uint64_t s = 0;
+    const int rd = 17 * (threadIdx.x & 15) + (threadIdx.x >> 4);
 #pragma unroll
-    for (int j = 0; j < 16; ++j) s += part[j][threadIdx.x];
+    for (int j = 0; j < 16; ++j) s += part[j][rd];
     const int64_t ch = (int64_t)bx * 256 + threadIdx.x;
     if (ch < cols && s != 0ull) atomicAdd((unsigned long long *)&scores[ch], (unsigned long long)s);
     float m = block_max(rmax, red);

@@ -205,28 +205,43 @@ __device__ __forceinline__ void route_rank_body(int bid, int64_t T, int E, int k
                                                 int32_t *__restrict__ counts,
                                                 int32_t *__restrict__ ranks) {
   __shared__ uint32_t mask[kMaxE][kTokBlock / 32];
+  __shared__ uint8_t before[kMaxE][kTokBlock / 32];   // tokens of e in earlier words
   const int64_t t0 = (int64_t)bid * kTokBlock;
   for (int i = threadIdx.x; i < E * (kTokBlock / 32); i += blockDim.x) (&mask[0][0])[i] = 0u;
   __syncthreads();
   const int tl = threadIdx.x;
   const int64_t t = t0 + tl;
+  // this token's experts, loaded once (k <= 8 in registers)
+  int idr[8];
+#pragma unroll
+  for (int s = 0; s < 8; ++s) idr[s] = (t < T && s < k) ? ids[t * k + s] : 0;
   if (t < T) {
-    for (int s = 0; s < k; ++s) atomicOr(&mask[ids[t * k + s]][tl >> 5], 1u << (tl & 31));
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      if (s < k) atomicOr(&mask[idr[s]][tl >> 5], 1u << (tl & 31));
+    for (int s = 8; s < k; ++s) atomicOr(&mask[ids[t * k + s]][tl >> 5], 1u << (tl & 31));
   }
   __syncthreads();
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
     int c = 0;
 #pragma unroll
-    for (int w = 0; w < kTokBlock / 32; ++w) c += __popc(mask[e][w]);
+    for (int w = 0; w < kTokBlock / 32; ++w) {
+      before[e][w] = (uint8_t)c;          // < 256: at most 224 tokens before word 7
+      c += __popc(mask[e][w]);
+    }
     counts[(int64_t)bid * E + e] = c;
   }
+  __syncthreads();
   if (t < T) {
-    for (int s = 0; s < k; ++s) {
+    const uint32_t low = (1u << (tl & 31)) - 1u;
+    const int wd = tl >> 5;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      if (s < k)
+        ranks[t * k + s] = (int)before[idr[s]][wd] + __popc(mask[idr[s]][wd] & low);
+    for (int s = 8; s < k; ++s) {
       const int e = ids[t * k + s];
-      int r = 0;
-      for (int w = 0; w < (tl >> 5); ++w) r += __popc(mask[e][w]);
-      r += __popc(mask[e][tl >> 5] & ((1u << (tl & 31)) - 1u));
-      ranks[t * k + s] = r;
+      ranks[t * k + s] = (int)before[e][wd] + __popc(mask[e][wd] & low);
     }
   }
 }
