@@ -211,4 +211,16 @@ void launch_fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 // its compact form (rq_sel).
 bool gemm_wants_rq_sel(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
                        int32_t epilogue);
+// Whether the grouped GEMM on these sizes takes the residual in bitmap mode
+// (the decode kernel, K <= 4096).
+bool gemm_takes_bitmap(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
+                       int32_t epilogue);
+// moe_w4a4_grouped_gemm in bitmap mode: bitmap [K / 32] marks the selected
+// channels S in place of a list; the decode kernel writes S in ascending
+// order to sel_out.  QD_ERR_UNSUPPORTED where gemm_takes_bitmap is false.
+qd_status grouped_gemm_bitmap(const qd_nvfp4 *a, const int32_t *row_token,
+                              const int32_t *expert_offsets, int32_t E, int64_t rows,
+                              const qd_nvfp4 *w, const qd_nvfp4 *rq, const uint32_t *bitmap,
+                              int32_t Ks, int32_t *sel_out, int32_t epilogue, void *out,
+                              float *amax_partials, hipStream_t stream);
 }  // namespace qdi

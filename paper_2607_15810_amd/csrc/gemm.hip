@@ -47,6 +47,10 @@ struct GemmArgs {
   int Ks;
   const uint16_t *r_sel;   // f16 [a rows][ksa]: the residual at the selected channels
   int ksa;                 // row length of r_sel (Ks rounded up to 16)
+  // bitmap mode (decode kernel only): r_bitmap [K / 32] marks S in place of
+  // sel, and the kernel lists S into sel_out
+  const uint32_t *r_bitmap;
+  int32_t *sel_out;
   uint16_t *out;
   float *amax_part;
 };
@@ -324,11 +328,14 @@ constexpr int SK_LDS_MAX = 160 * 1024;
 constexpr int SK_GRID = 256;             // one workgroup per CU
 
 struct SkLayout {
-  int b, pan, xraw, offs, pu, sw, smask, red, total;
+  int b, pan, xraw, offs, pu, sw, smask, bm, red, total;
 };
 
-// panels: [source x, residual][slot 0, 1]; raw slots: [decoding wave][slot]
-__host__ __device__ inline SkLayout sk_layout(int K, int E, bool rac) {
+constexpr int SK_BM_KMAX = 4096;         // bitmap mode: at most 128 words of S
+
+// panels: [source x, residual][slot 0, 1]; raw slots: [decoding wave][slot];
+// bm: the selection bitmap (bitmap mode)
+__host__ __device__ inline SkLayout sk_layout(int K, int E, bool rac, bool bm) {
   SkLayout L{};
   int o = 0;
   auto take = [&](int bytes) { int at = o; o += (bytes + 15) & ~15; return at; };
@@ -339,10 +346,12 @@ __host__ __device__ inline SkLayout sk_layout(int K, int E, bool rac) {
   L.pu = take((E + 1) * 4);
   L.sw = take(E * 4);
   L.smask = take(rac ? (K >> 8) * 4 : 0);
+  L.bm = take(rac && bm ? (K >> 5) * 4 : 0);
   L.red = take(16 * 4);
   L.total = o;
   return L;
 }
+
 
 // Position in a workgroup's stage sequence: unit u = (expert e, pass p,
 // block nb), iteration it over K.  All fields are workgroup-uniform.
@@ -458,7 +467,8 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
   const int lr = lane & 15, g = lane >> 4;
   const int K = p.K, N = p.N, E = p.E;
   const int64_t kb2 = K >> 1, kb16 = K >> 4;
-  const SkLayout L = sk_layout(K, E, RAC);
+  const bool bmode = RAC && p.r_bitmap != nullptr;
+  const SkLayout L = sk_layout(K, E, RAC, bmode);
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   int32_t *offs = reinterpret_cast<int32_t *>(lds + L.offs);
   int32_t *pu = reinterpret_cast<int32_t *>(lds + L.pu);
@@ -477,10 +487,25 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     for (int i = tid; i < niter; i += SK_THREADS) smask[i] = 0u;
   }
   __syncthreads();
-  if (RAC) {
+  if (RAC && !bmode) {
     for (int i = tid; i < p.Ks; i += SK_THREADS) {
       const int c = min(max(p.sel[i], 0), K - 1);
       atomicOr(&smask[c >> 8], 1u << (((c >> 5) & 1) * 4 + ((c & 31) >> 3)));
+    }
+  }
+  uint32_t *bml = reinterpret_cast<uint32_t *>(lds + L.bm);
+  if (bmode) {
+    // word i holds channels 32 i .. 32 i + 31: k-step bits (i & 1) * 4 + q
+    // of iteration i / 8 for its non-zero bytes q
+    const int nw = K >> 5;
+    for (int i = tid; i < nw; i += SK_THREADS) {
+      const uint32_t m = p.r_bitmap[i];
+      bml[i] = m;
+      uint32_t bits = 0u;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if ((m >> (8 * q)) & 0xFFu) bits |= 1u << ((i & 1) * 4 + q);
+      if (bits) atomicOr(&smask[i >> 3], bits);
     }
   }
   {
@@ -764,6 +789,29 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
     }
     // loads past the last stage still target this workgroup's LDS
     wait_vm<0>();
+  }
+  if (bmode && blockIdx.x == 0 && w == 0) {
+    // S in ascending order from the bitmap in LDS, by workgroup 0's first
+    // wave once its stages are done (<= 128 words: two per lane)
+    const int nw = K >> 5;
+    uint32_t m0 = 2 * lane < nw ? bml[2 * lane] : 0u;
+    uint32_t m1 = 2 * lane + 1 < nw ? bml[2 * lane + 1] : 0u;
+    const int c = __popc(m0) + __popc(m1);
+    int xs = c;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(xs, o, 64);
+      if (lane >= o) xs += y;
+    }
+    int pos = xs - c;
+    while (m0) {
+      p.sel_out[pos++] = 64 * lane + (__ffs(m0) - 1);
+      m0 &= m0 - 1u;
+    }
+    while (m1) {
+      p.sel_out[pos++] = 64 * lane + 32 + (__ffs(m1) - 1);
+      m1 &= m1 - 1u;
+    }
   }
   const float m = block_max(vmax, red);
   if (p.amax_part && tid == 0) p.amax_part[P] = m;
@@ -1182,14 +1230,17 @@ inline int64_t skinny_nblk(int64_t N, int epilogue) {
 
 // Decode-sized problems: few rows per expert and whole 256-element
 // iterations.
-inline SkPlan skinny_plan(int64_t rows, int E, int64_t N, int64_t K, int Ks, int epilogue) {
+// bm: the residual in bitmap mode (K <= SK_BM_KMAX).
+inline SkPlan skinny_plan(int64_t rows, int E, int64_t N, int64_t K, int Ks, int epilogue,
+                          bool bm = false) {
   SkPlan pl{};
   const bool rac = Ks > 0;
   if (K < 256 || K % 256 != 0 || K > SK_KMAX || E > SK_EMAX || rows > (int64_t)E * 48) return pl;
+  if (bm && (!rac || K > SK_BM_KMAX)) return pl;
   const int64_t nblk = skinny_nblk(N, epilogue);
   pl.nblk = (int)nblk;
   pl.grid = (int)std::min<int64_t>(SK_GRID, (int64_t)E * nblk * 4);
-  pl.lds = (size_t)sk_layout((int)K, E, rac).total;
+  pl.lds = (size_t)sk_layout((int)K, E, rac, bm).total;
   if (pl.lds > (size_t)SK_LDS_MAX) return pl;
   pl.ok = true;
   return pl;
@@ -1281,6 +1332,12 @@ bool qdi::gemm_wants_rq_sel(int64_t rows, int32_t E, int64_t N, int64_t K, int32
   return !skinny_plan(rows, E, N, K, Ks, epilogue).ok && tile_plan(rows, E, N, K, true, Ks).ok;
 }
 
+bool qdi::gemm_takes_bitmap(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
+                            int32_t epilogue) {
+  if (Ks <= 0 || rows <= 0 || E < 1 || N <= 0 || K <= 0) return false;
+  return skinny_plan(rows, E, N, K, Ks, epilogue, true).ok;
+}
+
 extern "C" int64_t moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int64_t K,
                                                     int32_t E, int32_t Ks, int32_t epilogue) {
   if (rows < 0 || N <= 0 || K <= 0 || E < 1 || Ks < 0) return 0;
@@ -1329,12 +1386,16 @@ extern "C" qd_status nvfp4_pack_frag_scales(const qd_nvfp4 *w, uint8_t *out, voi
   return qdh::check_launch();
 }
 
-extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
-                                           const int32_t *expert_offsets, int32_t E, int64_t rows,
-                                           const qd_nvfp4 *w, const qd_nvfp4 *rq,
-                                           const int32_t *sel_idx, int32_t Ks, const void *rq_sel,
-                                           int32_t epilogue, void *out, float *amax_partials,
-                                           void *stream) {
+namespace {
+
+// The grouped GEMM behind moe_w4a4_grouped_gemm and the layer's bitmap
+// mode (bitmap != NULL: bitmap [K / 32] marks S, sel_idx is written with S;
+// decode-shaped problems with K <= 4096 only).
+qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
+                            const int32_t *expert_offsets, int32_t E, int64_t rows,
+                            const qd_nvfp4 *w, const qd_nvfp4 *rq, const int32_t *sel_idx,
+                            int32_t Ks, const void *rq_sel, const uint32_t *bitmap,
+                            int32_t epilogue, void *out, float *amax_partials, void *stream) {
   if (!a || !w || !out) return QD_ERR_NULL;
   if (epilogue != QD_EPI_NONE && epilogue != QD_EPI_SWIGLU) return QD_ERR_DTYPE;
   if (E < 1 || rows < 0) return QD_ERR_SHAPE;
@@ -1357,6 +1418,7 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
     if (Ks > K || rq->rows != a->rows) return QD_ERR_SHAPE;
     if (K > 65536) return QD_ERR_UNSUPPORTED;
   }
+  if (bitmap && !rac) return QD_ERR_SHAPE;
   if (Ks < 0) return QD_ERR_SHAPE;
   if (!qdh::aligned16(out) || (amax_partials && ((uintptr_t)amax_partials & 3u)))
     return QD_ERR_ALIGN;
@@ -1364,6 +1426,8 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
   if (N > 0x7fffffff || K > 0x7fffffff) return QD_ERR_UNSUPPORTED;
   const int64_t gx = grid_x(rows, E, true), gy = grid_y(N, epilogue);
   if (gx > 0x7fffffffLL || gy > 65535) return QD_ERR_UNSUPPORTED;
+  const SkPlan pl = skinny_plan(rows, E, N, K, rac ? Ks : 0, epilogue, bitmap != nullptr);
+  if (bitmap && !pl.ok) return QD_ERR_UNSUPPORTED;
   if (qdh::fault_injected()) return QD_ERR_HIP;
   if (rows == 0) return QD_OK;
 
@@ -1389,10 +1453,13 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
     p.Ks = Ks;
     p.r_sel = static_cast<const uint16_t *>(rq_sel);
     p.ksa = (Ks + 15) / 16 * 16;
+    if (bitmap) {
+      p.r_bitmap = bitmap;
+      p.sel_out = const_cast<int32_t *>(sel_idx);
+    }
   }
   p.out = static_cast<uint16_t *>(out);
   p.amax_part = amax_partials;
-  const SkPlan pl = skinny_plan(rows, E, N, K, rac ? Ks : 0, epilogue);
   const TlPlan tp = tile_plan(rows, E, N, K, rac, Ks);
   // the tiled kernel takes the residual in its compact form only
   if (rac && !pl.ok && tp.ok && (!rq_sel || !qdh::aligned16(rq_sel))) return rq_sel ? QD_ERR_ALIGN : QD_ERR_NULL;
@@ -1406,4 +1473,26 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
     else launch_epi<false, false>(p, epilogue, grid, s, pl, tp);
   }
   return qdh::check_launch();
+}
+
+}  // namespace
+
+extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
+                                           const int32_t *expert_offsets, int32_t E, int64_t rows,
+                                           const qd_nvfp4 *w, const qd_nvfp4 *rq,
+                                           const int32_t *sel_idx, int32_t Ks, const void *rq_sel,
+                                           int32_t epilogue, void *out, float *amax_partials,
+                                           void *stream) {
+  return grouped_gemm_impl(a, row_token, expert_offsets, E, rows, w, rq, sel_idx, Ks, rq_sel,
+                           nullptr, epilogue, out, amax_partials, stream);
+}
+
+qd_status qdi::grouped_gemm_bitmap(const qd_nvfp4 *a, const int32_t *row_token,
+                                   const int32_t *expert_offsets, int32_t E, int64_t rows,
+                                   const qd_nvfp4 *w, const qd_nvfp4 *rq, const uint32_t *bitmap,
+                                   int32_t Ks, int32_t *sel_out, int32_t epilogue, void *out,
+                                   float *amax_partials, hipStream_t stream) {
+  if (!bitmap) return QD_ERR_NULL;
+  return grouped_gemm_impl(a, row_token, expert_offsets, E, rows, w, rq, sel_out, Ks, nullptr,
+                           bitmap, epilogue, out, amax_partials, stream);
 }

@@ -68,16 +68,11 @@ __global__ __launch_bounds__(256) void layer_scatter_kernel(
                           inv_row);
 }
 
-// masked residual quantisation; with sel_emit, workgroup 0 also lists S
-// from the bitmap (after the selection by rank)
 __global__ __launch_bounds__(256) void layer_resq_kernel(
     const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
     const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
     const float *__restrict__ ramax, const uint32_t *__restrict__ bitmap,
-    uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales, float *__restrict__ rgs,
-    int32_t *__restrict__ sel_emit) {
-  __shared__ int sh[1024 + 32];
-  if (sel_emit && blockIdx.x == 0) qdc::rac_emit_sel(bitmap, (int)K, sel_emit, sh);
+    uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales, float *__restrict__ rgs) {
   qdc::rac_resq_body(blockIdx.x, gridDim.x, x, xcodes, xscales, xgs, T, K, ramax, bitmap, rcodes,
                      rscales, rgs);
 }
@@ -93,18 +88,24 @@ __global__ __launch_bounds__(256) void layer_compact_kernel(
                         width, out, rgs);
 }
 
-// routing scatter (nr workgroups) | RAC channel selection by rank
-// (ceil(K / 8) workgroups, each writing one byte of the bitmap)
-__global__ __launch_bounds__(256) void layer_pre3r_kernel(
+// routing scatter (nr workgroups) | RAC channel selection by rank and the
+// masked residual, one workgroup per 16-channel block (K / 16 workgroups);
+// 1024 threads per workgroup
+__global__ __launch_bounds__(qdc::kRankSelThreads) void layer_pre3r_kernel(
     int64_t T, int E, int k, int nr, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ counts, const int32_t *__restrict__ ranks,
     int32_t *__restrict__ offsets, int32_t *__restrict__ row_token, int32_t *__restrict__ inv_row,
-    const uint64_t *__restrict__ scores, int K, int Ks, uint32_t *__restrict__ bitmap) {
+    const uint64_t *__restrict__ scores, int K, int Ks, uint32_t *__restrict__ bitmap,
+    const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
+    const uint8_t *__restrict__ xscales, const float *__restrict__ xgs,
+    const float *__restrict__ ramax, uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales,
+    float *__restrict__ rgs) {
   const int b = blockIdx.x;
   if (b < nr)
     qdr::route_scatter_body(b, T, E, k, nr, ids, counts, ranks, offsets, row_token, inv_row);
   else
-    qdc::rac_rank_select_body(b - nr, scores, K, Ks, bitmap);
+    qdc::rac_rank_select_body(b - nr, scores, K, Ks, bitmap, x, xcodes, xscales, xgs, T, ramax,
+                              rcodes, rscales, rgs);
 }
 
 struct Layout {
@@ -222,7 +223,7 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   auto P = [&](int idx) { return b + L.off[idx]; };
   const int64_t R = T * k;
   auto mark = [&](int i) {
-    if (events) hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), qdh::S(stream));
+    if (events) (void)hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), qdh::S(stream));
   };
   int32_t *ids = (int32_t *)P(QD_VIEW_TOPK_IDS);
   float *wts = (float *)P(QD_VIEW_TOPK_W);
@@ -240,11 +241,13 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   const bool rac = Ks > 0;
   // the W13 kernel for many rows per expert takes the residual compacted
   const bool want_sel = rac && qdi::gemm_wants_rq_sel(R, E, 2 * I, H, Ks, QD_EPI_SWIGLU);
-  // otherwise, for H <= 4096, the selection by rank, with S listed from its
-  // bitmap by the masked-residual kernel (the compact residual reads S in
-  // every workgroup, so it keeps the one-workgroup selection, which lists
-  // S itself)
-  const bool rank_sel = rac && !want_sel && H <= qdc::kRankSelMaxK;
+  // where the W13 GEMM is the decode kernel (H <= 4096): the selection by
+  // rank with the masked residual, one workgroup per 16-channel block, and
+  // S listed by the GEMM from the bitmap (elsewhere the one-workgroup
+  // selection, which lists S itself, then the masked residual or its
+  // compact form)
+  const bool rank_sel = rac && !want_sel && H <= qdc::kRankSelMaxK &&
+                        qdi::gemm_takes_bitmap(R, E, 2 * I, H, Ks, QD_EPI_SWIGLU);
   void *rq_sel = want_sel ? P(QD_VIEW_RQ_SEL) : nullptr;
   hipStream_t s = qdh::S(stream);
   // routing scratch, amax partials of X and the channel bitmap (the same
@@ -278,9 +281,11 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   if (rac) {
     const dim3 g3((unsigned)(nr + 1));
     if (rank_sel)
-      hipLaunchKernelGGL(layer_pre3r_kernel, dim3((unsigned)(nr + (H + 7) / 8)), dim3(256), 0,
-                         s, T, E, k, nr, ids, counts, ranks, offs, row_token, inv_row, scores,
-                         (int)H, Ks, bitmap);
+      hipLaunchKernelGGL(layer_pre3r_kernel, dim3((unsigned)(nr + H / 16)),
+                         dim3(qdc::kRankSelThreads), 0, s, T,
+                         E, k, nr, ids, counts, ranks, offs, row_token, inv_row, scores, (int)H,
+                         Ks, bitmap, static_cast<const uint16_t *>(x), xq.codes, xq.scales,
+                         xq.gscale, ramax, rq.codes, rq.scales, rq.gscale);
     else if (H <= 2048)
       hipLaunchKernelGGL(layer_pre3_kernel<8>, g3, dim3(256), 0, s, T, E, k, nr, ids, counts,
                          ranks, offs, row_token, inv_row, scores, (int)H, Ks, sel, bitmap);
@@ -302,15 +307,14 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
       hipLaunchKernelGGL(layer_compact_kernel, dim3((unsigned)g), dim3(256), 0, s,
                          static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
                          ramax, sel, Ks, width, static_cast<uint16_t *>(rq_sel), rq.gscale);
-    } else {
+    } else if (!rank_sel) {
       const int64_t total = T * (H / 16);
       int64_t g = (total + 255) / 256;
       if (g > 4096) g = 4096;
       if (g < 1) g = 1;
       hipLaunchKernelGGL(layer_resq_kernel, dim3((unsigned)g), dim3(256), 0, s,
                          static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
-                         ramax, bitmap, rq.codes, rq.scales, rq.gscale,
-                         rank_sel ? sel : nullptr);
+                         ramax, bitmap, rq.codes, rq.scales, rq.gscale);
     }
   } else {
     hipLaunchKernelGGL(layer_scatter_kernel, dim3((unsigned)nr), dim3(256), 0, s, T, E, k, nr,
@@ -321,8 +325,12 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   uint16_t *h = (uint16_t *)P(QD_VIEW_H);
   float *hamax = (float *)P(QD_VIEW_H_AMAX);
   mark(QD_STAGE_W13);
-  st = moe_w4a4_grouped_gemm(&xq, row_token, offs, E, R, w13, rac ? &rq : nullptr,
-                             rac ? sel : nullptr, Ks, rq_sel, QD_EPI_SWIGLU, h, hamax, stream);
+  if (rank_sel)
+    st = qdi::grouped_gemm_bitmap(&xq, row_token, offs, E, R, w13, &rq, bitmap, Ks, sel,
+                                  QD_EPI_SWIGLU, h, hamax, s);
+  else
+    st = moe_w4a4_grouped_gemm(&xq, row_token, offs, E, R, w13, rac ? &rq : nullptr,
+                               rac ? sel : nullptr, Ks, rq_sel, QD_EPI_SWIGLU, h, hamax, stream);
   if (st) return st;
   qd_nvfp4 hq{(uint8_t *)P(QD_VIEW_HQ_CODES), (uint8_t *)P(QD_VIEW_HQ_SCALES),
               (float *)P(QD_VIEW_HQ_GSCALE), 1, R, I};

@@ -289,73 +289,101 @@ __device__ __forceinline__ void rac_select_body(const uint64_t *__restrict__ sco
   }
 }
 
-// Selection by rank for K <= kRankSelMaxK, spread over ceil(K / 8)
-// workgroups (the layer's fused path).  Workgroup g ranks channels
-// 8 g .. 8 g + 7 against all K channels in (score desc, index asc) order:
-// rank(c) = #{j : s_j > s_c, or s_j == s_c and j < c}.  The ranks are a
-// permutation of 0..K-1, so the channels of rank < K_s are exactly the K_s
-// the threshold selection above takes (top K_s by score, ties to the lower
-// index).  Each workgroup stores its byte of the bitmap; the next kernel
-// on the stream lists S from the bitmap (rac_emit_sel).  32 threads share a
-// channel: thread (part p, channel o) counts over the channels j = p
-// (mod 32) of a copy of the scores in LDS, so the eight channels of a wave
-// read eight consecutive scores per step.
+// Selection by rank for K <= kRankSelMaxK, one 1024-thread workgroup per
+// 16-channel block (the layer's fused path for few rows per expert).
+// Workgroup g ranks channels 16 g .. 16 g + 15 against all K channels in
+// (score desc, index asc) order: rank(c) = #{j : s_j > s_c, or s_j == s_c
+// and j < c}.  The ranks are a permutation of 0..K-1, so the channels of
+// rank < K_s are exactly the K_s the threshold selection above takes (top
+// K_s by score, ties to the lower index).  The workgroup stores its 16 bits
+// of the bitmap, then quantises the residual of its column block for every
+// row and masks it (the block arithmetic of rac_resq_body).  64 threads
+// share a channel: thread (part p, channel o) counts over the channels
+// j = p (mod 64) of a copy of the scores in LDS, so the four parts of a
+// wave read four consecutive scores per step.
 constexpr int kRankSelMaxK = 4096;
+constexpr int kRankSelThreads = 1024;
 
-__device__ __forceinline__ void rac_rank_select_body(int g, const uint64_t *__restrict__ scores,
-                                                     int K, int Ks,
-                                                     uint32_t *__restrict__ bitmap) {
+__device__ __forceinline__ void rac_rank_select_body(
+    int g, const uint64_t *__restrict__ scores, int K, int Ks, uint32_t *__restrict__ bitmap,
+    const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
+    const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T,
+    const float *__restrict__ ramax, uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales,
+    float *__restrict__ rgs) {
+  constexpr int NT = kRankSelThreads, NP = NT / 16, NW = NT / 64;
   __shared__ uint64_t sk[kRankSelMaxK];
-  __shared__ int red[4][8];
+  __shared__ int red[NW][16];
+  __shared__ uint32_t s_bits;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  for (int i = tid; i < K; i += 256) sk[i] = scores[i];
+  for (int i = tid; i < K; i += NT) sk[i] = scores[i];
   __syncthreads();
-  const int own = tid & 7, part = tid >> 3;
-  const int c = 8 * g + own;
+  const int own = tid & 15, part = tid >> 4;
+  const int c = 16 * g + own;
   const uint64_t sc = c < K ? sk[c] : 0ull;
   int r = 0;
   int j = part;
-  for (; j + 32 * 7 < K; j += 32 * 8) {
-    uint64_t u[8];
+  for (; j + NP * 3 < K; j += NP * 4) {
+    uint64_t u[4];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) u[q] = sk[j + 32 * q];
+    for (int q = 0; q < 4; ++q) u[q] = sk[j + NP * q];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int jq = j + 32 * q;
+    for (int q = 0; q < 4; ++q) {
+      const int jq = j + NP * q;
       r += (int)((u[q] > sc) | ((u[q] == sc) & (jq < c)));
     }
   }
-  for (; j < K; j += 32) {
+  for (; j < K; j += NP) {
     const uint64_t u = sk[j];
     r += (int)((u > sc) | ((u == sc) & (j < c)));
   }
-  // sum over the eight parts of the wave (lanes own + 8 i), then the waves
-  r += __shfl_xor(r, 8, 64);
+  // sum over the four parts of the wave (lanes own + 16 i), then the waves
   r += __shfl_xor(r, 16, 64);
   r += __shfl_xor(r, 32, 64);
-  if (lane < 8) red[wid][own] = r;
+  if (lane < 16) red[wid][own] = r;
   __syncthreads();
   if (wid == 0) {
-    const int rank = lane < 8 ? red[0][own] + red[1][own] + red[2][own] + red[3][own] : 0;
-    const uint64_t b = __ballot(lane < 8 && c < K && rank < Ks);
-    if (lane == 0) reinterpret_cast<uint8_t *>(bitmap)[g] = (uint8_t)b;
+    int rank = 0;
+    if (lane < 16)
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) rank += red[ww][own];
+    const uint32_t b = (uint32_t)__ballot(lane < 16 && c < K && rank < Ks) & 0xFFFFu;
+    if (lane == 0) {
+      reinterpret_cast<uint16_t *>(bitmap)[g] = (uint16_t)b;
+      s_bits = b;
+    }
   }
-}
-
-// S in ascending order from the selection bitmap (K <= 8192: one word per
-// thread of a 256-thread workgroup), into `out` (global or LDS).  Every
-// thread of the workgroup calls it; sh: 1024 + 32 ints of LDS.
-__device__ __forceinline__ void rac_emit_sel(const uint32_t *__restrict__ bitmap, int K,
-                                             int32_t *out, int *sh) {
-  const int tid = threadIdx.x;
-  const int nw = (K + 31) >> 5;
-  uint32_t m = tid < nw ? bitmap[tid] : 0u;
-  if (tid == nw - 1 && (K & 31)) m &= (1u << (K & 31)) - 1u;
-  int tot;
-  int pos = block_exclusive_scan(__popc(m), sh, tot);
-  while (m) {
-    out[pos++] = tid * 32 + (__ffs(m) - 1);
-    m &= m - 1u;
+  __syncthreads();
+  // the masked residual of column block g
+  const uint32_t m16 = s_bits;
+  const float amax_r = ramax[0];
+  float s_enc, s_dec;
+  tensor_scale(amax_r, s_enc, s_dec);
+  const bool zero_tensor = !(amax_r >= kZeroAmax);
+  if (g == 0 && tid == 0) {
+    rgs[0] = s_enc;
+    rgs[1] = s_dec;
+  }
+  const float xs_dec = xgs[1];
+  const int64_t nbc = K >> 4;
+  uint32_t mlo = 0u, mhi = 0u;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    if ((m16 >> i) & 1u) mlo |= 15u << (4 * i);
+    if ((m16 >> (i + 8)) & 1u) mhi |= 15u << (4 * i);
+  }
+  for (int64_t t = tid; t < T; t += NT) {
+    const int64_t bi = t * nbc + g;
+    uint32_t lo = 0u, hi = 0u, sb = 0u;
+    if (m16) {
+      float v[16], rr[16];
+      load_bf16x16(x + bi * 16, v);
+      block_residual(v, reinterpret_cast<const uint2 *>(xcodes)[bi], xscales[bi], xs_dec, rr);
+      sb = quantize_block(rr, s_enc, zero_tensor, lo, hi);
+      lo &= mlo;
+      hi &= mhi;
+    }
+    reinterpret_cast<uint2 *>(rcodes)[bi] = make_uint2(lo, hi);
+    rscales[bi] = (uint8_t)sb;
   }
 }
 

@@ -13,7 +13,8 @@
 //                        every (token, slot) its rank among the block's tokens
 //                        of the same expert, and per-block expert counts.
 //   route_scatter_body   scan of the counts -> expert offsets; row =
-//                        offset[e] + rows of e in earlier blocks + rank.
+//                        offset[e] + rows of e in earlier blocks + rank
+//                        (256 or more threads).
 // No atomic slot claims: the row order (expert asc, token asc) is a pure
 // function of the routing, so the permutation is bit-reproducible.
 #pragma once
@@ -265,14 +266,37 @@ __device__ __forceinline__ void route_scatter_body(
     base[e] = pre;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {            // exclusive scan over experts (E <= 1024)
-    int run = 0;
-    for (int e = 0; e < E; ++e) {
-      int c = total[e];
-      total[e] = run;
-      run += c;
+  {
+    // exclusive scan over experts (E <= 1024): threads 0..255 hold four
+    // consecutive experts each, scanned across lanes and the four waves
+    __shared__ int wsum[4];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    int c[4], tsum = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * tid + q;
+      c[q] = (tid < 256 && e < E) ? total[e] : 0;
+      tsum += c[q];
     }
-    if (b == 0) offsets[E] = run;
+    int xs = tsum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(xs, o, 64);
+      if (lane >= o) xs += y;
+    }
+    if (tid < 256 && lane == 63) wsum[wid] = xs;
+    __syncthreads();
+    if (tid < 256) {
+      int ex = xs - tsum;
+      for (int ww = 0; ww < wid; ++ww) ex += wsum[ww];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = 4 * tid + q;
+        if (e < E) total[e] = ex;
+        ex += c[q];
+      }
+    }
+    if (tid == 0 && b == 0) offsets[E] = wsum[0] + wsum[1] + wsum[2] + wsum[3];
   }
   __syncthreads();
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
@@ -281,7 +305,7 @@ __device__ __forceinline__ void route_scatter_body(
   }
   __syncthreads();
   const int64_t t = (int64_t)b * kTokBlock + threadIdx.x;
-  if (t < T) {
+  if (threadIdx.x < kTokBlock && t < T) {
     for (int s = 0; s < k; ++s) {
       const int e = ids[t * k + s];
       const int row = base[e] + ranks[t * k + s];
