@@ -124,20 +124,99 @@ __device__ __forceinline__ void route_topk_rank_body(int bid, const float *__res
   }
 }
 
-// workgroups the top-k step needs for T tokens and E experts
-inline int topk_groups(int64_t T, int E) {
-  return (int)(E <= kRankMaxE ? T : (T + 3) / 4);
+// Top-k for E <= 256 experts and many tokens: one wavefront per token, four
+// tokens per workgroup.  The wave broadcasts all E keys from their lanes in
+// turn and counts, for each of its lane's experts, the larger ones, so every
+// expert's rank is known without LDS or barriers; the expert of rank s < k
+// takes slot s.  Same arithmetic as the rank body above (softmax terms in
+// slot order).
+constexpr int64_t kTopkWaveMinT = 1024;
+// PER = ceil(E / 64) experts per lane
+template <int PER>
+__device__ __forceinline__ void route_topk_wave_body(int bid, const float *__restrict__ logits,
+                                                     int64_t T, int E, int k, int renorm,
+                                                     int32_t *__restrict__ ids,
+                                                     float *__restrict__ wts) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int64_t t = (int64_t)bid * 4 + wid;
+  if (t >= T) return;                           // whole wave; no barriers below
+  float v[PER];
+  uint64_t key[PER];
+  int r[PER];
+  bool ok[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int e = lane + 64 * j;
+    ok[j] = e < E;
+    v[j] = ok[j] ? logits[t * E + e] : 0.0f;
+    key[j] = ok[j] ? topk_key(v[j], e) : 0ull;
+    r[j] = 0;
+  }
+#pragma unroll
+  for (int j2 = 0; j2 < PER; ++j2) {
+    const uint32_t kh = (uint32_t)(key[j2] >> 32), kl = (uint32_t)key[j2];
+#pragma unroll 16
+    for (int i = 0; i < 64; ++i) {
+      const uint64_t u = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)kh, i) << 32) |
+                         (uint32_t)__builtin_amdgcn_readlane((int)kl, i);
+#pragma unroll
+      for (int j = 0; j < PER; ++j) r[j] += u > key[j] ? 1 : 0;
+    }
+  }
+  // the value of slot s, broadcast from the lane holding the expert of rank s
+  auto slot_value = [&](int sl) {
+    float val = 0.0f;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const uint64_t b = __ballot(ok[j] && r[j] == sl);
+      if (b) val = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[j]), __ffsll((long long)b) - 1));
+    }
+    return val;
+  };
+  const float top_v = slot_value(0);
+  float denom = 0.0f;
+  if (renorm) {
+    for (int sl = 0; sl < k; ++sl) denom += expf(slot_value(sl) - top_v);   // slot order
+  } else {                 // full softmax denominator over all E experts
+    float part = 0.0f;
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      if (ok[j]) part += expf(v[j] - top_v);
+    for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
+    denom = part;
+  }
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    if (ok[j] && r[j] < k) {
+      ids[t * k + r[j]] = lane + 64 * j;
+      wts[t * k + r[j]] = expf(v[j] - top_v) / denom;
+    }
+  }
 }
 
-// E <= 256: the rank body above.  Otherwise one wavefront per token, four
-// tokens per workgroup (workgroup index bid): k rounds of a wave-wide arg-max
-// (any E up to kMaxE).
+// workgroups the top-k step needs for T tokens and E experts
+inline int topk_groups(int64_t T, int E) {
+  return (int)(E <= kRankMaxE && T < kTopkWaveMinT ? T : (T + 3) / 4);
+}
+
+// E <= 256: the rank body (T < 1024) or the wave body above.  Otherwise one
+// wavefront per token, four tokens per workgroup (workgroup index bid): k
+// rounds of a wave-wide arg-max (any E up to kMaxE).
 __device__ __forceinline__ void route_topk_body(int bid, const float *__restrict__ logits,
                                                 int64_t T, int E, int k, int renorm,
                                                 int32_t *__restrict__ ids,
                                                 float *__restrict__ wts) {
   if (E <= kRankMaxE) {
-    route_topk_rank_body(bid, logits, T, E, k, renorm, ids, wts);
+    if (T < kTopkWaveMinT) {
+      route_topk_rank_body(bid, logits, T, E, k, renorm, ids, wts);
+    } else {
+      switch ((E + 63) >> 6) {
+        case 1: route_topk_wave_body<1>(bid, logits, T, E, k, renorm, ids, wts); break;
+        case 2: route_topk_wave_body<2>(bid, logits, T, E, k, renorm, ids, wts); break;
+        case 3: route_topk_wave_body<3>(bid, logits, T, E, k, renorm, ids, wts); break;
+        default: route_topk_wave_body<4>(bid, logits, T, E, k, renorm, ids, wts); break;
+      }
+    }
     return;
   }
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;

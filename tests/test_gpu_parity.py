@@ -240,6 +240,34 @@ def test_layer_w2_site_rac(case):
     assert not torch.equal(y0, y)
 
 
+ROUTE_CASES = [
+    # T, E, k: one workgroup per token (T < 1024), one wave per token
+    # (T >= 1024), and the arg-max rounds for E > 256
+    (100, 8, 2), (100, 128, 8), (1500, 128, 8), (1100, 256, 6), (1030, 64, 1), (600, 300, 4),
+]
+
+
+@pytest.mark.parametrize("renorm", [True, False])
+@pytest.mark.parametrize("T,E,k", ROUTE_CASES)
+def test_route_topk_paths(T, E, k, renorm):
+    rng = np.random.default_rng(T * 7 + E + k)
+    lg = rng.standard_normal((T, E)).astype(np.float32)
+    lg[::7, : E // 2] = np.float32(0.5)            # ties, broken by the lower index
+    lg[1::9, 0] = np.float32(-0.0)
+    lg[1::9, 1] = np.float32(0.0)
+    lg[2::11] = np.round(lg[2::11] * 2) / 2        # many equal values
+    ids, wts, offs, row_token, inv_row = ops.route_permute(torch.from_numpy(lg).to(DEV), k,
+                                                           renorm=renorm)
+    ref_ids = ORt.topk(lg, k)
+    assert np.array_equal(ids.cpu().numpy(), ref_ids)
+    np.testing.assert_allclose(wts.cpu().numpy(), ORt.weights(lg, ref_ids, renorm), rtol=2e-6,
+                               atol=1e-7)
+    perm = ORt.permute(ref_ids, E)
+    assert np.array_equal(offs.cpu().numpy(), perm["offsets"])
+    assert np.array_equal(row_token.cpu().numpy(), perm["row_token"])
+    assert np.array_equal(inv_row.cpu().numpy(), perm["inv_row"])
+
+
 def test_dense_gemm_with_rac():
     """16 tokens x K=256 x N=128, 4 outlier channels x30, RAC on 8 channels."""
     inp = synth.generate("dense_t16_k256_n128")
