@@ -355,6 +355,28 @@ qd_status qd_mxfp4_moe_layer_forward(const void *x, const float *logits, int64_t
                                      void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------
+ * moe_w4a16_grouped_gemm -- the trainer-side forward of Sec. 3.2, Eq.
+ * (w4a16-qat-forward): bf16 activations times the NVFP4 fake-quantised
+ * weights (asymmetric W4A16; the same QDQ_W as the rollout side, Eq.
+ * (weight-qdq-align)), grouped over experts:
+ *   v[r][n] = s_dec_w[e(r)] * sum_k a[src(r)][k] * what[e(r)][n][k]
+ * with what = e2m1 * e4m3 (exact in bf16), products exact, f32 sums.
+ *   a               : bf16 [a_rows][K], 16-byte aligned; row_token values
+ *                     must lie in [0, a_rows).
+ *   row_token       : int32 [rows] gather map (NULL: row r reads a row r).
+ *   expert_offsets  : int32 [E+1] row ranges per expert (NULL: E must be 1).
+ *   w               : E groups of [N][K]; K % 64 == 0, N % 32 == 0.
+ *   epilogue        : QD_EPI_NONE: out bf16 [rows][N] = bf16(v);
+ *                     QD_EPI_SWIGLU: gate rows [0, N/2), up rows [N/2, N);
+ *                     out bf16 [rows][N/2] = bf16(silu(g) * u).
+ * E <= 1024.  The backward pass (straight-through estimator) needs no
+ * kernel of its own.
+ * ------------------------------------------------------------------- */
+qd_status moe_w4a16_grouped_gemm(const void *a, int64_t a_rows, const int32_t *row_token,
+                                 const int32_t *expert_offsets, int32_t E, int64_t rows,
+                                 const qd_nvfp4 *w, int32_t epilogue, void *out, void *stream);
+
+/* ---------------------------------------------------------------------
  * qd_moe_layer_forward -- the whole rollout-side layer in one call: route,
  * quantise X with fused RAC scores, select, W13 GEMM with fused residual
  * and SwiGLU, quantise h, W2 GEMM, combine.  Same results as the seven

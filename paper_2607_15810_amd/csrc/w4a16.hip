@@ -1,0 +1,243 @@
+// The trainer-side forward of QUADS (Sec. 3.2, Eq. (w4a16-qat-forward)):
+// asymmetric W4A16, i.e. bf16 activations times the NVFP4 fake-quantised
+// weights, Y = X * W_hat^T, as a grouped GEMM over the experts of the MoE
+// layer.  W_hat is the same QDQ the rollout side uses (Sec. 3.2, Eq.
+// (weight-qdq-align)), so the weights are read in their NVFP4 form (E2M1
+// codes, E4M3 scale per 16, FP32 tensor scale) and decoded exactly:
+// e2m1 * e4m3 has at most six significant bits, so it is exact in bf16, and
+// a bf16 activation times it is exact in f32.  The tensor scale s_dec of the
+// expert multiplies the f32 sum in the epilogue.
+//
+// Kernel: tiles of 128 grouped rows x 128 weight rows (SwiGLU: 64 gate rows
+// and the matching 64 up rows), four waves in a 2 x 2 grid of 64 x 64 on
+// v_mfma_f32_32x32x16_bf16.  K streams in stages of 64 through a double
+// buffer in LDS: each thread loads a half row (32 elements) of activations
+// and of weight codes for the next stage into registers while the current
+// stage is multiplied, then stores the activations as they are and the
+// weights decoded to bf16.  Rows are padded to 72 elements (144 bytes) so
+// that the fragment reads hit distinct banks.  M-tiles follow the shared
+// tile scheduler (no tile straddles two experts; tiles contiguous per XCD).
+#include "common.h"
+#include "tile_sched.h"
+
+namespace {
+
+using namespace qd;
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int WA_M = 128;            // grouped rows per tile
+constexpr int WA_N = 128;            // weight rows per tile
+constexpr int WA_K = 64;             // elements per stage
+constexpr int WA_LD = WA_K + 8;      // LDS row stride in bf16 elements
+
+struct W16Args {
+  const uint16_t *a;                 // bf16 [a_rows][K]
+  const int32_t *row_token;
+  const int32_t *offsets;
+  int E;
+  int64_t rows;
+  const uint8_t *w_codes;
+  const uint8_t *w_scales;
+  const float *w_gs;
+  int N;
+  int K;
+  uint16_t *out;
+};
+
+__device__ __forceinline__ f32x16_t mfma_bf16(bf16x8_t a, bf16x8_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// e2m1(code) * e4m3 scale, exact, as bf16 bits
+__device__ __forceinline__ uint32_t weight_bf16(uint32_t code, float sbf) {
+  float v = e2m1_value(code) * sbf;
+  if (code & 8u) v = -v;
+  return __float_as_uint(v) >> 16;   // exact: at most six significant bits
+}
+
+template <bool GATHER, int EPI>
+__global__ __launch_bounds__(256) void gemm_w4a16_kernel(W16Args p, int ntn) {
+  __shared__ __align__(16) uint16_t As[2][WA_M * WA_LD];
+  __shared__ __align__(16) uint16_t Bs[2][WA_N * WA_LD];
+  __shared__ int32_t src_row[WA_M];
+  __shared__ int sh_w[4], sh_t[4];
+  const qdt::Tile t = qdt::find_tile<WA_M>(p.offsets, p.E, p.rows, ntn, sh_w, sh_t);
+  if (t.e < 0) return;                        // whole workgroup
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w >> 1, wn = w & 1;
+  const int K = p.K, N = p.N;
+  for (int r = tid; r < WA_M; r += 256) {
+    const int64_t g = t.row0 + (r < t.nrows ? r : 0);   // rows past the tile read its first
+    src_row[r] = GATHER ? p.row_token[g] : (int32_t)g;
+  }
+  __syncthreads();
+
+  // this thread's half row (32 elements) of each stage: tile row / weight
+  // row ar, half hf
+  const int ar = tid >> 1, hf = tid & 1;
+  const uint16_t *ag = p.a + (int64_t)src_row[ar] * K + hf * 32;
+  int wr;
+  if (EPI == QD_EPI_SWIGLU) {
+    const int I = N >> 1;
+    wr = ar < 64 ? t.nt * 64 + ar : I + t.nt * 64 + (ar - 64);
+  } else {
+    wr = t.nt * WA_N + ar;
+  }
+  const int64_t wrow = (int64_t)t.e * N + (wr < N ? wr : 0);   // others are never stored
+  const uint8_t *bc = p.w_codes + wrow * (K >> 1) + hf * 16;
+  const uint8_t *bs = p.w_scales + wrow * (K >> 4) + hf * 2;
+
+  uint4 ra[4], rb;
+  uint32_t rs = 0u;
+  auto load = [&](int k0) {
+    const uint4 *pa = reinterpret_cast<const uint4 *>(ag + k0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) ra[q] = pa[q];
+    rb = *reinterpret_cast<const uint4 *>(bc + (k0 >> 1));
+    rs = *reinterpret_cast<const uint16_t *>(bs + (k0 >> 4));
+  };
+  auto store = [&](int buf) {
+    uint4 *da = reinterpret_cast<uint4 *>(&As[buf][ar * WA_LD + hf * 32]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) da[q] = ra[q];
+    const float s0 = e4m3_to_f32(rs & 0xFFu), s1 = e4m3_to_f32((rs >> 8) & 0xFFu);
+    const uint32_t words[4] = {rb.x, rb.y, rb.z, rb.w};
+    uint32_t o[16];
+#pragma unroll
+    for (int j = 0; j < 32; j += 2) {
+      const uint32_t wv = words[j >> 3];
+      const float sb = j < 16 ? s0 : s1;
+      o[j >> 1] = weight_bf16((wv >> (4 * (j & 7))) & 15u, sb) |
+                  (weight_bf16((wv >> (4 * ((j + 1) & 7))) & 15u, sb) << 16);
+    }
+    uint4 *db = reinterpret_cast<uint4 *>(&Bs[buf][ar * WA_LD + hf * 32]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) db[q] = make_uint4(o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]);
+  };
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
+
+  // fragment rows: A rows wm*64 + 32 i, B rows of fragment j (SwiGLU: j = 0
+  // gate rows, j = 1 the matching up rows)
+  const int lr = lane & 31, kh = 8 * (lane >> 5);
+  int brow[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+    brow[j] = EPI == QD_EPI_SWIGLU ? j * 64 + wn * 32 + lr : wn * 64 + j * 32 + lr;
+
+  const int nst = K / WA_K;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int s = 0; s < nst; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < nst) load((s + 1) * WA_K);
+#pragma unroll
+    for (int kk = 0; kk < WA_K; kk += 16) {
+      bf16x8_t af[2], bf[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        af[i] = *reinterpret_cast<const bf16x8_t *>(&As[buf][(wm * 64 + i * 32 + lr) * WA_LD + kk + kh]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        bf[j] = *reinterpret_cast<const bf16x8_t *>(&Bs[buf][brow[j] * WA_LD + kk + kh]);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma_bf16(af[i], bf[j], acc[i][j]);
+    }
+    // the buffer written here was last read in iteration s - 1, which every
+    // thread left through the barrier at its end
+    if (s + 1 < nst) store((s + 1) & 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: the expert's tensor scale, SwiGLU or plain, bf16 stores
+  const float alpha = p.w_gs[2 * t.e + 1];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int rl = wm * 64 + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+      if (rl >= t.nrows) continue;
+      const int64_t row = t.row0 + rl;
+      if (EPI == QD_EPI_SWIGLU) {
+        const int I = N >> 1;
+        const int col = t.nt * 64 + wn * 32 + lr;
+        if (col < I) {
+          const float gv = alpha * acc[i][0][q];
+          const float uv = alpha * acc[i][1][q];
+          const float h = gv / (1.0f + expf(-gv)) * uv;
+          p.out[row * I + col] = (uint16_t)f32_to_bf16_bits(h);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int col = t.nt * WA_N + wn * 64 + j * 32 + lr;
+          if (col < N) p.out[row * N + col] = (uint16_t)f32_to_bf16_bits(alpha * acc[i][j][q]);
+        }
+      }
+    }
+  }
+}
+
+}  // namespace
+
+extern "C" qd_status moe_w4a16_grouped_gemm(const void *a, int64_t a_rows,
+                                            const int32_t *row_token,
+                                            const int32_t *expert_offsets, int32_t E,
+                                            int64_t rows, const qd_nvfp4 *w, int32_t epilogue,
+                                            void *out, void *stream) {
+  if (!w) return QD_ERR_NULL;
+  if (epilogue != QD_EPI_NONE && epilogue != QD_EPI_SWIGLU) return QD_ERR_DTYPE;
+  if (E < 1 || E > 1024 || rows < 0 || a_rows < 0) return QD_ERR_SHAPE;
+  qd_status st = qdh::check_nvfp4(w, E, w->rows, w->cols);
+  if (st) return st;
+  const int64_t N = w->rows, K = w->cols;
+  if (K <= 0 || K % WA_K != 0 || N <= 0 || N % 32 != 0) return QD_ERR_SHAPE;
+  if (!expert_offsets && E != 1) return QD_ERR_SHAPE;
+  if (!row_token && rows > a_rows) return QD_ERR_SHAPE;
+  if (N > 0x7fffffff || K > 0x7fffffff || rows > 0x7fffffff) return QD_ERR_UNSUPPORTED;
+  if (rows == 0) return QD_OK;
+  if (!a || !out) return QD_ERR_NULL;
+  if (!qdh::aligned16(a) || !qdh::aligned16(out) || !qdh::aligned16(w->codes))
+    return QD_ERR_ALIGN;
+  if (qdh::fault_injected()) return QD_ERR_HIP;
+  W16Args p{};
+  p.a = static_cast<const uint16_t *>(a);
+  p.row_token = row_token;
+  p.offsets = expert_offsets;
+  p.E = E;
+  p.rows = rows;
+  p.w_codes = w->codes;
+  p.w_scales = w->scales;
+  p.w_gs = w->gscale;
+  p.N = (int)N;
+  p.K = (int)K;
+  p.out = static_cast<uint16_t *>(out);
+  const int ntn = epilogue == QD_EPI_SWIGLU ? (int)((N / 2 + 63) / 64) : (int)((N + WA_N - 1) / WA_N);
+  const int64_t grid = qdt::tile_grid(rows, E, WA_M, ntn);
+  if (grid > 0x7fffffffLL) return QD_ERR_UNSUPPORTED;
+  hipStream_t s = qdh::S(stream);
+  const dim3 g((unsigned)grid);
+  if (row_token) {
+    if (epilogue == QD_EPI_SWIGLU)
+      hipLaunchKernelGGL((gemm_w4a16_kernel<true, QD_EPI_SWIGLU>), g, dim3(256), 0, s, p, ntn);
+    else
+      hipLaunchKernelGGL((gemm_w4a16_kernel<true, QD_EPI_NONE>), g, dim3(256), 0, s, p, ntn);
+  } else {
+    if (epilogue == QD_EPI_SWIGLU)
+      hipLaunchKernelGGL((gemm_w4a16_kernel<false, QD_EPI_SWIGLU>), g, dim3(256), 0, s, p, ntn);
+    else
+      hipLaunchKernelGGL((gemm_w4a16_kernel<false, QD_EPI_NONE>), g, dim3(256), 0, s, p, ntn);
+  }
+  return qdh::check_launch();
+}

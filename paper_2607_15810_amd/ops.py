@@ -299,6 +299,40 @@ class MoELayer:
         )
 
 
+# ---------------------------------------------------------------- W4A16 (trainer-side forward)
+
+def w4a16_grouped_gemm(a, w, rows, row_token=None, offsets=None, epilogue=Q.QD_EPI_NONE):
+    """bf16 activations a [a_rows][K] times the NVFP4 weights w (E groups of
+    [N][K]) through moe_w4a16_grouped_gemm."""
+    _require_cuda(a)
+    a = a.contiguous()
+    if a.dtype != torch.bfloat16:
+        raise TypeError("a must be bfloat16")
+    N = w.rows
+    ncol = N // 2 if epilogue == Q.QD_EPI_SWIGLU else N
+    out = torch.empty((rows, ncol), dtype=torch.bfloat16, device=a.device)
+    Q.call("moe_w4a16_grouped_gemm", a.data_ptr(), a.shape[0], _ptr(row_token), _ptr(offsets),
+           w.groups, rows, _nv(w), epilogue, out.data_ptr(), _stream())
+    return out
+
+
+class W4A16MoELayer:
+    """The layer's forward with bf16 activations and the fake-quantised
+    weights (the trainer side of Sec. 3.2): routing, W13 with SwiGLU, W2 and
+    the combine, every step on the library's kernels."""
+
+    def __init__(self, w13, w2, k, renorm=True):
+        self.w13, self.w2, self.k, self.renorm = w13, w2, k, renorm
+
+    def __call__(self, x, logits):
+        T = x.shape[0]
+        ids, wts, offs, row_token, inv_row = route_permute(logits, self.k, self.renorm)
+        R = T * self.k
+        h = w4a16_grouped_gemm(x, self.w13, R, row_token, offs, Q.QD_EPI_SWIGLU)
+        z = w4a16_grouped_gemm(h, self.w2, R, None, offs)
+        return unpermute_combine(z, inv_row, wts)
+
+
 # ---------------------------------------------------------------- FP8 W8A8 comparison layer
 
 def fp8_quantize_rows(x):

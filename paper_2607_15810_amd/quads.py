@@ -92,6 +92,8 @@ SIGNATURES = {
                                            c_int32, c_int64, c_int32, c_void_p, c_void_p,
                                            c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
                                            c_void_p]),
+    "moe_w4a16_grouped_gemm": (c_int, [c_void_p, c_int64, c_void_p, c_void_p, c_int32, c_int64,
+                                       PN, c_int32, c_void_p, c_void_p]),
     "qd_moe_layer_workspace": (c_size_t, [c_int64, c_int64, c_int32, c_int32, c_int64]),
     "qd_moe_layer_forward": (c_int, [c_void_p, c_void_p, c_int64, c_int64, c_int32, c_int32,
                                      c_int64, c_int32, c_int32, c_int32, PN, PN, c_void_p,
