@@ -387,8 +387,8 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
     """The measurement rows beside the headline: the FP8 W8A8 layer (same
     routing and shapes, per-token / per-channel E4M3, no residual), the
     MXFP4 W4A4 layer (the hardware's native FP4 format, no residual), the
-    plain NVFP4 W4A4 layer (K_s = 0), RAC at K_s = 50% of the channels, and
-    RAC at both the W13 and the W2 inputs."""
+    plain NVFP4 W4A4 layer (K_s = 0), RAC at K_s = 50% of the channels, RAC
+    at both the W13 and the W2 inputs, and the trainer-side W4A16 forward."""
     import torch
     from paper_2607_15810_amd import ops
     dev = "cuda"
@@ -431,6 +431,15 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
                          time_vs_headline=round(ms / ms_step, 3))
         if k2:
             res[name]["rac_channels_w2"] = k2
+    # the trainer-side forward on the same weights (Sec. 3.2: bf16
+    # activations, fake-quantised NVFP4 weights, no activation quantiser)
+    lay16 = [ops.W4A16MoELayer(b13, b2, wl.k) for b13, b2 in banks]
+    ms16 = time_steps([lambda c=c: lay16[c](xs[c], lgs[c]) for c in range(len(lay16))], steps, warm)
+    flop = 2.0 * wl.T * wl.k * (2 * wl.I * wl.H + wl.H * wl.I)
+    res["w4a16_trainer_forward"] = dict(ms_per_step=round(ms16, 5),
+                                        value=round(wl.T / (ms16 * 1e-3), 1), unit="tokens/s",
+                                        gemm_tflops=round(flop / (ms16 * 1e-3) / 1e12, 1),
+                                        time_vs_headline=round(ms16 / ms_step, 3))
     torch.cuda.synchronize()
     return res
 

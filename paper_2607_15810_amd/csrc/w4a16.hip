@@ -11,12 +11,13 @@
 // Kernel: tiles of 128 grouped rows x 128 weight rows (SwiGLU: 64 gate rows
 // and the matching 64 up rows), four waves in a 2 x 2 grid of 64 x 64 on
 // v_mfma_f32_32x32x16_bf16.  K streams in stages of 64 through a double
-// buffer in LDS: each thread loads a half row (32 elements) of activations
-// and of weight codes for the next stage into registers while the current
-// stage is multiplied, then stores the activations as they are and the
-// weights decoded to bf16.  Rows are padded to 72 elements (144 bytes) so
-// that the fragment reads hit distinct banks.  M-tiles follow the shared
-// tile scheduler (no tile straddles two experts; tiles contiguous per XCD).
+// buffer in LDS: each thread keeps a half row (32 elements) of activations
+// and of weight codes of the next two stages in registers (two loads in
+// flight) while the current stage is multiplied, then stores the next
+// stage's activations as they are and its weights decoded to bf16.  Rows
+// are padded to 72 elements (144 bytes) so that the fragment reads hit
+// distinct banks.  M-tiles follow the shared tile scheduler (no tile
+// straddles two experts; tiles contiguous per XCD).
 #include "common.h"
 #include "tile_sched.h"
 
@@ -26,6 +27,7 @@ using namespace qd;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x8_t __attribute__((ext_vector_type(8)));
 
 constexpr int WA_M = 128;            // grouped rows per tile
 constexpr int WA_N = 128;            // weight rows per tile
@@ -50,12 +52,6 @@ __device__ __forceinline__ f32x16_t mfma_bf16(bf16x8_t a, bf16x8_t b, f32x16_t c
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// e2m1(code) * e4m3 scale, exact, as bf16 bits
-__device__ __forceinline__ uint32_t weight_bf16(uint32_t code, float sbf) {
-  float v = e2m1_value(code) * sbf;
-  if (code & 8u) v = -v;
-  return __float_as_uint(v) >> 16;   // exact: at most six significant bits
-}
 
 template <bool GATHER, int EPI>
 __global__ __launch_bounds__(256) void gemm_w4a16_kernel(W16Args p, int ntn) {
@@ -89,32 +85,31 @@ __global__ __launch_bounds__(256) void gemm_w4a16_kernel(W16Args p, int ntn) {
   const uint8_t *bc = p.w_codes + wrow * (K >> 1) + hf * 16;
   const uint8_t *bs = p.w_scales + wrow * (K >> 4) + hf * 2;
 
-  uint4 ra[4], rb;
-  uint32_t rs = 0u;
-  auto load = [&](int k0) {
+  // a stage's half row in registers: activations, weight codes, two scales
+  struct Regs {
+    uint4 a[4], b;
+    uint32_t s;
+  };
+  auto load = [&](Regs &r, int k0) {
     const uint4 *pa = reinterpret_cast<const uint4 *>(ag + k0);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) ra[q] = pa[q];
-    rb = *reinterpret_cast<const uint4 *>(bc + (k0 >> 1));
-    rs = *reinterpret_cast<const uint16_t *>(bs + (k0 >> 4));
+    for (int q = 0; q < 4; ++q) r.a[q] = pa[q];
+    r.b = *reinterpret_cast<const uint4 *>(bc + (k0 >> 1));
+    r.s = *reinterpret_cast<const uint16_t *>(bs + (k0 >> 4));
   };
-  auto store = [&](int buf) {
+  auto store = [&](const Regs &r, int buf) {
     uint4 *da = reinterpret_cast<uint4 *>(&As[buf][ar * WA_LD + hf * 32]);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) da[q] = ra[q];
-    const float s0 = e4m3_to_f32(rs & 0xFFu), s1 = e4m3_to_f32((rs >> 8) & 0xFFu);
-    const uint32_t words[4] = {rb.x, rb.y, rb.z, rb.w};
-    uint32_t o[16];
+    for (int q = 0; q < 4; ++q) da[q] = r.a[q];
+    // the exact f16 decode of the rollout GEMMs (words 0, 1: the first
+    // 16-block, words 2, 3: the second), widened to bf16 without rounding
+    const f16x2 pair = __builtin_bit_cast(f16x2, scale_pair_f16(r.s & 0xFFu, (r.s >> 8) & 0xFFu));
+    const uint32_t words[4] = {r.b.x, r.b.y, r.b.z, r.b.w};
+    bf16x8_t *db = reinterpret_cast<bf16x8_t *>(&Bs[buf][ar * WA_LD + hf * 32]);
 #pragma unroll
-    for (int j = 0; j < 32; j += 2) {
-      const uint32_t wv = words[j >> 3];
-      const float sb = j < 16 ? s0 : s1;
-      o[j >> 1] = weight_bf16((wv >> (4 * (j & 7))) & 15u, sb) |
-                  (weight_bf16((wv >> (4 * ((j + 1) & 7))) & 15u, sb) << 16);
-    }
-    uint4 *db = reinterpret_cast<uint4 *>(&Bs[buf][ar * WA_LD + hf * 32]);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) db[q] = make_uint4(o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]);
+    for (int q = 0; q < 4; ++q)
+      db[q] = __builtin_convertvector(__builtin_convertvector(decode8_sel(words[q], pair, q >= 2), f32x8_t),
+                                      bf16x8_t);
   };
 
   f32x16_t acc[2][2];
@@ -133,13 +128,15 @@ __global__ __launch_bounds__(256) void gemm_w4a16_kernel(W16Args p, int ntn) {
   for (int j = 0; j < 2; ++j)
     brow[j] = EPI == QD_EPI_SWIGLU ? j * 64 + wn * 32 + lr : wn * 64 + j * 32 + lr;
 
+  // Two stages of loads in flight: at the top of iteration s the LDS
+  // buffer s & 1 holds stage s and the two register sets hold (or are
+  // receiving) stages s + 1 and s + 2.  Iteration s multiplies stage s,
+  // stores stage s + 1 into the other buffer (last read in iteration s - 1,
+  // which every thread left through the barrier at its end), and reloads
+  // the freed register set with stage s + 3.  The loop is unrolled by two
+  // so that the register sets keep fixed names.
   const int nst = K / WA_K;
-  load(0);
-  store(0);
-  __syncthreads();
-  for (int s = 0; s < nst; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nst) load((s + 1) * WA_K);
+  auto mma = [&](int buf) {
 #pragma unroll
     for (int kk = 0; kk < WA_K; kk += 16) {
       bf16x8_t af[2], bf[2];
@@ -154,10 +151,22 @@ __global__ __launch_bounds__(256) void gemm_w4a16_kernel(W16Args p, int ntn) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = mfma_bf16(af[i], bf[j], acc[i][j]);
     }
-    // the buffer written here was last read in iteration s - 1, which every
-    // thread left through the barrier at its end
-    if (s + 1 < nst) store((s + 1) & 1);
+  };
+  Regs r0, r1;
+  load(r0, 0);
+  if (nst > 1) load(r1, WA_K);
+  store(r0, 0);
+  if (nst > 2) load(r0, 2 * WA_K);
+  __syncthreads();
+  auto step = [&](int s, Regs &next) {     // next: stage s + 1
+    mma(s & 1);
+    if (s + 1 < nst) store(next, (s + 1) & 1);
+    if (s + 3 < nst) load(next, (s + 3) * WA_K);
     __syncthreads();
+  };
+  for (int s = 0; s < nst; s += 2) {
+    step(s, r1);
+    if (s + 1 < nst) step(s + 1, r0);
   }
 
   // ---- epilogue: the expert's tensor scale, SwiGLU or plain, bf16 stores
