@@ -53,8 +53,48 @@ __device__ __forceinline__ f32x16_t mfma_bf16(bf16x8_t a, bf16x8_t b, f32x16_t c
 }
 
 
+// two workgroups per CU (LDS 74 KB each): two waves per SIMD, so the
+// register budget is 256 per lane and nothing needs to spill
+// A thread's half row (32 elements) of one stage in registers: activations,
+// weight codes and the two E4M3 scale bytes (scalar members, so that it
+// stays in registers).
+struct StageRegs {
+  uint4 a0, a1, a2, a3, b;
+  uint32_t s;
+};
+
+__device__ __forceinline__ StageRegs w16_load(const uint16_t *ag, const uint8_t *bc,
+                                              const uint8_t *bs, int k0) {
+  StageRegs r;
+  const uint4 *pa = reinterpret_cast<const uint4 *>(ag + k0);
+  r.a0 = pa[0];
+  r.a1 = pa[1];
+  r.a2 = pa[2];
+  r.a3 = pa[3];
+  r.b = *reinterpret_cast<const uint4 *>(bc + (k0 >> 1));
+  r.s = *reinterpret_cast<const uint16_t *>(bs + (k0 >> 4));
+  return r;
+}
+
+// activations as they are; weights with the exact f16 decode of the rollout
+// GEMMs (words 0, 1: the first 16-block, words 2, 3: the second), widened to
+// bf16 without rounding
+__device__ __forceinline__ void w16_store(const StageRegs r, uint16_t *arow, uint16_t *brow) {
+  uint4 *da = reinterpret_cast<uint4 *>(arow);
+  da[0] = r.a0;
+  da[1] = r.a1;
+  da[2] = r.a2;
+  da[3] = r.a3;
+  const f16x2 pair = __builtin_bit_cast(f16x2, scale_pair_f16(r.s & 0xFFu, (r.s >> 8) & 0xFFu));
+  bf16x8_t *db = reinterpret_cast<bf16x8_t *>(brow);
+  db[0] = __builtin_convertvector(__builtin_convertvector(decode8_sel(r.b.x, pair, false), f32x8_t), bf16x8_t);
+  db[1] = __builtin_convertvector(__builtin_convertvector(decode8_sel(r.b.y, pair, false), f32x8_t), bf16x8_t);
+  db[2] = __builtin_convertvector(__builtin_convertvector(decode8_sel(r.b.z, pair, true), f32x8_t), bf16x8_t);
+  db[3] = __builtin_convertvector(__builtin_convertvector(decode8_sel(r.b.w, pair, true), f32x8_t), bf16x8_t);
+}
+
 template <bool GATHER, int EPI>
-__global__ __launch_bounds__(256) void gemm_w4a16_kernel(W16Args p, int ntn) {
+__global__ __launch_bounds__(256, 1) void gemm_w4a16_kernel(W16Args p, int ntn) {
   __shared__ __align__(16) uint16_t As[2][WA_M * WA_LD];
   __shared__ __align__(16) uint16_t Bs[2][WA_N * WA_LD];
   __shared__ int32_t src_row[WA_M];
@@ -84,33 +124,6 @@ __global__ __launch_bounds__(256) void gemm_w4a16_kernel(W16Args p, int ntn) {
   const int64_t wrow = (int64_t)t.e * N + (wr < N ? wr : 0);   // others are never stored
   const uint8_t *bc = p.w_codes + wrow * (K >> 1) + hf * 16;
   const uint8_t *bs = p.w_scales + wrow * (K >> 4) + hf * 2;
-
-  // a stage's half row in registers: activations, weight codes, two scales
-  struct Regs {
-    uint4 a[4], b;
-    uint32_t s;
-  };
-  auto load = [&](Regs &r, int k0) {
-    const uint4 *pa = reinterpret_cast<const uint4 *>(ag + k0);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) r.a[q] = pa[q];
-    r.b = *reinterpret_cast<const uint4 *>(bc + (k0 >> 1));
-    r.s = *reinterpret_cast<const uint16_t *>(bs + (k0 >> 4));
-  };
-  auto store = [&](const Regs &r, int buf) {
-    uint4 *da = reinterpret_cast<uint4 *>(&As[buf][ar * WA_LD + hf * 32]);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) da[q] = r.a[q];
-    // the exact f16 decode of the rollout GEMMs (words 0, 1: the first
-    // 16-block, words 2, 3: the second), widened to bf16 without rounding
-    const f16x2 pair = __builtin_bit_cast(f16x2, scale_pair_f16(r.s & 0xFFu, (r.s >> 8) & 0xFFu));
-    const uint32_t words[4] = {r.b.x, r.b.y, r.b.z, r.b.w};
-    bf16x8_t *db = reinterpret_cast<bf16x8_t *>(&Bs[buf][ar * WA_LD + hf * 32]);
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      db[q] = __builtin_convertvector(__builtin_convertvector(decode8_sel(words[q], pair, q >= 2), f32x8_t),
-                                      bf16x8_t);
-  };
 
   f32x16_t acc[2][2];
 #pragma unroll
@@ -152,21 +165,25 @@ __global__ __launch_bounds__(256) void gemm_w4a16_kernel(W16Args p, int ntn) {
         for (int j = 0; j < 2; ++j) acc[i][j] = mfma_bf16(af[i], bf[j], acc[i][j]);
     }
   };
-  Regs r0, r1;
-  load(r0, 0);
-  if (nst > 1) load(r1, WA_K);
-  store(r0, 0);
-  if (nst > 2) load(r0, 2 * WA_K);
+  uint16_t *arow0 = &As[0][ar * WA_LD + hf * 32], *arow1 = &As[1][ar * WA_LD + hf * 32];
+  uint16_t *brow0 = &Bs[0][ar * WA_LD + hf * 32], *brow1 = &Bs[1][ar * WA_LD + hf * 32];
+  StageRegs r0 = w16_load(ag, bc, bs, 0), r1 = r0;
+  if (nst > 1) r1 = w16_load(ag, bc, bs, WA_K);
+  w16_store(r0, arow0, brow0);
+  if (nst > 2) r0 = w16_load(ag, bc, bs, 2 * WA_K);
   __syncthreads();
-  auto step = [&](int s, Regs &next) {     // next: stage s + 1
-    mma(s & 1);
-    if (s + 1 < nst) store(next, (s + 1) & 1);
-    if (s + 3 < nst) load(next, (s + 3) * WA_K);
-    __syncthreads();
-  };
   for (int s = 0; s < nst; s += 2) {
-    step(s, r1);
-    if (s + 1 < nst) step(s + 1, r0);
+    // r1: stage s + 1, r0: stage s + 2 (in flight)
+    mma(0);
+    if (s + 1 < nst) w16_store(r1, arow1, brow1);
+    if (s + 3 < nst) r1 = w16_load(ag, bc, bs, (s + 3) * WA_K);
+    __syncthreads();
+    if (s + 1 >= nst) break;
+    // r0: stage s + 2, r1: stage s + 3 (in flight)
+    mma(1);
+    if (s + 2 < nst) w16_store(r0, arow0, brow0);
+    if (s + 4 < nst) r0 = w16_load(ag, bc, bs, (s + 4) * WA_K);
+    __syncthreads();
   }
 
   // ---- epilogue: the expert's tensor scale, SwiGLU or plain, bf16 stores
