@@ -259,7 +259,7 @@ qd_status nvfp4_pack_frag_scales(const qd_nvfp4 *w, uint8_t *out, void *stream);
  * moe_unpermute_combine -- weighted sum of the k expert outputs per token:
  *   y[t][n] = bf16( sum_{s=0..k-1} topk_w[t][s] * z[inv_row[t][s]][n] ),
  * accumulated in f32 in slot order.
- *   z : bf16 [T*k][H]; y : bf16 [T][H].
+ *   z : bf16 [T*k][H]; y : bf16 [T][H]; 1 <= k <= 32, H % 8 == 0.
  * ------------------------------------------------------------------- */
 qd_status moe_unpermute_combine(const void *z, const int32_t *inv_row, const float *topk_w,
                                 int64_t T, int32_t k, int64_t H, void *y, void *stream);

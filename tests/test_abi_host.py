@@ -159,6 +159,7 @@ def test_select_and_combine_validation(lib):
              None) == Q.QD_ERR_WORKSPACE
     c = lambda *x: Q.raw("moe_unpermute_combine", *x)
     assert c(FAKE, FAKE, FAKE, 4, 2, 12, FAKE, None) == Q.QD_ERR_SHAPE     # H % 8
+    assert c(FAKE, FAKE, FAKE, 4, 33, 16, FAKE, None) == Q.QD_ERR_SHAPE    # k > 32
     assert c(None, None, None, 0, 2, 16, None, None) == Q.QD_OK           # empty batch
 
 

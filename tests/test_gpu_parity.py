@@ -268,6 +268,21 @@ def test_route_topk_paths(T, E, k, renorm):
     assert np.array_equal(inv_row.cpu().numpy(), perm["inv_row"])
 
 
+@pytest.mark.parametrize("T,k,H", [(5, 1, 8), (64, 8, 2048), (7, 12, 4104), (3, 32, 136)])
+def test_combine_slot_counts(T, k, H):
+    """A9 on its own: k <= 8 (all loads in flight) and the generic loop
+    (k > 8), column blocks past one workgroup's 2048 columns, ragged H."""
+    rng = np.random.default_rng(T + k + H)
+    R = T * k
+    zb = np_bf16(torch.from_numpy(rng.standard_normal((R, H)).astype(np.float32)))
+    inv = rng.permutation(R).astype(np.int32).reshape(T, k)
+    w = rng.random((T, k)).astype(np.float32)
+    y = ops.unpermute_combine(bf16_tensor(zb), torch.from_numpy(inv).to(DEV),
+                              torch.from_numpy(w).to(DEV))
+    ref, mag = OL.combine(zb, inv, w)
+    check_close_bf16(np_bf16(y), ref, mag, "combine")
+
+
 def test_dense_gemm_with_rac():
     """16 tokens x K=256 x N=128, 4 outlier channels x30, RAC on 8 channels."""
     inp = synth.generate("dense_t16_k256_n128")
