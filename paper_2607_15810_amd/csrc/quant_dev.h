@@ -163,12 +163,12 @@ inline int amax_grid(int64_t n16) {
 }
 
 // (gx, gy) grid of the quantiser: 16 column blocks per workgroup along x;
-// with RAC at most 256 workgroups (one u64 atomic per channel and workgroup)
+// with RAC at most 1024 workgroups (one u64 atomic per channel and workgroup)
 inline void quant_grid(int64_t rows, int64_t cols, bool rac, int &gx, int &gy) {
   const int64_t nbc = cols / 16;
   gx = (int)((nbc + 15) / 16);
   int64_t g = (rows + 15) / 16;
-  const int64_t cap = rac ? 256 : 4096;
+  const int64_t cap = rac ? 1024 : 4096;
   int64_t lim = cap / gx;
   if (lim < 1) lim = 1;
   if (g > lim) g = lim;

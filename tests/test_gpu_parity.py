@@ -274,7 +274,7 @@ def test_combine_slot_counts(T, k, H):
     (k > 8), column blocks past one workgroup's 2048 columns, ragged H."""
     rng = np.random.default_rng(T + k + H)
     R = T * k
-    zb = np_bf16(torch.from_numpy(rng.standard_normal((R, H)).astype(np.float32)))
+    zb = np_bf16(torch.from_numpy(rng.standard_normal((R, H)).astype(np.float32)).to(torch.bfloat16))
     inv = rng.permutation(R).astype(np.int32).reshape(T, k)
     w = rng.random((T, k)).astype(np.float32)
     y = ops.unpermute_combine(bf16_tensor(zb), torch.from_numpy(inv).to(DEV),
