@@ -154,7 +154,7 @@ __device__ __forceinline__ void quantize_act_body(
   }
 }
 
-constexpr int kAmaxPartials = 256;      // per-call partial maxima (workspace)
+constexpr int kAmaxPartials = 1024;     // per-call partial maxima (workspace)
 
 // workgroups of the amax pass over n16 16-element blocks
 inline int amax_grid(int64_t n16) {
