@@ -61,6 +61,9 @@ SMALL = [
     ("tile_rac_zipf_edges", 300, 512, 8, 2, 128, 40,
      dict(routing="zipf", acts="student_t3", edge_cases=True, outlier_frac=0.0)),
     ("tile_rac_all", 256, 256, 4, 2, 64, 256, {}),
+    # H > 4096 at decode shapes: the one-workgroup selection and the separate
+    # masked-residual pass instead of the fused selection by rank
+    ("wide_h_resq", 16, 5120, 4, 2, 64, 40, {}),
     # many rows per expert: the tiled (prefill) kernel instead of the skinny one
     ("many_rows", 256, 256, 4, 2, 64, 8, {}),
     ("many_rows_ktail", 300, 384, 4, 2, 96, 12, {}),
