@@ -16,10 +16,11 @@ struct Tile {
   int nt;      // weight-row tile index
 };
 
-// Every thread of a 256-thread workgroup calls this; experts E <= 1024 (four
-// per thread).  offsets: expert row offsets [E + 1] (NULL: one expert with
-// `rows` rows).  sh_w, sh_t: 4-int LDS scratch each.
-template <int TM>
+// Every thread of a workgroup of NW waves (NW * 64 threads, NW = 4 or 8)
+// calls this; experts E <= 1024 (the first 256 threads hold four each).
+// offsets: expert row offsets [E + 1] (NULL: one expert with `rows` rows).
+// sh_w: NW ints, sh_t: 4 ints of LDS scratch.
+template <int TM, int NW = 4>
 __device__ __forceinline__ Tile find_tile(const int32_t *__restrict__ offsets, int E, int64_t rows,
                                           int ntn, int *sh_w, int *sh_t) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -43,7 +44,9 @@ __device__ __forceinline__ Tile find_tile(const int32_t *__restrict__ offsets, i
   if (lane == 63) sh_w[w] = xs;
   if (tid == 0) sh_t[0] = -1;
   __syncthreads();
-  const int mt_total = sh_w[0] + sh_w[1] + sh_w[2] + sh_w[3];
+  int mt_total = 0;
+#pragma unroll
+  for (int ww = 0; ww < NW; ++ww) mt_total += sh_w[ww];
   // XCD x = b % 8 takes tiles x * per .. x * per + per - 1
   const int b = blockIdx.x;
   const int ntile = mt_total * ntn;

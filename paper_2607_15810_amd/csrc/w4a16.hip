@@ -8,9 +8,10 @@
 // a bf16 activation times it is exact in f32.  The tensor scale s_dec of the
 // expert multiplies the f32 sum in the epilogue.
 //
-// Kernel: tiles of 128 grouped rows x 128 weight rows (SwiGLU: 64 gate rows
-// and the matching 64 up rows), four waves in a 2 x 2 grid of 64 x 64 on
-// v_mfma_f32_32x32x16_bf16.  K streams in stages of 64 through a double
+// Kernel: tiles of 128 grouped rows x 256 weight rows (SwiGLU: 128 gate rows
+// and the matching 128 up rows), eight waves in a 2 x 4 grid of 64 x 64 on
+// v_mfma_f32_32x32x16_bf16; the wide weight tile halves how often the bf16
+// activations are re-read (once per weight tile).  K streams in stages of 64 through a double
 // buffer in LDS: each thread keeps a half row (32 elements) of activations
 // and of weight codes of the next two stages in registers (two loads in
 // flight) while the current stage is multiplied, then stores the next
@@ -30,7 +31,8 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x8_t __attribute__((ext_vector_type(8)));
 
 constexpr int WA_M = 128;            // grouped rows per tile
-constexpr int WA_N = 128;            // weight rows per tile
+constexpr int WA_N = 256;            // weight rows per tile
+constexpr int WA_THREADS = 512;
 constexpr int WA_K = 64;             // elements per stage
 constexpr int WA_LD = WA_K + 8;      // LDS row stride in bf16 elements
 
@@ -52,14 +54,11 @@ __device__ __forceinline__ f32x16_t mfma_bf16(bf16x8_t a, bf16x8_t b, f32x16_t c
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-
-// two workgroups per CU (LDS 74 KB each): two waves per SIMD, so the
-// register budget is 256 per lane and nothing needs to spill
-// A thread's half row (32 elements) of one stage in registers: activations,
-// weight codes and the two E4M3 scale bytes (scalar members, so that it
-// stays in registers).
+// A thread's share of one stage in registers: a quarter row (16 elements)
+// of activations, a half row of weight codes (32) and their two E4M3 scale
+// bytes (scalar members, so that it stays in registers).
 struct StageRegs {
-  uint4 a0, a1, a2, a3, b;
+  uint4 a0, a1, b;
   uint32_t s;
 };
 
@@ -69,8 +68,6 @@ __device__ __forceinline__ StageRegs w16_load(const uint16_t *ag, const uint8_t 
   const uint4 *pa = reinterpret_cast<const uint4 *>(ag + k0);
   r.a0 = pa[0];
   r.a1 = pa[1];
-  r.a2 = pa[2];
-  r.a3 = pa[3];
   r.b = *reinterpret_cast<const uint4 *>(bc + (k0 >> 1));
   r.s = *reinterpret_cast<const uint16_t *>(bs + (k0 >> 4));
   return r;
@@ -83,8 +80,6 @@ __device__ __forceinline__ void w16_store(const StageRegs r, uint16_t *arow, uin
   uint4 *da = reinterpret_cast<uint4 *>(arow);
   da[0] = r.a0;
   da[1] = r.a1;
-  da[2] = r.a2;
-  da[3] = r.a3;
   const f16x2 pair = __builtin_bit_cast(f16x2, scale_pair_f16(r.s & 0xFFu, (r.s >> 8) & 0xFFu));
   bf16x8_t *db = reinterpret_cast<bf16x8_t *>(brow);
   db[0] = __builtin_convertvector(__builtin_convertvector(decode8_sel(r.b.x, pair, false), f32x8_t), bf16x8_t);
@@ -94,32 +89,33 @@ __device__ __forceinline__ void w16_store(const StageRegs r, uint16_t *arow, uin
 }
 
 template <bool GATHER, int EPI>
-__global__ __launch_bounds__(256, 1) void gemm_w4a16_kernel(W16Args p, int ntn) {
+__global__ __launch_bounds__(WA_THREADS) void gemm_w4a16_kernel(W16Args p, int ntn) {
   __shared__ __align__(16) uint16_t As[2][WA_M * WA_LD];
   __shared__ __align__(16) uint16_t Bs[2][WA_N * WA_LD];
   __shared__ int32_t src_row[WA_M];
-  __shared__ int sh_w[4], sh_t[4];
-  const qdt::Tile t = qdt::find_tile<WA_M>(p.offsets, p.E, p.rows, ntn, sh_w, sh_t);
+  __shared__ int sh_w[8], sh_t[4];
+  const qdt::Tile t = qdt::find_tile<WA_M, 8>(p.offsets, p.E, p.rows, ntn, sh_w, sh_t);
   if (t.e < 0) return;                        // whole workgroup
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w >> 2, wn = w & 3;
   const int K = p.K, N = p.N;
-  for (int r = tid; r < WA_M; r += 256) {
+  for (int r = tid; r < WA_M; r += WA_THREADS) {
     const int64_t g = t.row0 + (r < t.nrows ? r : 0);   // rows past the tile read its first
     src_row[r] = GATHER ? p.row_token[g] : (int32_t)g;
   }
   __syncthreads();
 
-  // this thread's half row (32 elements) of each stage: tile row / weight
-  // row ar, half hf
-  const int ar = tid >> 1, hf = tid & 1;
-  const uint16_t *ag = p.a + (int64_t)src_row[ar] * K + hf * 32;
+  // this thread's share of each stage: a quarter row (16 elements) of tile
+  // row ar, and a half row (32 elements) of weight row br
+  const int ar = tid >> 2, aq = tid & 3;
+  const int br = tid >> 1, hf = tid & 1;
+  const uint16_t *ag = p.a + (int64_t)src_row[ar] * K + aq * 16;
   int wr;
   if (EPI == QD_EPI_SWIGLU) {
     const int I = N >> 1;
-    wr = ar < 64 ? t.nt * 64 + ar : I + t.nt * 64 + (ar - 64);
+    wr = br < 128 ? t.nt * 128 + br : I + t.nt * 128 + (br - 128);
   } else {
-    wr = t.nt * WA_N + ar;
+    wr = t.nt * WA_N + br;
   }
   const int64_t wrow = (int64_t)t.e * N + (wr < N ? wr : 0);   // others are never stored
   const uint8_t *bc = p.w_codes + wrow * (K >> 1) + hf * 16;
@@ -139,7 +135,7 @@ __global__ __launch_bounds__(256, 1) void gemm_w4a16_kernel(W16Args p, int ntn) 
   int brow[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j)
-    brow[j] = EPI == QD_EPI_SWIGLU ? j * 64 + wn * 32 + lr : wn * 64 + j * 32 + lr;
+    brow[j] = EPI == QD_EPI_SWIGLU ? j * 128 + wn * 32 + lr : wn * 64 + j * 32 + lr;
 
   // Two stages of loads in flight: at the top of iteration s the LDS
   // buffer s & 1 holds stage s and the two register sets hold (or are
@@ -165,8 +161,8 @@ __global__ __launch_bounds__(256, 1) void gemm_w4a16_kernel(W16Args p, int ntn) 
         for (int j = 0; j < 2; ++j) acc[i][j] = mfma_bf16(af[i], bf[j], acc[i][j]);
     }
   };
-  uint16_t *arow0 = &As[0][ar * WA_LD + hf * 32], *arow1 = &As[1][ar * WA_LD + hf * 32];
-  uint16_t *brow0 = &Bs[0][ar * WA_LD + hf * 32], *brow1 = &Bs[1][ar * WA_LD + hf * 32];
+  uint16_t *arow0 = &As[0][ar * WA_LD + aq * 16], *arow1 = &As[1][ar * WA_LD + aq * 16];
+  uint16_t *brow0 = &Bs[0][br * WA_LD + hf * 32], *brow1 = &Bs[1][br * WA_LD + hf * 32];
   StageRegs r0 = w16_load(ag, bc, bs, 0), r1 = r0;
   if (nst > 1) r1 = w16_load(ag, bc, bs, WA_K);
   w16_store(r0, arow0, brow0);
@@ -197,7 +193,7 @@ __global__ __launch_bounds__(256, 1) void gemm_w4a16_kernel(W16Args p, int ntn) 
       const int64_t row = t.row0 + rl;
       if (EPI == QD_EPI_SWIGLU) {
         const int I = N >> 1;
-        const int col = t.nt * 64 + wn * 32 + lr;
+        const int col = t.nt * 128 + wn * 32 + lr;
         if (col < I) {
           const float gv = alpha * acc[i][0][q];
           const float uv = alpha * acc[i][1][q];
@@ -249,21 +245,21 @@ extern "C" qd_status moe_w4a16_grouped_gemm(const void *a, int64_t a_rows,
   p.N = (int)N;
   p.K = (int)K;
   p.out = static_cast<uint16_t *>(out);
-  const int ntn = epilogue == QD_EPI_SWIGLU ? (int)((N / 2 + 63) / 64) : (int)((N + WA_N - 1) / WA_N);
+  const int ntn = epilogue == QD_EPI_SWIGLU ? (int)((N / 2 + 127) / 128) : (int)((N + WA_N - 1) / WA_N);
   const int64_t grid = qdt::tile_grid(rows, E, WA_M, ntn);
   if (grid > 0x7fffffffLL) return QD_ERR_UNSUPPORTED;
   hipStream_t s = qdh::S(stream);
   const dim3 g((unsigned)grid);
   if (row_token) {
     if (epilogue == QD_EPI_SWIGLU)
-      hipLaunchKernelGGL((gemm_w4a16_kernel<true, QD_EPI_SWIGLU>), g, dim3(256), 0, s, p, ntn);
+      hipLaunchKernelGGL((gemm_w4a16_kernel<true, QD_EPI_SWIGLU>), g, dim3(WA_THREADS), 0, s, p, ntn);
     else
-      hipLaunchKernelGGL((gemm_w4a16_kernel<true, QD_EPI_NONE>), g, dim3(256), 0, s, p, ntn);
+      hipLaunchKernelGGL((gemm_w4a16_kernel<true, QD_EPI_NONE>), g, dim3(WA_THREADS), 0, s, p, ntn);
   } else {
     if (epilogue == QD_EPI_SWIGLU)
-      hipLaunchKernelGGL((gemm_w4a16_kernel<false, QD_EPI_SWIGLU>), g, dim3(256), 0, s, p, ntn);
+      hipLaunchKernelGGL((gemm_w4a16_kernel<false, QD_EPI_SWIGLU>), g, dim3(WA_THREADS), 0, s, p, ntn);
     else
-      hipLaunchKernelGGL((gemm_w4a16_kernel<false, QD_EPI_NONE>), g, dim3(256), 0, s, p, ntn);
+      hipLaunchKernelGGL((gemm_w4a16_kernel<false, QD_EPI_NONE>), g, dim3(WA_THREADS), 0, s, p, ntn);
   }
   return qdh::check_launch();
 }
