@@ -110,6 +110,19 @@ __device__ __forceinline__ uint32_t quantize_block(const float (&x)[16], float s
 }
 
 // Q8 value of one code: fl(fl(e2m1 * sbf) * s_dec); the first product is exact.
+// The 8 codes of a word (element j in bits 4j .. 4j+3) as their exact signed
+// E2M1 values: the hardware conversion with a unit scale, two per
+// instruction.
+typedef float f32x2_pair __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void e2m1_word_values(uint32_t w, float *v) {
+  const f32x2_pair p0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 0);
+  const f32x2_pair p1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 1);
+  const f32x2_pair p2 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 2);
+  const f32x2_pair p3 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 3);
+  v[0] = p0[0]; v[1] = p0[1]; v[2] = p1[0]; v[3] = p1[1];
+  v[4] = p2[0]; v[5] = p2[1]; v[6] = p3[0]; v[7] = p3[1];
+}
+
 __device__ __forceinline__ float dequant_value(uint32_t code, float sbf, float s_dec) {
   float p = e2m1_value(code) * sbf;
   p = (code & 8u) ? -p : p;

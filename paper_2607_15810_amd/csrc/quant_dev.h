@@ -122,11 +122,14 @@ __device__ __forceinline__ void quantize_act_body(
       reinterpret_cast<uint2 *>(codes + r * (cols >> 1))[cb] = make_uint2(lo, hi);
       scales[r * nbc + cb] = (uint8_t)sb;
       if (RAC) {
+        // x_hat = fl(fl(e2m1 * e4m3) * s_dec), as dequant_value
         const float sbf = e4m3_to_f32(sb);
+        float ev[16];
+        e2m1_word_values(lo, ev);
+        e2m1_word_values(hi, ev + 8);
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          uint32_t c = ((i < 8 ? lo : hi) >> (4 * (i & 7))) & 15u;
-          float xh = dequant_value(c, sbf, s_dec);
+          float xh = (ev[i] * sbf) * s_dec;
           float rr = xh - v[i];
           rmax = fmaxf(rmax, fabsf(rr));
           acc[i] += fixed_point_term(rr * rr, F);   // each term < 2^37

@@ -23,11 +23,11 @@ __device__ __forceinline__ void load_bf16x16(const uint16_t *p, float (&x)[16]) 
 __device__ __forceinline__ void block_residual(const float (&x)[16], uint2 cw, uint32_t sb,
                                                float s_dec, float (&r)[16]) {
   const float sbf = e4m3_to_f32(sb);
+  float ev[16];
+  e2m1_word_values(cw.x, ev);
+  e2m1_word_values(cw.y, ev + 8);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    uint32_t c = ((i < 8 ? cw.x : cw.y) >> (4 * (i & 7))) & 15u;
-    r[i] = dequant_value(c, sbf, s_dec) - x[i];
-  }
+  for (int i = 0; i < 16; ++i) r[i] = (ev[i] * sbf) * s_dec - x[i];   // as dequant_value
 }
 
 // Block-wide exclusive scan of one int per thread (1024 threads).
