@@ -79,12 +79,24 @@ __global__ __launch_bounds__(256) void layer_resq_kernel(
 
 // the residual at the selected channels, compacted per token (what the
 // prefill W13 kernel consumes), with the residual's tensor scale
+// (bitmap not NULL: S comes as the selection bitmap; every workgroup lists
+// it into LDS, and workgroup 0 also into sel for the GEMM)
 __global__ __launch_bounds__(256) void layer_compact_kernel(
     const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
     const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
-    const float *__restrict__ ramax, const int32_t *__restrict__ sel, int Ks, int width,
-    uint16_t *__restrict__ out, float *__restrict__ rgs) {
-  qdc::rac_compact_body(blockIdx.x, gridDim.x, x, xcodes, xscales, xgs, T, K, ramax, sel, Ks,
+    const float *__restrict__ ramax, int32_t *__restrict__ sel, int Ks, int width,
+    uint16_t *__restrict__ out, float *__restrict__ rgs, const uint32_t *__restrict__ bitmap) {
+  __shared__ int32_t lsel[qdc::kRankSelMaxK];
+  __shared__ int sh[1024 + 32];
+  const int32_t *sp = sel;
+  if (bitmap) {
+    qdc::rac_list_selected(bitmap, (int)K, lsel, sh);
+    __syncthreads();
+    if (blockIdx.x == 0)
+      for (int i = threadIdx.x; i < Ks; i += blockDim.x) sel[i] = lsel[i];
+    sp = lsel;
+  }
+  qdc::rac_compact_body(blockIdx.x, gridDim.x, x, xcodes, xscales, xgs, T, K, ramax, sp, Ks,
                         width, out, rgs);
 }
 
@@ -248,6 +260,9 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   // compact form)
   const bool rank_sel = rac && !want_sel && H <= qdc::kRankSelMaxK &&
                         qdi::gemm_takes_bitmap(R, E, 2 * I, H, Ks, QD_EPI_SWIGLU);
+  // for the compact residual (H <= 4096) the selection by rank alone, with S
+  // listed from the bitmap by the compact-residual kernel
+  const bool rank_only = want_sel && H <= qdc::kRankSelMaxK;
   void *rq_sel = want_sel ? P(QD_VIEW_RQ_SEL) : nullptr;
   hipStream_t s = qdh::S(stream);
   // routing scratch, amax partials of X and the channel bitmap (the same
@@ -280,12 +295,12 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   mark(QD_STAGE_SELECT);
   if (rac) {
     const dim3 g3((unsigned)(nr + 1));
-    if (rank_sel)
+    if (rank_sel || rank_only)
       hipLaunchKernelGGL(layer_pre3r_kernel, dim3((unsigned)(nr + H / 16)),
                          dim3(qdc::kRankSelThreads), 0, s, T,
                          E, k, nr, ids, counts, ranks, offs, row_token, inv_row, scores, (int)H,
                          Ks, bitmap, static_cast<const uint16_t *>(x), xq.codes, xq.scales,
-                         xq.gscale, ramax, rq.codes, rq.scales, rq.gscale);
+                         xq.gscale, ramax, rank_sel ? rq.codes : nullptr, rq.scales, rq.gscale);
     else if (H <= 2048)
       hipLaunchKernelGGL(layer_pre3_kernel<8>, g3, dim3(256), 0, s, T, E, k, nr, ids, counts,
                          ranks, offs, row_token, inv_row, scores, (int)H, Ks, sel, bitmap);
@@ -306,7 +321,8 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
       if (g < 1) g = 1;
       hipLaunchKernelGGL(layer_compact_kernel, dim3((unsigned)g), dim3(256), 0, s,
                          static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
-                         ramax, sel, Ks, width, static_cast<uint16_t *>(rq_sel), rq.gscale);
+                         ramax, sel, Ks, width, static_cast<uint16_t *>(rq_sel), rq.gscale,
+                         rank_only ? bitmap : nullptr);
     } else if (!rank_sel) {
       const int64_t total = T * (H / 16);
       int64_t g = (total + 255) / 256;

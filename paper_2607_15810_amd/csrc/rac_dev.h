@@ -296,8 +296,8 @@ __device__ __forceinline__ void rac_select_body(const uint64_t *__restrict__ sco
 // and j < c}.  The ranks are a permutation of 0..K-1, so the channels of
 // rank < K_s are exactly the K_s the threshold selection above takes (top
 // K_s by score, ties to the lower index).  The workgroup stores its 16 bits
-// of the bitmap, then quantises the residual of its column block for every
-// row and masks it (the block arithmetic of rac_resq_body).  64 threads
+// of the bitmap, then (rcodes not NULL) quantises the residual of its column
+// block for every row and masks it (the block arithmetic of rac_resq_body).  64 threads
 // share a channel: thread (part p, channel o) counts over the channels
 // j = p (mod 64) of a copy of the scores in LDS, so the four parts of a
 // wave read four consecutive scores per step.
@@ -353,6 +353,7 @@ __device__ __forceinline__ void rac_rank_select_body(
     }
   }
   __syncthreads();
+  if (!rcodes) return;                  // selection only (the compact residual follows)
   // the masked residual of column block g
   const uint32_t m16 = s_bits;
   const float amax_r = ramax[0];
@@ -384,6 +385,23 @@ __device__ __forceinline__ void rac_rank_select_body(
     }
     reinterpret_cast<uint2 *>(rcodes)[bi] = make_uint2(lo, hi);
     rscales[bi] = (uint8_t)sb;
+  }
+}
+
+// S in ascending order from the selection bitmap (K <= 8192, at most one
+// word per thread of a 256-thread workgroup) into `out` (LDS or global).
+// Every thread of the workgroup calls it; sh: 1024 + 32 ints of LDS.
+__device__ __forceinline__ void rac_list_selected(const uint32_t *__restrict__ bitmap, int K,
+                                                  int32_t *out, int *sh) {
+  const int tid = threadIdx.x;
+  const int nw = (K + 31) >> 5;
+  uint32_t m = tid < nw ? bitmap[tid] : 0u;
+  if (tid == nw - 1 && (K & 31)) m &= (1u << (K & 31)) - 1u;
+  int tot;
+  int pos = block_exclusive_scan(__popc(m), sh, tot);
+  while (m) {
+    out[pos++] = tid * 32 + (__ffs(m) - 1);
+    m &= m - 1u;
   }
 }
 
