@@ -355,7 +355,9 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   qd_nvfp4 hr{(uint8_t *)P(QD_VIEW_HR_CODES), (uint8_t *)P(QD_VIEW_HR_SCALES),
               (float *)P(QD_VIEW_HR_GSCALE), 1, R, I};
   int32_t *sel2 = (int32_t *)P(QD_VIEW_SEL2);
+  uint32_t *bitmap2 = reinterpret_cast<uint32_t *>(b + L.sel2_ws);
   void *hr_sel = nullptr;
+  bool bm2 = false;                 // the W2 GEMM takes S as a bitmap
   if (!rac2) {
     st = nvfp4_quantize_act(h, QD_DTYPE_BF16, R, I, hamax,
                             moe_w4a4_grouped_gemm_amax_count(R, 2 * I, H, E, Ks, QD_EPI_SWIGLU),
@@ -370,19 +372,51 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
     st = nvfp4_quantize_act(h, QD_DTYPE_BF16, R, I, nullptr, 0, &hq, hscores, hramax,
                             b + L.q2_ws, nvfp4_quantize_act_workspace(R, I), stream);
     if (st) return st;
-    st = rac_select_channels(h, &hq, Ks2, hscores, hramax, 1, sel2, &hr, b + L.sel2_ws,
-                             rac_select_channels_workspace(R, I), stream);
-    if (st) return st;
-    if (qdi::gemm_wants_rq_sel(R, E, H, I, Ks2, QD_EPI_NONE)) {
-      hr_sel = P(QD_VIEW_HR_SEL);
-      st = rac_gather_selected(&hr, sel2, Ks2, hr_sel, stream);
+    // as at the W13 site: for I <= 4096 the selection by rank (one
+    // workgroup per 16-channel block; no routing workgroups here), with the
+    // masked residual for the decode GEMM in bitmap mode, or with S listed
+    // by the compact-residual kernel for the tile GEMM
+    const bool want2 = qdi::gemm_wants_rq_sel(R, E, H, I, Ks2, QD_EPI_NONE);
+    bm2 = !want2 && I <= qdc::kRankSelMaxK &&
+          qdi::gemm_takes_bitmap(R, E, H, I, Ks2, QD_EPI_NONE);
+    const bool ro2 = want2 && I <= qdc::kRankSelMaxK;
+    if (want2) hr_sel = P(QD_VIEW_HR_SEL);
+    if (bm2 || ro2) {
+      hipLaunchKernelGGL(layer_pre3r_kernel, dim3((unsigned)(I / 16)),
+                         dim3(qdc::kRankSelThreads), 0, s, R, E, k, 0, ids, counts, ranks, offs,
+                         row_token, inv_row, hscores, (int)I, Ks2, bitmap2, h, hq.codes,
+                         hq.scales, hq.gscale, hramax, bm2 ? hr.codes : nullptr, hr.scales,
+                         hr.gscale);
+      if (ro2) {
+        const int width = rac_selected_width(Ks2);
+        int64_t g = (R * width + 255) / 256;
+        if (g > 8192) g = 8192;
+        if (g < 1) g = 1;
+        hipLaunchKernelGGL(layer_compact_kernel, dim3((unsigned)g), dim3(256), 0, s, h, hq.codes,
+                           hq.scales, hq.gscale, R, I, hramax, sel2, Ks2, width,
+                           static_cast<uint16_t *>(hr_sel), hr.gscale, bitmap2);
+      }
+      st = qdh::check_launch();
       if (st) return st;
+    } else {
+      st = rac_select_channels(h, &hq, Ks2, hscores, hramax, 1, sel2, &hr, b + L.sel2_ws,
+                               rac_select_channels_workspace(R, I), stream);
+      if (st) return st;
+      if (want2) {
+        st = rac_gather_selected(&hr, sel2, Ks2, hr_sel, stream);
+        if (st) return st;
+      }
     }
   }
   uint16_t *z = (uint16_t *)P(QD_VIEW_Z);
   mark(QD_STAGE_W2);
-  st = moe_w4a4_grouped_gemm(&hq, nullptr, offs, E, R, w2, rac2 ? &hr : nullptr,
-                             rac2 ? sel2 : nullptr, Ks2, hr_sel, QD_EPI_NONE, z, nullptr, stream);
+  if (bm2)
+    st = qdi::grouped_gemm_bitmap(&hq, nullptr, offs, E, R, w2, &hr, bitmap2, Ks2, sel2,
+                                  QD_EPI_NONE, z, nullptr, s);
+  else
+    st = moe_w4a4_grouped_gemm(&hq, nullptr, offs, E, R, w2, rac2 ? &hr : nullptr,
+                               rac2 ? sel2 : nullptr, Ks2, hr_sel, QD_EPI_NONE, z, nullptr,
+                               stream);
   if (st) return st;
   mark(QD_STAGE_COMBINE);
   st = moe_unpermute_combine(z, inv_row, wts, T, k, H, y, stream);

@@ -186,6 +186,8 @@ W2RAC = [
     ("w2rac_all_ks0", 64, 256, 8, 2, 64, 0, 64, {}),
     ("w2rac_zipf_edges", 300, 512, 8, 2, 128, 40, 20,
      dict(routing="zipf", acts="student_t3", edge_cases=True, outlier_frac=0.0)),
+    # many rows per expert at W2 (the tile kernel with the compact residual)
+    ("w2rac_prefill_tile", 512, 256, 2, 2, 256, 8, 24, {}),
 ]
 
 
@@ -229,8 +231,14 @@ def test_layer_w2_site_rac(case):
     assert torch.equal(v["hq_codes"], hq_g.codes[0])
     assert torch.equal(v["h_scores"], sc_g)
     assert torch.equal(v["sel2"], sel_g)
-    assert torch.equal(v["hr_codes"], hr_g.codes[0])
-    assert torch.equal(v["hr_scales"], hr_g.scales[0])
+    # the W2 residual: in full, or compacted to S for the tile kernel (many
+    # rows per expert, I and H multiples of 128, I >= 256)
+    tile_w2 = R > E * 48 and I >= 256 and I % 128 == 0 and H % 128 == 0
+    if tile_w2:
+        assert torch.equal(v["hr_sel"], ops.gather_selected(hr_g, sel_g))
+    else:
+        assert torch.equal(v["hr_codes"], hr_g.codes[0])
+        assert torch.equal(v["hr_scales"], hr_g.scales[0])
     zg, _ = ops.grouped_gemm(hq_g, w2, R, None, v["offsets"], hr_g, sel_g)
     yg = ops.unpermute_combine(zg, v["inv_row"], v["w"])
     assert torch.equal(y.view(torch.int16), yg.view(torch.int16))
