@@ -244,3 +244,20 @@ def test_mxfp4_validation(lib):
     assert f(FAKE, FAKE, 16, 256, 4, 2, 256, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16,
              None) == Q.QD_ERR_WORKSPACE
 
+
+def test_w4a16_validation(lib):
+    F = 1 << 20
+    w = Q.NVFP4(F, F, F, 2, 64, 128)          # E = 2 groups of [64][128]
+    g = lambda *a: Q.raw("moe_w4a16_grouped_gemm", *a)
+    assert g(F, 16, None, F, 2, 16, None, 0, F, None) == Q.QD_ERR_NULL           # no weights
+    assert g(F, 16, None, F, 2, 16, ctypes.byref(w), 7, F, None) == Q.QD_ERR_DTYPE
+    assert g(F, 16, None, None, 2, 16, ctypes.byref(w), 0, F, None) == Q.QD_ERR_SHAPE  # E > 1, no offsets
+    assert g(F, 8, None, F, 2, 16, ctypes.byref(w), 0, F, None) == Q.QD_ERR_SHAPE  # rows > a_rows
+    assert g(F, 16, None, F, 1025, 16, ctypes.byref(w), 0, F, None) == Q.QD_ERR_SHAPE
+    w_bad_k = Q.NVFP4(F, F, F, 2, 64, 96)     # K % 64
+    assert g(F, 16, None, F, 2, 16, ctypes.byref(w_bad_k), 0, F, None) == Q.QD_ERR_SHAPE
+    w_bad_n = Q.NVFP4(F, F, F, 2, 48, 128)    # N % 32
+    assert g(F, 16, None, F, 2, 16, ctypes.byref(w_bad_n), 0, F, None) == Q.QD_ERR_SHAPE
+    assert g(F + 2, 16, None, F, 2, 16, ctypes.byref(w), 0, F, None) == Q.QD_ERR_ALIGN
+    assert g(None, 0, None, F, 2, 0, ctypes.byref(w), 0, None, None) == Q.QD_OK   # no rows
+
