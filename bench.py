@@ -440,6 +440,23 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
                                         value=round(wl.T / (ms16 * 1e-3), 1), unit="tokens/s",
                                         gemm_tflops=round(flop / (ms16 * 1e-3) / 1e12, 1),
                                         time_vs_headline=round(ms16 / ms_step, 3))
+    # train/inference alignment (the analogue of the paper's layer-output
+    # comparison, Sec. 4): relative L2 distance of each rollout layer's output
+    # from the trainer-side W4A16 forward on the same weights and tokens
+    b13, b2 = banks[0]
+    y_train = lay16[0](xs[0], lgs[0]).float()
+    ref = torch.linalg.vector_norm(y_train).item()
+
+    def gap(y):
+        return round(torch.linalg.vector_norm(y.float() - y_train).item() / max(ref, 1e-30), 6)
+
+    mism = {}
+    for name, ks, k2 in (("w4a4_ks0", 0, 0), ("nvfp4_rac", wl.Ks, 0), ("rac_ks_half", wl.H // 2, 0),
+                         ("rac_w13_and_w2", wl.Ks, ks2)):
+        lay = ops.MoELayer(b13, b2, wl.T, wl.k, ks, ws=ws, Ks2=k2)
+        mism[name] = gap(lay(xs[0], lgs[0]))
+    res["train_infer_rel_l2"] = mism
+    del lay16
     torch.cuda.synchronize()
     return res
 
