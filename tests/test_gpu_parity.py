@@ -587,3 +587,35 @@ def test_layer_graph_replay():
             g.replay()
             torch.cuda.synchronize()
             assert torch.equal(y.view(torch.int16), y_eager.view(torch.int16)), (name, rep)
+
+
+@pytest.mark.parametrize("chans", [tuple(range(64)), (5, 200, 511), (511,), (0, 63, 64, 127, 448)],
+                         ids=["one_stage_64", "spread_3", "last_channel", "stage_edges"])
+def test_tile_gemm_rac_clustered_selection(chans):
+    """The prefill tile GEMM with RAC (2 experts x 256 rows, K=512, N=256)
+    when the selected channels crowd into one 64-channel stage, sit at stage
+    edges or on the last channel: the compact weight table is filled stage by
+    stage (Sec. 3.3, Eq. (residual-recon)).  The planted channels carry x1000
+    outliers, so they are the selection."""
+    E, T, K, N = 2, 512, 512, 256
+    g = torch.Generator().manual_seed(zlib.crc32(repr(chans).encode()))
+    x = torch.randn((T, K), generator=g)
+    x[:, list(chans)] *= 1000.0
+    x = x.to(torch.bfloat16)
+    wb = (torch.randn((E, N, K), generator=g) * 0.02).to(torch.bfloat16)
+    w = ops.quantize_weight(wb.to(DEV))
+    W = oracle_bank(wb)
+    assert_bank_equal(w, W, list(range(E)))
+    Ks = len(chans)
+    xg = x.to(DEV)
+    xq, scores, ramax = ops.quantize_act(xg, rac=True)
+    act = OR.rac_activation(np_bf16(x), Ks)
+    assert_nvfp4_equal(xq, act["xq"], "xq")
+    sel, rq, _, _ = ops.select_channels(xg, xq, Ks, scores, ramax)
+    assert np.array_equal(sel.cpu().numpy(), act["sel"])
+    assert sorted(act["sel"].tolist()) == sorted(chans)
+    offsets = np.array([0, 256, 512])
+    out, _ = ops.grouped_gemm(xq, w, T, offsets=torch.tensor(offsets, dtype=torch.int32, device=DEV),
+                              rq=rq, sel=sel)
+    ref, mag = OL.w13_stage(act["xq"], act["rq"], None, offsets, W)
+    check_close_bf16(np_bf16(out), ref, mag, f"tile rac {chans[:3]}")
