@@ -1078,6 +1078,17 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
 #pragma unroll
           for (int t = 0; t < 16; ++t) acc[i][j][t] = 0.0f;
       TlRaw R0, R1;
+      // RAC: the tokens of this lane's residual rows, loaded before the K
+      // loop so the residual steps after it wait for one load, not two
+      int32_t tkr[MTV > 0 ? MTV : 1];
+      if constexpr (RAC && MTV > 0) {
+#pragma unroll
+        for (int i = 0; i < MTV; ++i) {
+          const int rr = 32 * (fa0 + i) + (lane & 31);
+          const int rc = rr < nrows ? rr : 0;
+          tkr[i] = GATHER ? p.row_token[row0 + rc] : row0 + rc;
+        }
+      }
 #pragma unroll
       for (int t = 0; t < NS - 1; ++t) issue(t, t);
       wait_vm<(NS - 2) * 5>();
@@ -1132,12 +1143,7 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
             const int h = lane >> 5;
             const uint16_t *ar[MTV];
 #pragma unroll
-            for (int i = 0; i < MTV; ++i) {
-              const int rr = 32 * (fa0 + i) + (lane & 31);
-              const int rc = rr < nrows ? rr : 0;
-              const int64_t tk = GATHER ? (int64_t)p.row_token[row0 + rc] : (int64_t)(row0 + rc);
-              ar[i] = p.r_sel + tk * ksa + 8 * h;
-            }
+            for (int i = 0; i < MTV; ++i) ar[i] = p.r_sel + (int64_t)tkr[i] * ksa + 8 * h;
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
