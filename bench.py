@@ -10,13 +10,19 @@ between steps.  Prints one JSON line.
     python bench.py [--steps K] [--warmup W] [--workload NAME]
     python bench.py --copy-bytes N     # plain device copy, for counter calibration
 
-`roofline` describes the dominant kernel (the W13 grouped GEMM): its
-algorithmic bytes (decode) or FLOPs (prefill) per launch over its average
-duration, timed with HIP events recorded on the layer's stream at the stage
-boundaries.  `roofline.traffic` is the kernel's measured HBM traffic per
-launch, taken from the counter summary under profiles/ when that summary was
-made from the current GEMM source (its SHA-256 is recorded there), else
-null.  `cpu_baseline` times the CPU oracle on a bounded sample.
+The headline workload is the largest one that fits a GPU (4096 tokens,
+H = 4096, I = 1536); `per_config` adds the other MoE workloads, timed in the
+same run.  Step times are the median of per-step HIP-event intervals over
+the K timed steps (the mean beside it).  `roofline` describes the dominant
+kernel (the W13 grouped GEMM): its algorithmic bytes (decode) or FLOPs
+(prefill) per launch over its average duration, timed with HIP events
+recorded on the layer's stream at the stage boundaries, against the
+published peak and against the achievable peak measured by the library's
+probes in the same run.  `roofline.traffic` is the kernel's measured HBM
+traffic per launch, taken from the counter summary under profiles/ when that
+summary was made from the current GEMM source (its SHA-256 is recorded
+there), else null.  `cpu_baseline` times the CPU oracle's whole forward on a
+token sample of the headline workload.
 """
 
 import argparse
@@ -38,6 +44,9 @@ PEAK_FP8_TFLOPS = 5000.0
 PEAK_FP4_TFLOPS = 10100.0
 NVFP4_BYTES_PER_ELEM = 0.5625   # 4-bit code + one E4M3 byte per 16 elements
 
+HEADLINE = "moe_prefill_t4096_h4096"
+PER_CONFIG = ["moe_decode_t256_h2048", "moe_prefill_t8192_h2048", "moe_zipf_decode_t64_h4096",
+              "moe_prefill_t4096_h4096"]
 DECODE = {"moe_decode_t256_h2048", "moe_zipf_decode_t64_h4096", "dense_t16_k256_n128"}
 
 
@@ -46,16 +55,18 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="moe_decode_t256_h2048")
+    ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--copies", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparisons", action="store_true",
                     help="skip the FP8 / MXFP4 layers and the K_s = 0 / 50%% rows")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="time the headline workload only")
     ap.add_argument("--ks-sweep", action="store_true",
                     help="add a K_s sweep (0, 12.5, 25, 50, 75, 100%% of the channels and the "
                          "configured K_s): step time and compensated-activation error")
-    ap.add_argument("--cpu-experts", type=int, default=0,
-                    help="experts in the oracle sample (0: automatic)")
+    ap.add_argument("--cpu-tokens", type=int, default=8,
+                    help="tokens of the headline batch in the oracle's timed sample")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device-to-device copy of this many bytes "
                          "(5 times), the reference kernel for HBM counter calibration")
@@ -124,119 +135,131 @@ def algorithmic(wl, counts):
                 w13_bytes=w13_launch_bytes, w13_flops=w13_flops)
 
 
-def cpu_baseline(inp, n_sample_experts):
-    """The oracle's free-running forward, timed on the host cores.
+def _oracle_banks(inp, experts):
+    """The oracle's own quantisation of the given experts' weights (the others
+    stay zero and receive no rows); experts are independent, so they are
+    quantised on a pool of threads."""
+    import concurrent.futures as cf
+    from oracle import quant as OQ
+    wl = inp.wl
+    banks = []
+    for src, N, K in ((inp.w13, 2 * wl.I, wl.H), (inp.w2, wl.H, wl.I)):
+        b = dict(codes=np.zeros((wl.E, N, K), np.uint8),
+                 scales=np.zeros((wl.E, N, K // 16), np.uint8),
+                 gscale=np.ones((wl.E, 2), np.float32))
 
-    Bounded sample: routing and the RAC activation path run on the whole
-    batch; the expert GEMMs run for the rows of `n_sample_experts` of the
-    most loaded experts and their time is scaled by touched/sampled.  The
-    oracle quantises the sampled experts' weights itself (not timed: weights
-    are quantised once per weight sync, not per forward).
-    """
-    import torch
-    from oracle import layer as OL, quant as OQ, rac as OR, route as ORt
-    from oracle.formats import bf16_round_f64
+        def one(e, b=b, src=src):
+            q = OQ.quantize(src[e].float().numpy())
+            b["codes"][e], b["scales"][e] = q["codes"], q["scales"]
+            b["gscale"][e] = (q["s_enc"], q["s_dec"])
+
+        with cf.ThreadPoolExecutor(min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(one, [int(e) for e in experts]))
+        banks.append(b)
+    return banks
+
+
+def cpu_baseline(name, n_tok):
+    """The oracle's free-running forward of the whole layer (routing, Q_A of X
+    with RAC, W13 + SwiGLU, Q_A(h), W2, combine; float64 contractions), timed
+    on the host cores on the first n_tok tokens of the workload's batch.  The
+    oracle quantises the touched experts' weights itself first (not timed:
+    weights are quantised once per weight sync, not per forward)."""
+    from oracle import layer as OL, route as ORt
+    from paper_2607_15810_amd import synth
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
-    wl = inp.wl
-    x = inp.x.float().numpy()
-    lg = inp.logits.numpy()
-    ids = ORt.topk_fast(lg, wl.k)
-    perm = ORt.permute(ids, wl.E)
-    counts = perm["counts"]
-    order = np.sort(np.argsort(-counts, kind="stable")[:n_sample_experts])
-    E = wl.E
-    # the sampled experts' weights, quantised by the oracle (not timed: the
-    # weights are quantised once per weight sync, not per forward)
-    W13 = dict(codes=np.zeros((E, 2 * wl.I, wl.H), np.uint8),
-               scales=np.zeros((E, 2 * wl.I, wl.H // 16), np.uint8), gscale=np.ones((E, 2), np.float32))
-    W2 = dict(codes=np.zeros((E, wl.H, wl.I), np.uint8),
-              scales=np.zeros((E, wl.H, wl.I // 16), np.uint8), gscale=np.ones((E, 2), np.float32))
-    for e in order:
-        for bank, src in ((W13, inp.w13), (W2, inp.w2)):
-            q = OQ.quantize(src[int(e)].float().numpy())
-            bank["codes"][e], bank["scales"][e] = q["codes"], q["scales"]
-            bank["gscale"][e] = (q["s_enc"], q["s_dec"])
-    rows = np.concatenate([np.arange(perm["offsets"][e], perm["offsets"][e + 1]) for e in order])
-    sub_off = np.zeros(E + 1, np.int64)
-    for e in order:
-        sub_off[e + 1] = counts[e]
-    sub_off = np.cumsum(sub_off)
-    # repeat the timed forward until about 10 s of CPU work has been measured
-    t_act = t_exp = t_comb = 0.0
-    reps = 0
-    while reps == 0 or (t_act + t_exp + t_comb < 10.0 and reps < 200):
+    wl = synth.WORKLOADS[name]
+    lg_all = synth.generate(name, with_weights=False)
+    x = lg_all.x[:n_tok].float().numpy()
+    lg = lg_all.logits[:n_tok].numpy()
+    touched = np.unique(ORt.topk_fast(lg, wl.k))
+    inp = synth.generate(name, experts=touched)
+    t_q = time.perf_counter()
+    W13, W2 = _oracle_banks(inp, touched)
+    t_q = time.perf_counter() - t_q
+    reps, t_sum = 0, 0.0
+    while reps == 0 or (t_sum < 10.0 and reps < 100):
         t0 = time.perf_counter()
-        ids = ORt.topk_fast(lg, wl.k)
-        wts = ORt.weights(lg, ids, True)
-        perm = ORt.permute(ids, wl.E)
-        act = OR.rac_activation(x, wl.Ks)
-        t1 = time.perf_counter()
-        gu, _ = OL.w13_stage(act["xq"], act["rq"], perm["row_token"], perm["offsets"], W13,
-                             rows=rows)
-        h = OL.swiglu(gu, wl.I)
-        hq = OQ.quantize(h.astype(np.float32))
-        z, _ = OL.w2_stage(hq, sub_off, W2)
-        bf16_round_f64(z)
-        t2 = time.perf_counter()
-        OL.combine(np.zeros((wl.T * wl.k, wl.H)), perm["inv_row"], wts)
-        t3 = time.perf_counter()
-        t_act += t1 - t0
-        t_exp += t2 - t1
-        t_comb += t3 - t2
+        OL.moe_layer(x, lg, W13, W2, wl.k, wl.Ks)
+        t_sum += time.perf_counter() - t0
         reps += 1
-    t_act, t_exp, t_comb = t_act / reps, t_exp / reps, t_comb / reps
-    touched = int(np.count_nonzero(counts))
-    est = t_act + t_exp * touched / max(1, len(order)) + t_comb
-    return dict(value=wl.T / est, unit="tokens/s", cores=int(threads), kind="oracle",
-                sample=(f"{reps} repetitions of: routing + RAC activation path on all {wl.T} tokens "
-                        f"({t_act:.3f} s); expert GEMMs for the {len(rows)} rows of the {len(order)} "
-                        f"most loaded of {touched} touched experts ({t_exp:.3f} s, scaled "
-                        f"x{touched / len(order):.1f}); combine ({t_comb:.3f} s); float64 numpy oracle"),
-                seconds_measured=round(reps * (t_act + t_exp + t_comb), 3))
+    per = t_sum / reps
+    return dict(value=round(n_tok / per, 2), unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=(f"{reps} free-running forwards of the whole layer (float64 numpy oracle) "
+                        f"on the first {n_tok} tokens of the {name} batch ({n_tok * wl.k} expert "
+                        f"rows over {touched.size} experts), {per:.3f} s each; the oracle's own "
+                        f"weight quantisation of those experts ({t_q:.1f} s) is not timed"),
+                seconds_measured=round(t_sum, 3))
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported: the layer is "
-              "built and measured on a single MI355X (no collectives, no sharding)",
-              file=sys.stderr)
-        sys.exit(2)
-    if args.copy_bytes:
-        copy_only(args.copy_bytes)
-        return
+def measure_ceilings():
+    """Achievable peaks on this GPU: a 4 GiB streaming read and a register-only
+    f16 MFMA loop (the library's probes), each the best of 3 launches."""
+    import torch
+    from paper_2607_15810_amd import quads as Q
+    L = Q.lib()
+    s = torch.cuda.current_stream().cuda_stream
+    nbytes = 4 << 30
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    out = torch.empty(L.qd_probe_hbm_read_out_count(), dtype=torch.int32, device="cuda")
+    best = None
+    for _ in range(4):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        Q.call("qd_probe_hbm_read", buf.data_ptr(), nbytes, out.data_ptr(), s)
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b)
+        best = ms if best is None else min(best, ms)
+    hbm = nbytes / (best * 1e-3) / 1e9
+    del buf
+    wg, rounds = 2048, 2000
+    outm = torch.empty(wg, dtype=torch.float32, device="cuda")
+    best = None
+    for _ in range(4):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        Q.call("qd_probe_mfma_f16", rounds, wg, outm.data_ptr(), s)
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b)
+        best = ms if best is None else min(best, ms)
+    mfma = L.qd_probe_mfma_f16_flops(rounds, wg) / (best * 1e-3) / 1e12
+    torch.cuda.empty_cache()
+    return {"hbm_read_GBps": round(hbm, 1), "mfma_f16_TFLOPs": round(mfma, 1),
+            "how": "streaming 16-byte reads of 4 GiB; 16 independent v_mfma_f32_32x32x16_f16 "
+                   "chains per wave, 8 waves per CU; best of 4 launches"}
+
+
+def clone_bank(b):
+    from paper_2607_15810_amd import ops
+    return ops.NVFP4Tensor(b.codes.clone(), b.scales.clone(), b.gscale.clone(), b.groups,
+                           b.rows, b.cols,
+                           b.scales_frag.clone() if b.scales_frag is not None else None)
+
+
+def measure(args, name, ceil, headline):
+    """Time one workload: the step (median and mean over args.steps), the
+    stages, and the W13 roofline.  With headline=True also the HIP-graph
+    replay, the comparison rows and the K_s sweep."""
     import torch
     from paper_2607_15810_amd import ops, synth
     from paper_2607_15810_amd import quads as Q
-
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        sys.exit(1)
-    Q.lib()
-    wl = synth.WORKLOADS[args.workload]
-    if wl.dense:
-        print("the dense GEMM workload is a parity case, not a bench line", file=sys.stderr)
-        sys.exit(2)
+    wl = synth.WORKLOADS[name]
     t_gen = time.perf_counter()
-    inp = synth.generate(args.workload)
+    inp = synth.generate(name)
     t_gen = time.perf_counter() - t_gen
-    print(f"[bench] generated {args.workload} in {t_gen:.1f} s", file=sys.stderr, flush=True)
+    print(f"[bench] generated {name} in {t_gen:.1f} s", file=sys.stderr, flush=True)
     dev = "cuda"
     x0 = inp.x.to(dev)
     lg0 = inp.logits.to(dev)
     w13_0 = ops.quantize_weight(inp.w13.to(dev))
     w2_0 = ops.quantize_weight(inp.w2.to(dev))
     torch.cuda.synchronize()
-
-    def clone_bank(b):
-        return ops.NVFP4Tensor(b.codes.clone(), b.scales.clone(), b.gscale.clone(), b.groups,
-                               b.rows, b.cols,
-                               b.scales_frag.clone() if b.scales_frag is not None else None)
-
     copies = max(1, args.copies)
     banks = [(w13_0, w2_0)] + [(clone_bank(w13_0), clone_bank(w2_0)) for _ in range(copies - 1)]
     xs = [x0] + [x0.clone() for _ in range(copies - 1)]
@@ -252,28 +275,28 @@ def main():
     torch.cuda.synchronize()
     counts = np.diff(layers[0].views()["offsets"].cpu().numpy())
 
-    # timed region 1: the layer alone -> ms_per_step
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
+    # timed region 1: the layer alone, an event between consecutive steps
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    start.record()
+    evs[0].record()
     for i in range(args.steps):
         c = i % copies
         layers[c](xs[c], lgs[c], y)
-    end.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_total = start.elapsed_time(end)
-    ms_step = ms_total / args.steps
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    ms_mean = evs[0].elapsed_time(evs[-1]) / args.steps
+    ms_step = float(np.median(per_step))
 
     # timed region 2: the same steps with HIP events recorded by the library
     # at the stage boundaries on the layer's stream -> per-stage times and
     # the W13 kernel's duration for the roofline
     n_ev = len(Q.STAGE_NAMES) + 1
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(args.steps)]
-    for evs in events:          # create the underlying HIP events
-        for e in evs:
+    for ee in events:          # create the underlying HIP events
+        for e in ee:
             e.record()
     torch.cuda.synchronize()
     start2 = torch.cuda.Event(enable_timing=True)
@@ -286,9 +309,9 @@ def main():
     torch.cuda.synchronize()
     ms_step_ev = start2.elapsed_time(end2) / args.steps
     stage_ms = np.zeros(n_ev - 1)
-    for evs in events:
+    for ee in events:
         for s in range(n_ev - 1):
-            stage_ms[s] += evs[s].elapsed_time(evs[s + 1])
+            stage_ms[s] += ee[s].elapsed_time(ee[s + 1])
     stage_ms /= args.steps
 
     alg = algorithmic(wl, counts)
@@ -296,43 +319,39 @@ def main():
     step_gbs = alg["step_bytes"] / (ms_step * 1e-3) / 1e9
     step_tflops = alg["step_flops"] / (ms_step * 1e-3) / 1e12
     w13_ms = stage_ms[Q.STAGE_NAMES.index("w13")]
-    decode = args.workload in DECODE
+    decode = name in DECODE
     # the W13 launch runs the decode kernel when the rows per expert are few
     skinny = Q.lib().moe_w4a4_grouped_gemm_amax_count(
         wl.T * wl.k, 2 * wl.I, wl.H, wl.E, wl.Ks, Q.QD_EPI_SWIGLU) <= 1024
     kname = ("gemm_skinny_kernel" if skinny else "gemm_tile_kernel") + \
         " (W13 + fused RAC residual + SwiGLU)"
-    traffic = measured_traffic(args.workload)
+    traffic = measured_traffic(name)
     if decode:
         achieved = alg["w13_bytes"] / (w13_ms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=round(achieved, 1), peak=PEAK_HBM_GBS, unit="GB/s",
                     frac=round(achieved / PEAK_HBM_GBS, 4), traffic=traffic,
-                    kernel=kname,
-                    algorithmic_bytes=int(alg["w13_bytes"]), avg_ms=round(w13_ms, 5))
+                    kernel=kname, algorithmic_bytes=int(alg["w13_bytes"]),
+                    avg_ms=round(w13_ms, 5))
+        if ceil:
+            roof["measured_peak"] = ceil["hbm_read_GBps"]
+            roof["frac_of_measured"] = round(achieved / ceil["hbm_read_GBps"], 4)
     else:
         achieved = alg["w13_flops"] / (w13_ms * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(achieved, 1), peak=PEAK_F16_TFLOPS,
                     unit="TFLOP/s", frac=round(achieved / PEAK_F16_TFLOPS, 4), traffic=traffic,
-                    kernel=kname,
-                    algorithmic_flops=alg["w13_flops"], avg_ms=round(w13_ms, 5),
+                    kernel=kname, algorithmic_flops=alg["w13_flops"], avg_ms=round(w13_ms, 5),
                     frac_of_fp8_peak=round(achieved / PEAK_FP8_TFLOPS, 4),
                     frac_of_fp4_peak=round(achieved / PEAK_FP4_TFLOPS, 4))
-    out = {
-        "metric": METRIC,
-        "value": round(tok_s, 1),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "nvfp4 (e2m1 x e4m3 decoded exactly to f16 MFMA operands, f32 accumulate)",
-        "data": "synthetic",
-        "config": {"workload": args.workload, "tokens": wl.T, "hidden": wl.H, "experts": wl.E,
-                   "top_k": wl.k, "intermediate": wl.I, "rac_channels": wl.Ks,
-                   "touched_experts": alg["touched"], "weight_copies": copies},
+        if ceil:
+            roof["measured_peak"] = ceil["mfma_f16_TFLOPs"]
+            roof["frac_of_measured"] = round(achieved / ceil["mfma_f16_TFLOPs"], 4)
+    res = {
+        "workload": name, "tokens": wl.T, "hidden": wl.H, "experts": wl.E, "top_k": wl.k,
+        "intermediate": wl.I, "rac_channels": wl.Ks, "touched_experts": alg["touched"],
+        "weight_copies": copies,
+        "ms_per_step": round(ms_step, 5), "ms_per_step_mean": round(ms_mean, 5),
+        "ms_per_step_min": round(float(per_step.min()), 5),
+        "tokens_per_s": round(tok_s, 1),
         "effective": {"GB/s": round(step_gbs, 1), "frac_hbm": round(step_gbs / PEAK_HBM_GBS, 4),
                       "TFLOP/s": round(step_tflops, 2),
                       "frac_f16_mfma": round(step_tflops / PEAK_F16_TFLOPS, 4),
@@ -343,26 +362,92 @@ def main():
         "wall_ms_per_step": round(wall * 1e3 / args.steps, 5),
         "roofline": roof,
     }
-    print(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step", file=sys.stderr, flush=True)
-    # the same steps replayed from HIP graphs (one captured layer call per
-    # weight copy): what a serving loop that captures its decode step sees
-    graphs = []
-    for c in range(copies):
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            layers[c](xs[c], lgs[c], y)
-        graphs.append(g)
-    ms_graph = time_steps([g.replay for g in graphs], args.steps, args.warmup)
-    out["hip_graph"] = dict(ms_per_step=round(ms_graph, 5),
-                            value=round(wl.T / (ms_graph * 1e-3), 1), unit="tokens/s")
-    del graphs
-    if not args.no_comparisons:
-        out["comparisons"] = comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws)
-    if args.ks_sweep:
-        out["ks_sweep"] = ks_sweep(args, wl, banks, xs, lgs, ws)
+    print(f"[bench] {name}: {ms_step:.4f} ms/step (median), {ms_mean:.4f} mean",
+          file=sys.stderr, flush=True)
+    if headline:
+        # the same steps replayed from HIP graphs (one captured layer call per
+        # weight copy): what a serving loop that captures its step sees
+        graphs = []
+        for c in range(copies):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                layers[c](xs[c], lgs[c], y)
+            graphs.append(g)
+        ms_graph = time_steps([g.replay for g in graphs], args.steps, args.warmup)
+        res["hip_graph"] = dict(ms_per_step=round(ms_graph, 5),
+                                value=round(wl.T / (ms_graph * 1e-3), 1), unit="tokens/s")
+        del graphs
+        if not args.no_comparisons:
+            res["comparisons"] = comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws)
+        if args.ks_sweep:
+            res["ks_sweep"] = ks_sweep(args, wl, banks, xs, lgs, ws)
+    del layers, banks, xs, lgs, ws, y, inp
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU; --gpus {args.gpus} is not supported: the layer is "
+              "built and measured on a single MI355X (no collectives, no sharding)",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.copy_bytes:
+        copy_only(args.copy_bytes)
+        return
+    import torch
+    from paper_2607_15810_amd import synth
+    from paper_2607_15810_amd import quads as Q
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    Q.lib()
+    wl = synth.WORKLOADS[args.workload]
+    if wl.dense:
+        print("the dense GEMM workload is a parity case, not a bench line", file=sys.stderr)
+        sys.exit(2)
+    ceil = measure_ceilings()
+    print(f"[bench] ceilings {ceil}", file=sys.stderr, flush=True)
+    head = measure(args, args.workload, ceil, headline=True)
+    out = {
+        "metric": METRIC,
+        "value": head["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "ms_per_step_mean": head["ms_per_step_mean"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "nvfp4 (e2m1 x e4m3 decoded exactly to f16 MFMA operands, f32 accumulate)",
+        "data": "synthetic",
+        "config": {k: head[k] for k in ("workload", "tokens", "hidden", "experts", "top_k",
+                                        "intermediate", "rac_channels", "touched_experts",
+                                        "weight_copies")},
+        "roofline": head["roofline"],
+        "measured_ceilings": ceil,
+    }
+    for k in ("effective", "stage_ms", "ms_per_step_with_stage_events", "wall_ms_per_step",
+              "ms_per_step_min", "hip_graph", "comparisons", "ks_sweep"):
+        if k in head:
+            out[k] = head[k]
+    if not args.no_per_config:
+        pc = {}
+        for name in PER_CONFIG:
+            if name == args.workload:
+                continue
+            r = measure(args, name, ceil, headline=False)
+            pc[name] = {k: r[k] for k in ("ms_per_step", "ms_per_step_mean", "tokens_per_s",
+                                          "touched_experts", "stage_ms", "roofline",
+                                          "effective")}
+        out["per_config"] = pc
     if not args.no_cpu_baseline:
-        ne = args.cpu_experts or (4 if wl.H <= 2048 else 2)
-        out["cpu_baseline"] = cpu_baseline(inp, ne)
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_tokens)
     print(json.dumps(out))
 
 

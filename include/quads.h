@@ -256,7 +256,10 @@ int64_t   nvfp4_frag_scales_bytes(int64_t groups, int64_t rows, int64_t cols);
 qd_status nvfp4_pack_frag_scales(const qd_nvfp4 *w, uint8_t *out, void *stream);
 
 /* ---------------------------------------------------------------------
- * moe_unpermute_combine -- weighted sum of the k expert outputs per token:
+ * moe_unpermute_combine -- the last step of the MoE layer whose expert
+ * GEMMs Sec. 3.3 quantises (the MoE model of Sec. 4.1; the paper gives no
+ * router or combine details, so this is the standard top-k combine): the
+ * weighted sum of the k expert outputs per token,
  *   y[t][n] = bf16( sum_{s=0..k-1} topk_w[t][s] * z[inv_row[t][s]][n] ),
  * accumulated in f32 in slot order.
  *   z : bf16 [T*k][H]; y : bf16 [T][H]; 1 <= k <= 32, H % 8 == 0.
@@ -442,6 +445,24 @@ enum {
 };
 qd_status qd_moe_layer_views(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I,
                              int64_t *off /* host, QD_VIEW_COUNT */);
+
+/* ---------------------------------------------------------------------
+ * Achievable-peak probes (measurement only, not part of the layer): the
+ * rates the chip reaches in practice, stated beside its published peaks.
+ * qd_probe_hbm_read -- streams `bytes` (a multiple of 16) of device memory
+ *   `buf` once with 16-byte loads; out: uint32 [qd_probe_hbm_read_out_count()]
+ *   scratch results.  Time it with events on `stream`: bytes / time is the
+ *   achievable read bandwidth (use a buffer far larger than the 256 MB
+ *   Infinity Cache).
+ * qd_probe_mfma_f16 -- `workgroups` workgroups of four waves, each wave
+ *   running `rounds` rounds of 16 independent v_mfma_f32_32x32x16_f16 on
+ *   registers; qd_probe_mfma_f16_flops(rounds, workgroups) is the work in
+ *   FLOP; out: float [workgroups].
+ * ------------------------------------------------------------------- */
+int64_t   qd_probe_hbm_read_out_count(void);
+qd_status qd_probe_hbm_read(const void *buf, int64_t bytes, uint32_t *out, void *stream);
+double    qd_probe_mfma_f16_flops(int64_t rounds, int32_t workgroups);
+qd_status qd_probe_mfma_f16(int64_t rounds, int32_t workgroups, float *out, void *stream);
 
 #if defined(__GNUC__) || defined(__clang__)
 #pragma GCC visibility pop

@@ -104,7 +104,8 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs p) {
   int64_t rb, re;
   const bool have = locate_tile(p, blockIdx.x, e, rb, re);
   if (RAC) {
-    for (int i = threadIdx.x; i < (K + 31) / 32; i += blockDim.x) selmap[i] = 0u;
+    // every word the chunk loop reads (four per 128-channel chunk)
+    for (int i = threadIdx.x; i < (K + 127) / 128 * 4; i += blockDim.x) selmap[i] = 0u;
     __syncthreads();
     for (int i = threadIdx.x; i < p.Ks; i += blockDim.x) {
       const int j = p.sel[i];
@@ -161,21 +162,34 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs p) {
       }
     if (wave_active) {
       const int nchunk = (K + 127) / 128;
+      // a lane group's 32 elements of a chunk: all inside K (gval), only the
+      // first 16 (ghalf: K % 32 == 16, the last chunk), or none
+      auto ld_codes = [](const uint8_t *q, bool full, bool half) -> uint4 {
+        if (full) return *reinterpret_cast<const uint4 *>(q);
+        if (half) {
+          const uint2 v = *reinterpret_cast<const uint2 *>(q);
+          return make_uint4(v.x, v.y, 0u, 0u);
+        }
+        return make_uint4(0u, 0u, 0u, 0u);
+      };
+      auto ld_scales = [](const uint8_t *q, bool full, bool half) -> uint32_t {
+        if (full) return *reinterpret_cast<const uint16_t *>(q);
+        return half ? (uint32_t)q[0] : 0u;
+      };
       for (int c = 0; c < nchunk; ++c) {
         const bool gval = (c * 128 + g * 32 + 32) <= K;
+        const bool ghalf = !gval && (c * 128 + g * 32 + 16) <= K;
         uint4 a4[2], b4[2], r4[2];
         uint32_t asc[2], bsc[2], rsc[2];
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
-          const bool ok = av[i] && gval;
-          a4[i] = ok ? *reinterpret_cast<const uint4 *>(ac[i] + c * 64) : make_uint4(0, 0, 0, 0);
-          asc[i] = ok ? *reinterpret_cast<const uint16_t *>(as[i] + c * 8) : 0u;
+          a4[i] = ld_codes(ac[i] + c * 64, av[i] && gval, av[i] && ghalf);
+          asc[i] = ld_scales(as[i] + c * 8, av[i] && gval, av[i] && ghalf);
         }
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          const bool ok = bv[j] && gval;
-          b4[j] = ok ? *reinterpret_cast<const uint4 *>(bc[j] + c * 64) : make_uint4(0, 0, 0, 0);
-          bsc[j] = ok ? *reinterpret_cast<const uint16_t *>(bs[j] + c * 8) : 0u;
+          b4[j] = ld_codes(bc[j] + c * 64, bv[j] && gval, bv[j] && ghalf);
+          bsc[j] = ld_scales(bs[j] + c * 8, bv[j] && gval, bv[j] && ghalf);
         }
         uint32_t smask = 0u;   // k-steps of this chunk holding a selected channel
         if (RAC) {
@@ -188,9 +202,8 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs p) {
           if (smask) {
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
-              const bool ok = av[i] && gval;
-              r4[i] = ok ? *reinterpret_cast<const uint4 *>(rc[i] + c * 64) : make_uint4(0, 0, 0, 0);
-              rsc[i] = ok ? *reinterpret_cast<const uint16_t *>(rs[i] + c * 8) : 0u;
+              r4[i] = ld_codes(rc[i] + c * 64, av[i] && gval, av[i] && ghalf);
+              rsc[i] = ld_scales(rs[i] + c * 8, av[i] && gval, av[i] && ghalf);
             }
           }
         }
@@ -1417,7 +1430,7 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
   st = qdh::check_nvfp4(w, E, w->rows, K);
   if (st) return st;
   const int64_t N = w->rows;
-  if (K % 32 != 0 || N % 16 != 0 || N <= 0) return QD_ERR_SHAPE;
+  if (K % 16 != 0 || N % 16 != 0 || N <= 0) return QD_ERR_SHAPE;
   if (epilogue == QD_EPI_SWIGLU && (N % 32 != 0)) return QD_ERR_SHAPE;
   if (!expert_offsets && E != 1) return QD_ERR_SHAPE;
   if (!row_token && rows > a->rows) return QD_ERR_SHAPE;

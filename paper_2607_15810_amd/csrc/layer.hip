@@ -214,7 +214,7 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
                                                 void *ws, size_t ws_bytes,
                                                 void *const *events, void *stream) {
   if (!w13 || !w2) return QD_ERR_NULL;
-  if (T < 0 || H <= 0 || H % 32 || I <= 0 || I % 32 || E < 1 || k < 1 || k > E) return QD_ERR_SHAPE;
+  if (T < 0 || H <= 0 || H % 16 || I <= 0 || I % 16 || E < 1 || k < 1 || k > E) return QD_ERR_SHAPE;
   if (Ks < 0 || Ks > H || Ks2 < 0 || Ks2 > I) return QD_ERR_SHAPE;
   // routing limits (as moe_route_permute) and the fused channel selection
   if (E > qdr::kMaxE || k > qdr::kMaxK || T * (int64_t)k > 0x7fffffffLL) return QD_ERR_SHAPE;

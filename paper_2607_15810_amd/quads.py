@@ -103,6 +103,10 @@ SIGNATURES = {
                                            c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]),
     "qd_moe_layer_views": (c_int, [c_int64, c_int64, c_int32, c_int32, c_int64,
                                    POINTER(c_int64)]),
+    "qd_probe_hbm_read_out_count": (c_int64, []),
+    "qd_probe_hbm_read": (c_int, [c_void_p, c_int64, c_void_p, c_void_p]),
+    "qd_probe_mfma_f16_flops": (ctypes.c_double, [c_int64, c_int32]),
+    "qd_probe_mfma_f16": (c_int, [c_int64, c_int32, c_void_p, c_void_p]),
 }
 
 _lib = None

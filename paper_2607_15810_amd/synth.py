@@ -153,12 +153,26 @@ def expert_weights(seed_seq, e, N, K, std):
     return np.random.default_rng(ss).standard_normal((N, K), dtype=np.float32) * np.float32(std)
 
 
-def make_bank(seed_seq, E, N, K, std, experts=None):
+def make_bank(seed_seq, E, N, K, std, experts=None, threads=None):
     """[E][N][K] bfloat16 weights.  experts: the experts to draw (default all);
-    the others are zero (full-size tests that check a sample of experts)."""
+    the others are zero (full-size tests that check a sample of experts).
+    Each expert has its own stream, so drawing them on a pool of threads
+    gives the same bank as drawing them in order."""
+    import concurrent.futures as cf
+    import os
     out = torch.zeros((E, N, K), dtype=torch.bfloat16)
-    for e in (range(E) if experts is None else experts):
-        out[e] = to_bf16(expert_weights(seed_seq, int(e), N, K, std))
+    todo = list(range(E)) if experts is None else [int(e) for e in experts]
+
+    def one(e):
+        out[e] = to_bf16(expert_weights(seed_seq, e, N, K, std))
+
+    n = threads or min(16, os.cpu_count() or 1)
+    if n <= 1 or len(todo) <= 1:
+        for e in todo:
+            one(e)
+    else:
+        with cf.ThreadPoolExecutor(n) as ex:
+            list(ex.map(one, todo))
     return out
 
 

@@ -86,20 +86,34 @@ def upload_nvfp4(q, device="cuda"):
     return t
 
 
-def oracle_bank(w_bf16, experts=None):
+def oracle_bank(w_bf16, experts=None, threads=None):
     """Oracle quantisation of a bf16 bank [E][N][K]; with `experts` only those
-    experts are quantised (the others stay zero and must not be used)."""
-    w = w_bf16.float().numpy()
-    E, N, K = w.shape
-    if experts is None:
-        return quant.quantize_weight_bank(w)
+    experts are quantised (the others stay zero and must not be used).
+
+    Experts are independent, so large banks are quantised by the oracle's own
+    per-matrix quantize() on a pool of threads (numpy releases the GIL inside
+    its array operations); the result is the same as one expert after the
+    other."""
+    import concurrent.futures as cf
+    import os
+    E, N, K = w_bf16.shape
+    todo = list(range(E)) if experts is None else [int(e) for e in experts]
     codes = np.zeros((E, N, K), np.uint8)
     scales = np.zeros((E, N, K // 16), np.uint8)
     gscale = np.ones((E, 2), np.float32)
-    for e in experts:
-        q = quant.quantize(w[e])
+
+    def one(e):
+        q = quant.quantize(w_bf16[e].float().numpy())
         codes[e], scales[e] = q["codes"], q["scales"]
         gscale[e] = (q["s_enc"], q["s_dec"])
+
+    n = threads or min(16, os.cpu_count() or 1)
+    if n <= 1 or len(todo) <= 1:
+        for e in todo:
+            one(e)
+    else:
+        with cf.ThreadPoolExecutor(n) as ex:
+            list(ex.map(one, todo))
     return dict(codes=codes, scales=scales, gscale=gscale)
 
 

@@ -67,6 +67,13 @@ SMALL = [
     # many rows per expert: the tiled (prefill) kernel instead of the skinny one
     ("many_rows", 256, 256, 4, 2, 64, 8, {}),
     ("many_rows_ktail", 300, 384, 4, 2, 96, 12, {}),
+    # a single token (single-sequence decode), and the narrowest width the
+    # format allows (one 16-element block per row: H = I = 16)
+    ("t1", 1, 256, 8, 2, 128, 8, {}),
+    ("t1_k8_ks0", 1, 512, 16, 8, 64, 0, {}),
+    ("h16_i16", 40, 16, 4, 2, 16, 4, {}),
+    ("h16_t1", 1, 16, 4, 2, 16, 16, {}),
+    ("h16_i48_zipf", 64, 16, 8, 4, 48, 3, dict(routing="zipf", acts="student_t3")),
 ]
 
 
@@ -426,8 +433,17 @@ def test_empty_batch():
     assert y.shape == (0, 128)
 
 
-FULL = ["moe_decode_t256_h2048", "moe_prefill_t8192_h2048", "moe_zipf_decode_t64_h4096",
-        "moe_prefill_t4096_h4096"]
+FULL = [
+    # workload, token count (None: the workload's), experts with real weights
+    # ("all": every expert that receives a row; "sampled": three of them)
+    ("moe_decode_t256_h2048", None, "all"),
+    ("moe_zipf_decode_t64_h4096", None, "all"),
+    ("moe_prefill_t8192_h2048", None, "sampled"),
+    ("moe_prefill_t4096_h4096", None, "sampled"),
+    # a single token (single-sequence decode) at the decode workloads' sizes
+    ("moe_decode_t256_h2048", 1, "all"),
+    ("moe_zipf_decode_t64_h4096", 1, "all"),
+]
 
 
 def _sampled_experts(counts):
@@ -437,28 +453,36 @@ def _sampled_experts(counts):
     return sorted({int(order[-1]), int(order[0]), int(order[len(order) // 2])})
 
 
-@pytest.mark.parametrize("name", FULL)
-def test_full_size_sampled(name):
-    """A MoE workload at its full size through the whole-layer call the
-    benchmark times (same shapes, hence the same kernels and grids).
+@pytest.mark.parametrize("name,T,which", FULL,
+                         ids=[f"{n}-T{T or 'full'}-{w}" for n, T, w in FULL])
+def test_full_size(name, T, which):
+    """A MoE workload at its full size (or a single token at its sizes)
+    through the whole-layer call the benchmark times (same shapes, hence the
+    same kernels and grids).
 
-    Three experts carry their real weights; the rest are zero.  The kernels do
-    the same work either way, and the zero experts make every output
-    computable by the oracle: their rows of h and z and their shares of y are
-    exactly zero, so h's tensor amax comes from the sampled rows alone.
-    Routing, the activation quantisation and the channel selection are
-    compared in full, bit for bit."""
+    "all": every expert that receives a row carries its real weights, so
+    every work unit of every kernel is compared with the oracle.  "sampled"
+    (the prefill workloads, whose full oracle takes minutes): three experts
+    carry their real weights and the rest are zero; the kernels do the same
+    work either way, and the zero experts make every output computable by the
+    oracle: their rows of h and z and their shares of y are exactly zero, so
+    h's tensor amax comes from the sampled rows alone.  Routing, the
+    activation quantisation and the channel selection are compared in full,
+    bit for bit, in both modes."""
     wl = synth.WORKLOADS[name]
-    lg = synth.generate(name, with_weights=False).logits.numpy()
+    lg = synth.generate(name, T=T, with_weights=False).logits.numpy()
     ref_ids = ORt.topk_fast(lg, wl.k)
     perm = ORt.permute(ref_ids, wl.E)
     offs_np = perm["offsets"]
-    S = _sampled_experts(np.diff(offs_np))
-    zero_e = next(e for e in range(wl.E) if e not in S)
-    inp = synth.generate(name, experts=S)
-    T, H, E, k, I, Ks = wl.T, wl.H, wl.E, wl.k, wl.I, wl.Ks
+    counts = np.diff(offs_np)
+    S = [int(e) for e in np.nonzero(counts)[0]] if which == "all" else _sampled_experts(counts)
+    zero_e = next((e for e in range(wl.E) if e not in S), None)
+    inp = synth.generate(name, T=T, experts=S)
+    T = inp.x.shape[0]
+    H, E, k, I, Ks = wl.H, wl.E, wl.k, wl.I, wl.Ks
     R = T * k
-    print(f"{name}: experts {S}, rows {[int(offs_np[e + 1] - offs_np[e]) for e in S]}", flush=True)
+    print(f"{name} T={T}: {len(S)} experts with weights, rows "
+          f"{sorted(int(counts[e]) for e in S)[-3:]} (largest)", flush=True)
 
     x = inp.x.to(DEV)
     logits = inp.logits.to(DEV)
@@ -469,10 +493,11 @@ def test_full_size_sampled(name):
     torch.cuda.synchronize()
     v = lay.views()
 
-    W13 = oracle_bank(inp.w13, S + [zero_e])
-    W2 = oracle_bank(inp.w2, S + [zero_e])
-    assert_bank_equal(w13, W13, S + [zero_e])
-    assert_bank_equal(w2, W2, S + [zero_e])
+    banked = S + ([zero_e] if zero_e is not None else [])
+    W13 = oracle_bank(inp.w13, banked)
+    W2 = oracle_bank(inp.w2, banked)
+    assert_bank_equal(w13, W13, banked)
+    assert_bank_equal(w2, W2, banked)
     # A1-A2
     assert np.array_equal(v["ids"].cpu().numpy(), ref_ids)
     assert np.array_equal(v["offsets"].cpu().numpy(), offs_np)
@@ -501,44 +526,48 @@ def test_full_size_sampled(name):
         assert np.array_equal(got[:, :Ks].astype(np.float64), ref_un[:, act["sel"]])
         assert not got[:, Ks:].any()
 
-    # A6 on the sampled rows; every other row of h is exactly zero
+    # A6 on the rows of the experts with weights; every other row of h is
+    # exactly zero
     rows = np.concatenate([np.arange(offs_np[e], offs_np[e + 1]) for e in S])
     other = np.ones(R, bool)
     other[rows] = False
+    rows_dev = torch.from_numpy(rows).to(DEV)
+    od = torch.from_numpy(other).to(DEV)
     gu, mag_gu = OL.w13_stage(act["xq"], act["rq"] if Ks else None, perm["row_token"], offs_np,
                               W13, rows=rows)
     h_or = OL.swiglu(gu, I)
     mag_h = (np.abs(OL.silu(gu[:, :I])) * mag_gu[:, I:] +
              1.1 * np.abs(gu[:, I:]) * mag_gu[:, :I])
     h_gpu = v["h"]
-    check_close_bf16(np_bf16(h_gpu[torch.from_numpy(rows).to(DEV)]), h_or, mag_h, "h (SwiGLU)")
-    assert h_gpu[torch.from_numpy(other).to(DEV)].abs().max().item() == 0.0
+    check_close_bf16(np_bf16(h_gpu[rows_dev]), h_or, mag_h, "h (SwiGLU)")
+    if other.any():
+        assert h_gpu[od].abs().max().item() == 0.0
 
-    # A7 on the oracle's h (zero outside the sampled rows), bit-exact; a
+    # A7 on the oracle's h (zero outside the rows with weights), bit-exact; a
     # zero row appended to the oracle's input gives the expected zero rows
     hq_or = OQ.quantize(np.vstack([h_or, np.zeros((1, I))]).astype(np.float32))
     h_full = torch.zeros((R, I), dtype=torch.bfloat16, device=DEV)
-    rows_dev = torch.from_numpy(rows).to(DEV)
     h_full[rows_dev] = bf16_tensor(h_or)
     hq, _, _ = ops.quantize_act(h_full)
     hq_c, hq_s = hq.codes[0], hq.scales[0]
     assert np.array_equal(hq_c[rows_dev].cpu().numpy(), hq_or["packed"][:-1])
     assert np.array_equal(hq_s[rows_dev].cpu().numpy(), hq_or["scales"][:-1])
-    od = torch.from_numpy(other).to(DEV)
-    assert bool((hq_c[od] == torch.from_numpy(hq_or["packed"][-1]).to(DEV)).all())
-    assert bool((hq_s[od] == torch.from_numpy(hq_or["scales"][-1]).to(DEV)).all())
+    if other.any():
+        assert bool((hq_c[od] == torch.from_numpy(hq_or["packed"][-1]).to(DEV)).all())
+        assert bool((hq_s[od] == torch.from_numpy(hq_or["scales"][-1]).to(DEV)).all())
     assert hq.gscale[0].cpu().numpy().view(np.uint32).tolist() == \
         np.array([hq_or["s_enc"], hq_or["s_dec"]], np.float32).view(np.uint32).tolist()
 
     # A8 on that hq: the oracle's rows, compacted (row_token maps a row to
-    # its place among the sampled rows)
+    # its place among the rows with weights)
     z, _ = ops.grouped_gemm(hq, w2, R, None, v["offsets"])
     hh = OQ.dequantize_f64(hq_or["codes"][:-1], hq_or["scales"][:-1], hq_or["s_dec"])
     place = np.zeros(R, np.int64)
     place[rows] = np.arange(rows.size)
     z_or, mag_z = OL.grouped_gemm(hh, place, offs_np, W2, rows=rows)
     check_close_bf16(np_bf16(z[rows_dev]), z_or, mag_z, "z")
-    assert z[od].abs().max().item() == 0.0
+    if other.any():
+        assert z[od].abs().max().item() == 0.0
 
     # A9 on the oracle's z (zero row appended for the zero experts' rows)
     from oracle.formats import bf16_round_f64
