@@ -447,6 +447,32 @@ qd_status qd_moe_layer_views(int64_t T, int64_t H, int32_t E, int32_t k, int64_t
                              int64_t *off /* host, QD_VIEW_COUNT */);
 
 /* ---------------------------------------------------------------------
+ * qd_moe_layer_forward_noalloc -- qd_moe_layer_forward without a caller
+ * workspace, for callers that cannot allocate device memory: code under
+ * HIP graph capture, serving loops and harnesses that forbid hipMalloc.
+ * Same arguments (minus ws / ws_bytes), same kernels, same results bit for
+ * bit.  The intermediates live in a scratch buffer of
+ * QD_NOALLOC_SCRATCH_BYTES (64 MiB) that the library holds as a static
+ * device array: each device the library runs on keeps its own copy until
+ * the process ends.  The call allocates nothing (no hipMalloc / hipFree,
+ * no allocating library routine); its first call on a device looks up that
+ * device's copy (the device current at the call must be the stream's).
+ *   Errors: QD_ERR_WORKSPACE if qd_moe_layer_workspace(T, H, E, k, I) exceeds
+ *   qd_moe_layer_noalloc_max_bytes() (decode batches fit: 17.3 MiB for 256
+ *   tokens at H = 2048, E = 128, k = 8, I = 768); otherwise as
+ *   qd_moe_layer_forward.
+ * Every call on one device shares that device's scratch buffer and leaves
+ * the last call's intermediates in it: calls that overlap on one device
+ * (several streams or host threads) race; calls on one stream are ordered.
+ * ------------------------------------------------------------------- */
+#define QD_NOALLOC_SCRATCH_BYTES (64u << 20)
+size_t    qd_moe_layer_noalloc_max_bytes(void);
+qd_status qd_moe_layer_forward_noalloc(const void *x, const float *logits, int64_t T,
+                                       int64_t H, int32_t E, int32_t k, int64_t I, int32_t Ks,
+                                       int32_t Ks2, int32_t renorm, const qd_nvfp4 *w13,
+                                       const qd_nvfp4 *w2, void *y, void *stream);
+
+/* ---------------------------------------------------------------------
  * Achievable-peak probes (measurement only, not part of the layer): the
  * rates the chip reaches in practice, stated beside its published peaks.
  * qd_probe_hbm_read -- streams `bytes` (a multiple of 16) of device memory
