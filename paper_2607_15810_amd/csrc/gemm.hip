@@ -53,7 +53,19 @@ struct GemmArgs {
   int32_t *sel_out;
   uint16_t *out;
   float *amax_part;
+  int64_t amax_n;          // entries of amax_part (>= the grid; the rest are zeroed)
 };
+
+// one maximum of |out| per workgroup into amax_part; workgroups also zero
+// the entries past the grid, so every one of the amax_n entries is written
+__device__ __forceinline__ void put_amax(const GemmArgs &p, float m) {
+  if (p.amax_part && threadIdx.x == 0) {
+    const int64_t g = (int64_t)gridDim.x * gridDim.y;
+    const int64_t b = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+    p.amax_part[b] = m;
+    for (int64_t j = b + g; j < p.amax_n; j += g) p.amax_part[j] = 0.0f;
+  }
+}
 
 constexpr int BM = 64;
 constexpr int BN = 64;     // weight rows per workgroup (32 gate/up pairs for SwiGLU)
@@ -278,7 +290,7 @@ __global__ __launch_bounds__(256) void gemm_w4a4_kernel(GemmArgs p) {
     }
   }
   const float m = block_max(vmax, red);
-  if (p.amax_part && threadIdx.x == 0) p.amax_part[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = m;
+  put_amax(p, m);
 }
 
 // ---------------------------------------------------------------------------
@@ -1238,7 +1250,445 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
     }
   }
   const float m = block_max(vmax, red);
-  if (p.amax_part && tid == 0) p.amax_part[blockIdx.x] = m;
+  put_amax(p, m);
+}
+
+// ---------------------------------------------------------------------------
+// Prefill-shaped grouped GEMM with wide tiles (hundreds of rows per expert).
+//
+// What bounds the exact-NVFP4 prefill GEMM on gfx950 is VALU work per MFMA,
+// not bytes: every operand fragment is decoded in registers (8 VALU ops per
+// 32x16 fragment), so the decode cost per MFMA falls with the wave tile.
+//
+//  * Workgroup tile 256 rows x 256 weight rows (SwiGLU: 128 gate rows and
+//    the matching 128 up rows), four waves in a 2 x 2 grid, each 128 x 128
+//    on v_mfma_f32_32x32x16_f16 (4 x 4 fragments, 256 accumulators): one
+//    wave per SIMD, 8 fragment decodes per 16 MFMAs.  M-tiles never straddle
+//    experts; a tile of at most 128 rows splits them 64 / 64 between the
+//    wave rows, and fragments wholly past the expert's last row are skipped.
+//  * K in stages of 128 elements through a two-slot LDS ring filled by direct
+//    global->LDS loads: every load brings 16 rows x 64 contiguous bytes, the
+//    16-byte pieces of a row placed by a row-dependent XOR so the fragment
+//    reads are free of bank conflicts.  A wave reads a stage's raw codes and
+//    scales into registers one stage before it multiplies them: halfway
+//    through stage s it waits for stage s + 1, meets the other waves at the
+//    one barrier of the stage, issues the loads of stage s + 2 into the slot
+//    stage s occupied and reads stage s + 1 while the MFMAs of stage s drain.
+//  * Inside a stage lane (row r, half h) owns elements 64 h .. 64 h + 63;
+//    MFMA k-step s (0..7) takes elements 8 s .. 8 s + 7 of each half, for A
+//    and B alike (a common permutation of K).
+//  * Scales: the weights' from their fragment-ordered copy (128 contiguous
+//    bytes per 16 rows and stage), the activations' 16 bytes per row every
+//    second stage into a ring of their own; odd stages issue a one-line
+//    placeholder load instead, so every stage issues ten loads per wave.
+//  * Persistent: one workgroup per CU walks a static list of tiles; halfway
+//    through the last two stages of a tile it issues the first two stages
+//    of its next tile, so the next tile's loads overlap the epilogue.
+//  * Plain W4A4 only (no fused residual): with the RAC residual fused, the
+//    compact weight table and the residual operand do not fit beside the
+//    256 accumulators of this tile shape, and the 256 x 128 tile kernel
+//    below takes those problems.
+constexpr int TW_THREADS = 256;
+constexpr int TW_M = 256;
+constexpr int TW_N = 256;
+constexpr int TW_K = 128;
+constexpr int TW_ACODE = 0;               // [8 fragments][2 halves][64 lanes][16 B]
+constexpr int TW_BCODE = 16384;          // the same for the 256 weight rows
+constexpr int TW_BSCL = 32768;           // [16 row groups][128 B]
+constexpr int TW_STAGE = 34816;
+constexpr int TW_ASCL = 2 * TW_STAGE;    // A-scale ring [2 slots][256 rows][16 B]
+constexpr int TW_DUMMY = TW_ASCL + 8192; // target of the odd stages' placeholder load
+constexpr int TW_TOK = TW_DUMMY + 1024;  // gathered rows: tokens of the current and next tile [2][256]
+constexpr int TW_SCHED = TW_TOK + 2 * TW_M * 4;   // the tile schedule: two int arrays [E + 1]
+constexpr int TW_LOADS = 10;             // loads per wave and stage
+__host__ __device__ inline int tw_lds_bytes(int E) { return TW_SCHED + 2 * (E + 1) * 4; }
+
+// 16-byte piece p of tile row ri (0..15 within a 16-row load) sits at piece
+// p ^ tw_swz(ri) of the row's 64-byte LDS record
+__device__ __forceinline__ int tw_swz(int ri) { return ((ri >> 1) ^ (ri >> 2)) & 3; }
+
+// the tile's weight row tb (0..255): for SwiGLU wave column wn = tb / 128
+// holds gate rows (fragments 0, 1) and the matching up rows (2, 3)
+template <int EPI>
+__device__ __forceinline__ int wide_wrow(int tb, int nt, int N) {
+  if (EPI == QD_EPI_SWIGLU) {
+    const int wn = tb >> 7, f = (tb >> 5) & 3, r = tb & 31;
+    return (f < 2 ? 0 : (N >> 1)) + nt * 128 + wn * 64 + (f & 1) * 32 + r;
+  }
+  return nt * TW_N + tb;
+}
+
+// a wave's raw operands of one stage, A fragments fa0 .. fa0 + 3 and B
+// fragments fb0 .. fb0 + 3: the codes of k-steps 0..3 with the scale dwords
+// (read halfway through the previous stage) and the codes of k-steps 4..7
+// (read at the start of the stage), so that only half a stage of codes is
+// held twice
+struct TwLo {
+  uint4 a[4], b[4];
+  uint32_t as[4], bs[4];
+};
+struct TwHi {
+  uint4 a[4], b[4];
+};
+
+// LDS byte offset of lane (r, h)'s piece c (0, 1) of fragment f in a code area
+__device__ __forceinline__ int tw_frag_off(int f, int lane, int c) {
+  const int r = lane & 31, h = lane >> 5, ri = r & 15;
+  return ((2 * f + (r >> 4)) * 64 + 4 * ri + ((2 * h + c) ^ tw_swz(ri))) * 16;
+}
+
+template <int MTV>
+__device__ __forceinline__ void tw_read_lo(TwLo &R, const unsigned char *sl, const unsigned char *ascl,
+                                           int s, int fa0, int fb0, int lane) {
+  const int r = lane & 31, h = lane >> 5;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int fb = fb0 + j;
+    R.b[j] = *reinterpret_cast<const uint4 *>(sl + TW_BCODE + tw_frag_off(fb, lane, 0));
+    R.bs[j] = *reinterpret_cast<const uint32_t *>(sl + TW_BSCL + (2 * fb + (r >> 4)) * 128 +
+                                                  (16 * h + (r & 15)) * 4);
+  }
+#pragma unroll
+  for (int i = 0; i < MTV; ++i) {
+    const int fa = fa0 + i;
+    R.a[i] = *reinterpret_cast<const uint4 *>(sl + TW_ACODE + tw_frag_off(fa, lane, 0));
+    R.as[i] = *reinterpret_cast<const uint32_t *>(ascl + (32 * fa + r) * 16 + (s & 1) * 8 + 4 * h);
+  }
+}
+
+template <int MTV>
+__device__ __forceinline__ void tw_read_hi(TwHi &R, const unsigned char *sl, int fa0, int fb0,
+                                           int lane) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    R.b[j] = *reinterpret_cast<const uint4 *>(sl + TW_BCODE + tw_frag_off(fb0 + j, lane, 1));
+#pragma unroll
+  for (int i = 0; i < MTV; ++i)
+    R.a[i] = *reinterpret_cast<const uint4 *>(sl + TW_ACODE + tw_frag_off(fa0 + i, lane, 1));
+}
+
+// k-steps 4c .. 4c + 3 of a stage from codes ca / cb and the scale dwords
+template <int MTV>
+__device__ __forceinline__ void tw_half(const uint4 (&ca)[4], const uint4 (&cb)[4],
+                                        const uint32_t (&as)[4], const uint32_t (&bs)[4],
+                                        f32x16 (&acc)[4][4], int c) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const bool hi = (q >> 1) != 0;
+    f16x8 bf[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bf[j] = decode8_sel(word_of(cb[j], q), scale_pair_of(bs[j], c), hi);
+#pragma unroll
+    for (int i = 0; i < MTV; ++i) {
+      const f16x8 af = decode8_sel(word_of(ca[i], q), scale_pair_of(as[i], c), hi);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af, bf[j], acc[i][j]);
+    }
+  }
+}
+
+// Tiles of the persistent wide kernel: m-tile mt of the experts' TW_M-row
+// tiles (M-tiles never straddle experts), weight-row tile nt.
+struct TwTile {
+  int e, row0, nrows, nt;
+};
+
+// The tile schedule in LDS: offs [E + 1] row offsets, mpre [E + 1] the
+// m-tiles of the experts before e.  Tiles t = mt * ntn + nt; XCD x = b % 8
+// owns the contiguous range [x * per, x * per + per) and its workgroups
+// (b / 8) take every (G / 8)-th tile of it, so the tiles in flight on an XCD
+// share an expert's weights or a block of activation rows in its L2.
+// Tiles are visited in increasing order, so an expert cursor advances by a
+// wave ballot over the next 64 experts.
+__device__ __forceinline__ TwTile tw_locate(const int32_t *offs, const int32_t *mpre, int E,
+                                            int ntn, int t, int &ecur, int lane) {
+  const int mt = t / ntn;
+  for (;;) {
+    const int c = (int)uni((uint32_t)ecur) + 1 + lane;
+    const bool le = c <= E && mpre[c] <= mt;
+    const uint64_t bal = __ballot(le);
+    const int adv = __popcll(bal);
+    ecur += adv;
+    if (adv < 64) break;
+  }
+  TwTile tl;
+  tl.e = (int)uni((uint32_t)ecur);
+  tl.row0 = (int)uni((uint32_t)(offs[tl.e] + (mt - mpre[tl.e]) * TW_M));
+  tl.nrows = (int)uni((uint32_t)min(TW_M, offs[tl.e + 1] - tl.row0));
+  tl.nt = (int)uni((uint32_t)(t - mt * ntn));
+  return tl;
+}
+
+template <bool GATHER, int EPI>
+__global__ __launch_bounds__(TW_THREADS, 1) void gemm_wide_kernel(GemmArgs p, int ntn) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  __shared__ int sh_w[4];
+  __shared__ float red[16];
+  const int tid = threadIdx.x, lane = tid & 63, w = (int)uni((uint32_t)tid >> 6);
+  const int K = p.K, N = p.N, E = p.E;
+  const int64_t kb2 = K >> 1, kb16 = K >> 4;
+  const int nst = K / TW_K;
+  int32_t *offs = reinterpret_cast<int32_t *>(lds + TW_SCHED);
+  int32_t *mpre = offs + (E + 1);
+  int32_t *tokb = reinterpret_cast<int32_t *>(lds + TW_TOK);
+  const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
+  const uint32_t tok0 = lds0 + (uint32_t)TW_TOK;
+
+  // ---- the schedule: row offsets and m-tile prefix counts (four experts
+  // per thread, E <= 1024)
+  {
+    int cnt[4], tsum = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * tid + q;
+      int o0 = 0, o1 = 0;
+      if (e <= E) {
+        o0 = p.offsets ? p.offsets[e] : (e == 0 ? 0 : (int)p.rows);
+        offs[e] = o0;
+      }
+      if (e < E) o1 = p.offsets ? p.offsets[e + 1] : (int)p.rows;
+      cnt[q] = e < E ? (max(o1 - o0, 0) + TW_M - 1) / TW_M : 0;
+      tsum += cnt[q];
+    }
+    int xs = tsum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(xs, o, 64);
+      if (lane >= o) xs += y;
+    }
+    if (lane == 63) sh_w[w] = xs;
+    __syncthreads();
+    int base = xs - tsum;
+    for (int ww = 0; ww < w; ++ww) base += sh_w[ww];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * tid + q;
+      if (e <= E) mpre[e] = base;
+      base += cnt[q];
+    }
+  }
+  const float a_dec = p.a_gs[1];
+  __syncthreads();
+  const int T = (int)uni((uint32_t)mpre[E]) * ntn;
+  const int G = gridDim.x, nsl = G >> 3, xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int per = (T + 7) >> 3;
+  const int t_end = min(T, (xcd + 1) * per);
+  int t = xcd * per + slot;
+  int ecur = 0;
+  float vmax = 0.0f;
+
+  const int wm = w & 1, wn = w >> 1, fb0 = 4 * wn;
+  const int ri = lane >> 2;
+  const uint32_t pc = 16u * (uint32_t)((lane & 3) ^ tw_swz(ri));
+  // per-lane load offsets of a tile: wave w loads A and B fragments 2w,
+  // 2w + 1 (two 16-row halves each), lane l row l / 4 of the half, piece
+  // (l % 4) ^ swz; B rows of one load are consecutive weight rows (one
+  // per-lane offset, a uniform row per load); B scales (fragment-ordered):
+  // load w & 1 covers tile row groups 8 (w & 1) .. + 7, lane l group
+  // 8 (w & 1) + l / 8, piece l % 8 (waves 2, 3 repeat waves 0, 1: equal
+  // bytes to equal places); A scales: rows 64 w + l, 16 bytes every second
+  // stage
+  struct Offs {
+    uint32_t oa[4], obs, oag;
+  };
+  const uint32_t ob = (uint32_t)ri * (uint32_t)kb2 + pc;
+  const int bg = 8 * (w & 1) + (lane >> 3);
+  auto b_off = [&](const TwTile &tl) __attribute__((always_inline)) -> Offs {
+    Offs o;
+    o.obs = (uint32_t)((wide_wrow<EPI>(16 * bg, tl.nt, N) >> 4) * (K >> 8)) * 256u +
+            16u * (uint32_t)(lane & 7);
+    if (!GATHER) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = 32 * (2 * w + (j >> 1)) + 16 * (j & 1) + ri;
+        o.oa[j] = (uint32_t)(tl.row0 + (r < tl.nrows ? r : 0)) * (uint32_t)kb2 + pc;
+      }
+      const int r = 64 * w + lane;
+      o.oag = (uint32_t)(tl.row0 + (r < tl.nrows ? r : 0)) * (uint32_t)kb16;
+    }
+    return o;
+  };
+  // gathered rows: the tile's 256 row tokens go to LDS by direct loads
+  // (wave w: rows 64 w + l; rows past the tile repeat its first row), so
+  // neither the next tile's load offsets nor the residual rows wait on a
+  // load the compiler tracks
+  auto tok_dma = [&](const TwTile &tl, int buf) __attribute__((always_inline)) {
+    const int r = 64 * w + lane;
+    dma4s(uni_ptr(p.row_token), (uint32_t)(tl.row0 + (r < tl.nrows ? r : 0)) * 4u,
+          uni(tok0 + buf * (TW_M * 4) + w * 256));
+  };
+  // the per-lane A offsets from the tokens in LDS buffer buf
+  auto a_off_tok = [&](Offs &o, int buf) __attribute__((always_inline)) {
+    const int32_t *tb = tokb + buf * TW_M;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      o.oa[j] = (uint32_t)tb[32 * (2 * w + (j >> 1)) + 16 * (j & 1) + ri] * (uint32_t)kb2 + pc;
+    o.oag = (uint32_t)tb[64 * w + lane] * (uint32_t)kb16;
+  };
+  auto issue = [&](const TwTile &tl, const Offs &o, int s, int q, int apar)
+                   __attribute__((always_inline)) {
+    const uint32_t sb = uni(lds0 + q * TW_STAGE);
+    const uint8_t *ac = uni_ptr(p.a_codes + s * 64);
+    const uint8_t *bc = uni_ptr(p.w_codes + (int64_t)tl.e * N * kb2 + s * 64);
+    const uint8_t *wsf = uni_ptr(p.w_sfrag + (int64_t)tl.e * N * kb16);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) dma16s(ac, o.oa[j], sb + TW_ACODE + (4 * w + j) * 1024);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      dma16s(uni_ptr(bc + (int64_t)wide_wrow<EPI>(32 * (2 * w + (j >> 1)) + 16 * (j & 1), tl.nt, N) * kb2),
+             ob, sb + TW_BCODE + (4 * w + j) * 1024);
+    dma16s(uni_ptr(wsf + (s >> 1) * 256 + (s & 1) * 128), o.obs, sb + TW_BSCL + (w & 1) * 1024);
+    if ((s & 1) == 0)
+      dma16s(uni_ptr(p.a_scales + (s >> 1) * 16), o.oag,
+             uni(lds0 + TW_ASCL + ((apar + (s >> 1)) & 1) * 4096 + w * 1024));
+    else
+      dma16s(uni_ptr(p.a_scales + (s >> 1) * 16), uni(o.oag), uni(lds0 + TW_DUMMY));
+  };
+
+  TwTile cur{};
+  bool have = t < t_end;
+  Offs oc{};
+  int apar = 0;          // A-scale ring slot of the tile's first stage pair
+  int tbuf = 0;          // token buffer of the current tile
+  if (have) {
+    cur = tw_locate(offs, mpre, E, ntn, t, ecur, lane);
+    oc = b_off(cur);
+    if (GATHER) {
+      tok_dma(cur, 0);
+      wait_vm<0>();
+      __syncthreads();
+      a_off_tok(oc, 0);
+    }
+    issue(cur, oc, 0, 0, apar);
+    issue(cur, oc, 1, 1, apar);
+  }
+  while (have) {
+    const int e = cur.e, nt = cur.nt, row0 = cur.row0, nrows = cur.nrows;
+    const int tn = t + nsl;
+    const bool hn = tn < t_end;
+    TwTile nx{};
+    if (hn) nx = tw_locate(offs, mpre, E, ntn, tn, ecur, lane);
+    Offs on{};           // the next tile's load offsets (set in the last stages)
+    const int apar_n = (apar + (nst >> 1)) & 1;
+    const float sw = p.w_gs[2 * e + 1];
+    const bool wide = nrows > 128;
+    const int fa0 = wide ? 4 * wm : 2 * wm;
+    const int mtv = wide ? min(max((nrows - 128 * wm + 31) >> 5, 0), 4)
+                         : min(max((nrows - 64 * wm + 31) >> 5, 0), 2);
+    auto a_src = [&](int s) __attribute__((always_inline)) -> const unsigned char * {
+      return lds + TW_ASCL + ((apar + (s >> 1)) & 1) * 4096;
+    };
+
+    auto run = [&](auto mtv_c) __attribute__((always_inline)) {
+      constexpr int MTV = decltype(mtv_c)::value;
+      f32x16 acc[4][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
+      TwLo L0, L1;
+      // stage 0 of this tile: issued during the previous tile (or above)
+      wait_vm<TW_LOADS>();
+      __syncthreads();
+      // the next tile's tokens into the buffer the previous tile used (every
+      // wave is past it now); landed by the first mid-stage wait
+      if (GATHER && hn) tok_dma(nx, tbuf ^ 1);
+      if constexpr (MTV > 0) tw_read_lo<MTV>(L0, lds, a_src(0), 0, fa0, fb0, lane);
+      // one stage; TAIL: one of the last two, whose mid issues the next
+      // tile's first stages instead of this tile's
+      auto body = [&](const TwLo &Lc, TwLo &Ln, int s, auto tail_c) __attribute__((always_inline)) {
+        constexpr bool TAIL = decltype(tail_c)::value;
+        TwHi Hc;
+        if constexpr (MTV > 0) {
+          tw_read_hi<MTV>(Hc, lds + (s & 1) * TW_STAGE, fa0, fb0, lane);
+          tw_half<MTV>(Lc.a, Lc.b, Lc.as, Lc.bs, acc, 0);
+        }
+        wait_vm<0>();
+        __syncthreads();
+        if constexpr (!TAIL) {
+          issue(cur, oc, s + 2, s & 1, apar);
+        } else if (hn) {
+          if (s + 2 == nst) {
+            on = b_off(nx);
+            if (GATHER) a_off_tok(on, tbuf ^ 1);
+          }
+          issue(nx, on, s + 2 - nst, s & 1, apar_n);
+        }
+        if (!TAIL || s + 1 < nst) {
+          if constexpr (MTV > 0)
+            tw_read_lo<MTV>(Ln, lds + ((s + 1) & 1) * TW_STAGE, a_src(s + 1), s + 1, fa0, fb0, lane);
+        }
+        if constexpr (MTV > 0) tw_half<MTV>(Hc.a, Hc.b, Lc.as, Lc.bs, acc, 1);
+      };
+      for (int s = 0; s < nst - 2; s += 2) {     // nst is even
+        body(L0, L1, s, std::false_type{});
+        body(L1, L0, s + 1, std::false_type{});
+      }
+      body(L0, L1, nst - 2, std::true_type{});
+      body(L1, L0, nst - 1, std::true_type{});
+      // ---- epilogue: tensor scales, SwiGLU (gate fragments 0, 1 with up
+      // fragments 2, 3) or plain, bf16 pairs of adjacent columns swapped
+      // between neighbouring lanes so that every store writes 4 bytes
+      const int h = lane >> 5;
+      const bool odd = (lane & 1) != 0;
+      const int cpair = (lane & 31) & ~1;
+      constexpr int NO = EPI == QD_EPI_SWIGLU ? 2 : 4;
+      const int ldo = EPI == QD_EPI_SWIGLU ? (N >> 1) : N;
+      const bool full = nrows == TW_M;
+      unsigned char *obase = reinterpret_cast<unsigned char *>(p.out);
+      const float alpha = a_dec * sw;
+#pragma unroll
+      for (int i = 0; i < MTV; ++i) {
+        const int rl = 32 * (fa0 + i) + 4 * h + (odd ? 1 : 0);
+#pragma unroll
+        for (int jj = 0; jj < NO; ++jj) {
+          const int cb = EPI == QD_EPI_SWIGLU ? nt * 128 + wn * 64 + 32 * jj
+                                              : nt * TW_N + 32 * (fb0 + jj);
+          const uint32_t voff = (uint32_t)((row0 + rl) * ldo + cb + cpair) * 2u;
+          float v[16];
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            if (EPI == QD_EPI_SWIGLU)
+              v[q] = swiglu_fast(alpha * acc[i][jj][q], alpha * acc[i][jj + 2][q]);
+            else
+              v[q] = alpha * acc[i][jj][q];
+          }
+#pragma unroll
+          for (int q = 0; q < 16; q += 2) {
+            const float send = odd ? v[q] : v[q + 1];
+            const float x = __int_as_float(
+                __builtin_amdgcn_mov_dpp(__float_as_int(send), 0xB1, 0xF, 0xF, false));
+            const f32x2_t pr = odd ? f32x2_t{x, v[q + 1]} : f32x2_t{v[q], x};
+            const uint32_t pk = __builtin_bit_cast(uint32_t, __builtin_convertvector(pr, bf16x2_t));
+            const int qr = 8 * (q >> 2) + (q & 3);
+            if (full || rl + qr < nrows) {
+              *reinterpret_cast<uint32_t *>(obase + (size_t)(qr * ldo * 2) + voff) = pk;
+              vmax = fmaxf(vmax, fmaxf(fabsf(__uint_as_float(pk << 16)),
+                                       fabsf(__uint_as_float(pk & 0xFFFF0000u))));
+            }
+          }
+        }
+      }
+    };
+    switch (mtv) {
+      case 4: run(std::integral_constant<int, 4>{}); break;
+      case 3: run(std::integral_constant<int, 3>{}); break;
+      case 2: run(std::integral_constant<int, 2>{}); break;
+      case 1: run(std::integral_constant<int, 1>{}); break;
+      default: run(std::integral_constant<int, 0>{}); break;
+    }
+    t = tn;
+    have = hn;
+    cur = nx;
+    oc = on;
+    apar = apar_n;
+    tbuf ^= 1;
+  }
+  wait_vm<0>();
+  const float m = block_max(vmax, red);
+  put_amax(p, m);
 }
 
 // host-side plan of the decode kernel
@@ -1330,13 +1780,55 @@ void launch_tile(const GemmArgs &p, const TlPlan &pl, hipStream_t s) {
                      pl.grp);
 }
 
+// host-side plan of the wide prefill kernel (needs the weights'
+// fragment-ordered scales)
+struct WdPlan {
+  bool ok;
+  int ntn, grid, lds;
+};
+
+inline WdPlan wide_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac, int Ks, bool sfrag) {
+  WdPlan pl{};
+  (void)Ks;
+  if (rac || !sfrag || K < 2 * TW_K || K % (2 * TW_K) != 0 || N % TW_N != 0 || E > TL_EMAX)
+    return pl;
+  if (N * K / 2 >= (1LL << 32) || (rows + 1) * K / 2 >= (1LL << 32)) return pl;
+  if ((rows + TW_M) * N * 2 >= (1LL << 32)) return pl;
+  pl.lds = tw_lds_bytes(E);
+  if (pl.lds > TL_LDS_MAX) return pl;
+  pl.ntn = (int)(N / TW_N);
+  // persistent: one workgroup per CU (256 on MI355X), a multiple of 8 (the
+  // XCDs), at most the tile count's upper bound
+  const int64_t g = qdt::tile_grid(rows, E, TW_M, pl.ntn);
+  pl.grid = (int)std::min<int64_t>(256, g);
+  pl.ok = true;
+  return pl;
+}
+
+template <bool GATHER, int EPI>
+void launch_wide(const GemmArgs &p, const WdPlan &pl, hipStream_t s) {
+  auto kern = gemm_wide_kernel<GATHER, EPI>;
+  static const bool attr = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               TL_LDS_MAX) == hipSuccess;
+  (void)attr;
+  hipLaunchKernelGGL(kern, dim3((unsigned)pl.grid), dim3(TW_THREADS), (size_t)pl.lds, s, p, pl.ntn);
+}
+
 template <bool GATHER, bool RAC>
 void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, const SkPlan &pl,
-                const TlPlan &tp) {
+                const TlPlan &tp, const WdPlan &wp) {
   if (pl.ok) {
     if (epi == QD_EPI_SWIGLU) launch_skinny<GATHER, RAC, QD_EPI_SWIGLU>(p, pl, s);
     else launch_skinny<GATHER, RAC, QD_EPI_NONE>(p, pl, s);
     return;
+  }
+  if constexpr (!RAC) {
+    if (wp.ok) {
+      if (epi == QD_EPI_SWIGLU) launch_wide<GATHER, QD_EPI_SWIGLU>(p, wp, s);
+      else launch_wide<GATHER, QD_EPI_NONE>(p, wp, s);
+      return;
+    }
   }
   if (tp.ok) {
     if (epi == QD_EPI_SWIGLU) launch_tile<GATHER, RAC, QD_EPI_SWIGLU>(p, tp, s);
@@ -1368,9 +1860,12 @@ extern "C" int64_t moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int
   if (rows < 0 || N <= 0 || K <= 0 || E < 1 || Ks < 0) return 0;
   const SkPlan pl = skinny_plan(rows, E, N, K, Ks, epilogue);
   if (pl.ok) return pl.grid;
+  // whichever of the other kernels runs (the wide one needs the weights'
+  // fragment-ordered scales) writes every entry of the largest grid
+  const WdPlan wp = wide_plan(rows, E, N, K, Ks > 0, Ks, true);
   const TlPlan tp = tile_plan(rows, E, N, K, Ks > 0, Ks);
-  if (tp.ok) return tp.grid;
-  return grid_x(rows, E, true) * grid_y(N, epilogue);
+  return std::max<int64_t>(std::max<int64_t>(wp.ok ? wp.grid : 0, tp.ok ? tp.grid : 0),
+                           grid_x(rows, E, true) * grid_y(N, epilogue));
 }
 
 // Fragment-ordered weight scales: one thread per output dword, i.e. per
@@ -1485,17 +1980,20 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
   }
   p.out = static_cast<uint16_t *>(out);
   p.amax_part = amax_partials;
+  p.amax_n = amax_partials ? moe_w4a4_grouped_gemm_amax_count(rows, N, K, E, rac ? Ks : 0, epilogue) : 0;
   const TlPlan tp = tile_plan(rows, E, N, K, rac, Ks);
-  // the tiled kernel takes the residual in its compact form only
-  if (rac && !pl.ok && tp.ok && (!rq_sel || !qdh::aligned16(rq_sel))) return rq_sel ? QD_ERR_ALIGN : QD_ERR_NULL;
+  const WdPlan wp = wide_plan(rows, E, N, K, rac, Ks, w->scales_frag != nullptr);
+  // the tiled kernels take the residual in its compact form only
+  if (rac && !pl.ok && (tp.ok || wp.ok) && (!rq_sel || !qdh::aligned16(rq_sel)))
+    return rq_sel ? QD_ERR_ALIGN : QD_ERR_NULL;
   dim3 grid((unsigned)gx, (unsigned)gy);
   hipStream_t s = qdh::S(stream);
   if (row_token) {
-    if (rac) launch_epi<true, true>(p, epilogue, grid, s, pl, tp);
-    else launch_epi<true, false>(p, epilogue, grid, s, pl, tp);
+    if (rac) launch_epi<true, true>(p, epilogue, grid, s, pl, tp, wp);
+    else launch_epi<true, false>(p, epilogue, grid, s, pl, tp, wp);
   } else {
-    if (rac) launch_epi<false, true>(p, epilogue, grid, s, pl, tp);
-    else launch_epi<false, false>(p, epilogue, grid, s, pl, tp);
+    if (rac) launch_epi<false, true>(p, epilogue, grid, s, pl, tp, wp);
+    else launch_epi<false, false>(p, epilogue, grid, s, pl, tp, wp);
   }
   return qdh::check_launch();
 }
