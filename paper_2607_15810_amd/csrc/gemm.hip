@@ -1136,20 +1136,22 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
           if constexpr (RAC) {
             // selected channels of stage s (slot s % NS holds it until the
             // next barrier): decoded weight values into the compact table
+            // (the hardware FP4 conversion with a power-of-two scale and one
+            // f16 multiply by the E4M3 scale, as in the operand decode: exact;
+            // the next channel of the wave is fetched before this one's work)
             const unsigned char *sl = lds + (s % NS) * TL_STAGE;
             const int tb = tid & 127, f = tb >> 5, r = tb & 31;
             while (nsel < TL_K * (s + 1)) {     // wave-uniform
-              const int el = nsel - TL_K * s;
-              float v = 0.0f;
-              if (el >= 0) {                    // S ascending: always
-                const uint32_t byte = sl[TL_BCODE + ((f * 64 + (el >> 5) * 32 + r) * 16) + ((el & 31) >> 1)];
-                const uint32_t code = (el & 1) ? byte >> 4 : byte & 15u;
-                v = e2m1_value(code) * e4m3_to_f32(sl[TL_BSCL + tb * 4 + (el >> 4)]);
-                if (code & 8u) v = -v;
-              }
-              *reinterpret_cast<_Float16 *>(bres + (tb * ksp + nk) * 2) = (_Float16)v;
-              nk += 2;
-              nsel = nk < p.Ks ? (int)uni((uint32_t)sel_l[nk]) : 0x7fffffff;
+              const int el = nsel - TL_K * s;   // >= 0: S is ascending
+              const int nk2 = nk + 2;
+              const int nxt = nk2 < p.Ks ? sel_l[nk2] : 0x7fffffff;
+              const uint32_t byte = sl[TL_BCODE + ((f * 64 + (el >> 5) * 32 + r) * 16) + ((el & 31) >> 1)];
+              const uint32_t sbyte = sl[TL_BSCL + tb * 4 + (el >> 4)];
+              const f16x2 v2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(byte, 256.0f, 0);
+              const f16x2 sc = __builtin_bit_cast(f16x2, sbyte << 7);
+              *reinterpret_cast<_Float16 *>(bres + (tb * ksp + nk) * 2) = (el & 1 ? v2[1] : v2[0]) * sc[0];
+              nk = nk2;
+              nsel = (int)uni((uint32_t)nxt);
             }
           }
         };
