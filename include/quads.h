@@ -483,12 +483,16 @@ qd_status qd_moe_layer_forward_noalloc(const void *x, const float *logits, int64
  * qd_probe_mfma_f16 -- `workgroups` workgroups of four waves, each wave
  *   running `rounds` rounds of 16 independent v_mfma_f32_32x32x16_f16 on
  *   registers; qd_probe_mfma_f16_flops(rounds, workgroups) is the work in
- *   FLOP; out: float [workgroups].
+ *   FLOP; out: float [workgroups].  random_operands = 0: slowly varying
+ *   operand values (few bits toggle); 1: operands with random signs,
+ *   exponents and mantissas, which draw more power and run at a lower
+ *   clock -- the ceiling that GEMMs on real data see.
  * ------------------------------------------------------------------- */
 int64_t   qd_probe_hbm_read_out_count(void);
 qd_status qd_probe_hbm_read(const void *buf, int64_t bytes, uint32_t *out, void *stream);
 double    qd_probe_mfma_f16_flops(int64_t rounds, int32_t workgroups);
-qd_status qd_probe_mfma_f16(int64_t rounds, int32_t workgroups, float *out, void *stream);
+qd_status qd_probe_mfma_f16(int64_t rounds, int32_t workgroups, int32_t random_operands,
+                            float *out, void *stream);
 
 #if defined(__GNUC__) || defined(__clang__)
 #pragma GCC visibility pop

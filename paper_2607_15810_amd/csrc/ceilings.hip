@@ -40,15 +40,29 @@ __global__ __launch_bounds__(kReadThreads) void stream_read_kernel(const uint4 *
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
+// A finite f16 bit pattern with random sign and mantissa and an exponent in
+// [2^-4, 2^3] from a 32-bit integer hash.
+__device__ __forceinline__ uint16_t random_f16_bits(uint32_t x) {
+  x ^= x >> 16; x *= 0x7FEB352Du; x ^= x >> 15; x *= 0x846CA68Bu; x ^= x >> 16;
+  return (uint16_t)((x & 0x83FFu) | ((11u + ((x >> 10) & 7u)) << 10));
+}
+
 // 16 independent accumulators per wave, each updated once per round by
-// v_mfma_f32_32x32x16_f16 on register operands.
-__global__ __launch_bounds__(256) void mfma_loop_kernel(int64_t rounds, float seed,
+// v_mfma_f32_32x32x16_f16 on register operands (slowly varying values, or
+// random ones).
+__global__ __launch_bounds__(256) void mfma_loop_kernel(int64_t rounds, float seed, int rnd,
                                                         float *__restrict__ out) {
   f16x8 a, b;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    a[i] = (_Float16)(seed * (float)(threadIdx.x + i));
-    b[i] = (_Float16)(seed * (float)i);
+    if (rnd) {
+      const uint32_t id = (blockIdx.x * 256u + threadIdx.x) * 16u + i;
+      a[i] = __builtin_bit_cast(_Float16, random_f16_bits(id));
+      b[i] = __builtin_bit_cast(_Float16, random_f16_bits(id + 8u));
+    } else {
+      a[i] = (_Float16)(seed * (float)(threadIdx.x + i));
+      b[i] = (_Float16)(seed * (float)i);
+    }
   }
   f32x16_t acc[16];
 #pragma unroll
@@ -85,11 +99,11 @@ extern "C" double qd_probe_mfma_f16_flops(int64_t rounds, int32_t workgroups) {
   return (double)workgroups * 4.0 * (double)rounds * 16.0 * 32.0 * 32.0 * 16.0 * 2.0;
 }
 
-extern "C" qd_status qd_probe_mfma_f16(int64_t rounds, int32_t workgroups, float *out,
-                                       void *stream) {
+extern "C" qd_status qd_probe_mfma_f16(int64_t rounds, int32_t workgroups,
+                                       int32_t random_operands, float *out, void *stream) {
   if (!out) return QD_ERR_NULL;
   if (rounds < 1 || workgroups < 1) return QD_ERR_SHAPE;
   hipLaunchKernelGGL(mfma_loop_kernel, dim3((unsigned)workgroups), dim3(256), 0, qdh::S(stream),
-                     rounds, 1e-3f, out);
+                     rounds, 1e-3f, random_operands ? 1 : 0, out);
   return qdh::check_launch();
 }

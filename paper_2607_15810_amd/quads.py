@@ -106,7 +106,7 @@ SIGNATURES = {
     "qd_probe_hbm_read_out_count": (c_int64, []),
     "qd_probe_hbm_read": (c_int, [c_void_p, c_int64, c_void_p, c_void_p]),
     "qd_probe_mfma_f16_flops": (ctypes.c_double, [c_int64, c_int32]),
-    "qd_probe_mfma_f16": (c_int, [c_int64, c_int32, c_void_p, c_void_p]),
+    "qd_probe_mfma_f16": (c_int, [c_int64, c_int32, c_int32, c_void_p, c_void_p]),
     "qd_moe_layer_noalloc_max_bytes": (c_size_t, []),
     "qd_moe_layer_forward_noalloc": (c_int, [c_void_p, c_void_p, c_int64, c_int64, c_int32,
                                              c_int32, c_int64, c_int32, c_int32, c_int32, PN, PN,
