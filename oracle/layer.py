@@ -19,6 +19,9 @@ the paper; readings, parity unpinned by the paper):
       as the batch (one channel set shared by all experts), and
       z = bf16_RNE((h_hat - M_S (.) Q_A(dh_q)) W2_hat[e]^T) as in
       Eq. (residual-recon).
+  L7  Optional per-expert channel sets at the W13 input (per_expert=True):
+      each expert selects S_e from the scores of its own rows (oracle.rac,
+      reading L7) and its rows subtract M_{S_e} (.) r_hat.
 
 Stage functions take the previous stage's values explicitly so the tests can
 teacher-force them with the GPU's own intermediates (bf16 h, z), and return
@@ -87,6 +90,41 @@ def w13_stage(xq, rq, row_token, offsets, w13, rows=None):
                         a_abs_src=np.abs(xh) + np.abs(rh))
 
 
+def w13_stage_per_expert(xq, rq, sel_pe, row_token, offsets, w13, rows=None):
+    """A6 with per-expert channel sets (L7): permuted row r of expert e
+    contracts x_hat[t] - M_{S_e} (.) r_hat[t] (t = row_token[r]) against
+    W13_hat[e].  rq: the unmasked residual quantisation.  Returns ([g; u],
+    abs-sum) like w13_stage."""
+    xh = quant.dequantize_f64(xq["codes"], xq["scales"], xq["s_dec"])
+    rh = quant.dequantize_f64(rq["codes"], rq["scales"], rq["s_dec"])
+    offsets = np.asarray(offsets, dtype=np.int64)
+    row_token = np.asarray(row_token, dtype=np.int64)
+    R = int(offsets[-1])
+    rows = np.arange(R) if rows is None else np.asarray(rows, dtype=np.int64)
+    H = xh.shape[1]
+    # the operand row of every permuted row, masked by its expert's set
+    eid = expert_of_rows(offsets, rows)
+    a = np.zeros((rows.size, H))
+    a_abs = np.zeros((rows.size, H))
+    for i, (r, e) in enumerate(zip(rows, eid)):
+        t = row_token[r]
+        m = np.zeros(H, dtype=bool)
+        m[np.asarray(sel_pe[e], dtype=np.int64)] = True
+        rr = np.where(m, rh[t], 0.0)
+        a[i] = xh[t] - rr
+        a_abs[i] = np.abs(xh[t]) + np.abs(rr)
+    # rows are evaluated in their own order: a dense product per expert
+    N = w13["codes"].shape[1]
+    out = np.zeros((rows.size, N))
+    mag = np.zeros((rows.size, N))
+    for e in np.unique(eid):
+        pick = np.nonzero(eid == e)[0]
+        W = dequant_bank_f64(w13, int(e))
+        out[pick] = a[pick] @ W.T
+        mag[pick] = a_abs[pick] @ np.abs(W).T
+    return out, mag
+
+
 def silu(g):
     g = np.asarray(g, dtype=np.float64)
     return g / (1.0 + np.exp(-g))
@@ -128,12 +166,13 @@ def combine(z, inv_row, w, tokens=None):
     return y, mag
 
 
-def moe_layer(x, logits, w13, w2, k, Ks, renorm=True, Ks2=0):
+def moe_layer(x, logits, w13, w2, k, Ks, renorm=True, Ks2=0, per_expert=False):
     """Free-running forward of the whole layer (A1-A9).
 
     x: float32 [T][H] (bf16-valued); logits float32 [T][E];
     w13 / w2: quantised banks from quant.quantize_weight_bank;
-    Ks2: channels of h compensated at the W2 input (L6; 0: none).
+    Ks2: channels of h compensated at the W2 input (L6; 0: none);
+    per_expert: one channel set per expert at the W13 input (L7).
     Returns a dict of every intermediate.
     """
     x = np.asarray(x, dtype=np.float32)
@@ -143,8 +182,13 @@ def moe_layer(x, logits, w13, w2, k, Ks, renorm=True, Ks2=0):
     ids = route.topk_fast(logits, k)
     wts = route.weights(logits, ids, renorm)
     perm = route.permute(ids, E)
-    act = rac.rac_activation(x, Ks)
-    gu, gu_mag = w13_stage(act["xq"], act["rq"], perm["row_token"], perm["offsets"], w13)
+    if per_expert:
+        act = rac.rac_activation_per_expert(x, Ks, perm["row_token"], perm["offsets"])
+        gu, gu_mag = w13_stage_per_expert(act["xq"], act["rq"], act["sel_pe"], perm["row_token"],
+                                          perm["offsets"], w13)
+    else:
+        act = rac.rac_activation(x, Ks)
+        gu, gu_mag = w13_stage(act["xq"], act["rq"], perm["row_token"], perm["offsets"], w13)
     h = swiglu(gu, I)
     if Ks2 > 0:
         act2 = rac.rac_activation(h.astype(np.float32), Ks2)

@@ -29,6 +29,11 @@ grouping is unpinned by the paper):
   R5  x~ = x_hat - M_S (.) r_hat  (float64, from the exact dequantised values)
   R6  y = x~ W_hat^T in float64; by linearity this equals the plain W4A4
       product minus the residual product over the selected channels.
+  L7  (per-expert channel sets, a variant of R2-R4) each expert e ranks the
+      channels by the scores of its own rows alone (the tokens routed to e,
+      same fixed point as R2) and keeps its own S_e; the residual is
+      quantised once over all channels (R4 without the mask), and the W13
+      input of permuted row (t, e) is x_hat[t] - M_{S_e} (.) r_hat[t].
 """
 
 import numpy as np
@@ -101,6 +106,52 @@ def reconstruct(xq, rq):
     xh = quant.dequantize_f64(xq["codes"], xq["scales"], xq["s_dec"])
     rh = quant.dequantize_f64(rq["codes"], rq["scales"], rq["s_dec"])
     return xh - rh          # r_hat is already zero outside S
+
+
+def channel_scores_per_expert(r, amax_x, row_token, offsets):
+    """R2 per expert (reading L7): score_e[j] over the rows routed to expert
+    e, i.e. the tokens row_token[off_e .. off_{e+1}), with the fixed point of
+    the whole batch (F from amax_x).  uint64 [E][K]."""
+    r = np.asarray(r, dtype=np.float32)
+    offsets = np.asarray(offsets, dtype=np.int64)
+    row_token = np.asarray(row_token, dtype=np.int64)
+    E = offsets.size - 1
+    out = np.zeros((E, r.shape[1]), dtype=np.uint64)
+    for e in range(E):
+        toks = row_token[offsets[e]:offsets[e + 1]]
+        if toks.size:
+            out[e] = channel_scores(r[toks], amax_x)
+    return out
+
+
+def select_per_expert(scores_pe, Ks):
+    """R3 per expert: S_e = top-K_s of score_e by (score desc, index asc),
+    ascending.  An expert without rows has all-zero scores, so its S_e is
+    channels 0 .. K_s - 1 (no row uses it).  int32 [E][K_s]."""
+    scores_pe = np.asarray(scores_pe, dtype=np.uint64)
+    return np.stack([select(s, Ks) for s in scores_pe]).astype(np.int32).reshape(
+        scores_pe.shape[0], Ks)
+
+
+def residual_quant(r):
+    """R4 without the mask: Q1-Q7 of the residual over all channels with its
+    own tensor scale (the per-expert variant masks it per expert, L7)."""
+    return quant.quantize(np.asarray(r, dtype=np.float32))
+
+
+def rac_activation_per_expert(x, Ks, row_token, offsets):
+    """A3-A5 with one channel set per expert (reading L7): quantise, residual,
+    per-expert scores over each expert's rows, per-expert selection, the
+    residual quantised once over all channels.  The W13 input of permuted row
+    (t, e) is x_hat[t] - M_{S_e} (.) r_hat[t]."""
+    x = np.asarray(x, dtype=np.float32)
+    xq = quant.quantize(x)
+    xhat = quant.dequantize_f32(xq["codes"], xq["scales"], xq["s_dec"])
+    r = residual(x, xhat)
+    scores_pe = channel_scores_per_expert(r, xq["amax"], row_token, offsets)
+    sel_pe = select_per_expert(scores_pe, Ks)
+    rq = residual_quant(r)
+    return dict(xq=xq, r=r, scores_pe=scores_pe, sel_pe=sel_pe, rq=rq)
 
 
 def rac_activation(x, Ks):
