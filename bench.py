@@ -521,6 +521,14 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
                          time_vs_headline=round(ms / ms_step, 3))
         if k2:
             res[name]["rac_channels_w2"] = k2
+    # one RAC channel set per expert (each expert's own rows rank the
+    # channels; reading L7), at the configured K_s
+    lpe = [ops.MoELayerPerExpert(b13, b2, wl.T, wl.k, wl.Ks) for b13, b2 in banks]
+    mspe = time_steps([lambda c=c: lpe[c](xs[c], lgs[c], y) for c in range(len(lpe))], steps, warm)
+    res["rac_per_expert_sets"] = dict(ms_per_step=round(mspe, 5),
+                                      value=round(wl.T / (mspe * 1e-3), 1), unit="tokens/s",
+                                      rac_channels=wl.Ks,
+                                      time_vs_headline=round(mspe / ms_step, 3))
     # the trainer-side forward on the same weights (Sec. 3.2: bf16
     # activations, fake-quantised NVFP4 weights, no activation quantiser)
     lay16 = [ops.W4A16MoELayer(b13, b2, wl.k) for b13, b2 in banks]
@@ -545,6 +553,8 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
                          ("rac_w13_and_w2", wl.Ks, ks2)):
         lay = ops.MoELayer(b13, b2, wl.T, wl.k, ks, ws=ws, Ks2=k2)
         mism[name] = gap(lay(xs[0], lgs[0]))
+    mism["rac_per_expert_sets"] = gap(lpe[0](xs[0], lgs[0]))
+    del lpe
     res["train_infer_rel_l2"] = mism
     del lay16
     torch.cuda.synchronize()

@@ -170,6 +170,34 @@ qd_status rac_select_channels(const void *x, const qd_nvfp4 *xq, int32_t Ks,
                               void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------
+ * rac_select_channels_per_expert -- one channel set per expert (a variant
+ * of Sec. 3.3 where Eq. (channel-score) and Eq. (channel-select) run over
+ * each expert's own rows, i.e. the tokens routed to it):
+ *   score_e[j] = sum over rows r of expert e of trunc(fl(r_tj^2) * 2^F),
+ *   t = row_token[r], with the fixed point F of rac_select_channels (from
+ *   the tensor amax of x); S_e = the Ks largest, ties to the lower channel,
+ *   ascending (an expert without rows gets channels 0 .. Ks-1).
+ *   x, xq          : the bf16 activation [T][K] and its NVFP4 quantisation.
+ *   row_token, expert_offsets, E, rows : from moe_route_permute (rows = T*k).
+ *   scores_pe      : uint64 [E][K] out; ramax: float [1] out (max |r|).
+ *   sel_pe         : int32 [E][Ks] out.
+ *   rq             : groups 1, T, K; written: the residual quantised over
+ *                    all channels with its own tensor scale (no mask).
+ *   rq_sel_rows    : f16 [rows][rac_selected_width(Ks)] out: row r holds
+ *                    rq[row_token[r]] at the channels of its expert's set,
+ *                    as rac_gather_selected does per token.
+ *   ws             : at least rac_select_channels_per_expert_workspace(T, K, E).
+ *   K <= 16384.
+ * ------------------------------------------------------------------- */
+size_t    rac_select_channels_per_expert_workspace(int64_t T, int64_t K, int32_t E);
+qd_status rac_select_channels_per_expert(const void *x, const qd_nvfp4 *xq, int32_t Ks,
+                                         const int32_t *row_token, const int32_t *expert_offsets,
+                                         int32_t E, int64_t rows, uint64_t *scores_pe,
+                                         float *ramax, int32_t *sel_pe, const qd_nvfp4 *rq,
+                                         void *rq_sel_rows, void *ws, size_t ws_bytes,
+                                         void *stream);
+
+/* ---------------------------------------------------------------------
  * rac_gather_selected -- the masked residual restricted to the selected
  * channels S, compacted per row: the operand r_S of the residual term
  * W[:, S] r_S of Eq. (residual-recon) without its tensor scale,
@@ -235,6 +263,30 @@ qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
                                 const int32_t *sel_idx, int32_t Ks, const void *rq_sel,
                                 int32_t epilogue, void *out, float *amax_partials,
                                 void *stream);
+
+/* ---------------------------------------------------------------------
+ * moe_w4a4_grouped_gemm_per_expert -- moe_w4a4_grouped_gemm with one
+ * channel set per expert (the variant of Sec. 3.3 computed by
+ * rac_select_channels_per_expert): rows of expert e subtract the residual
+ * at S_e,
+ *   v[r][n] = s_dec_a*s_dec_w[e] * acc - s_dec_r*s_dec_w[e] * sum_{j in S_e} rhat[t][j] w[e][n][j].
+ *   sel_pe          : int32 [E][Ks] (each ascending); Ks >= 1.
+ *   rq              : the residual (only its tensor scale is read).
+ *   rq_sel_rows     : f16 [rows][rac_selected_width(Ks)] by grouped row.
+ *   amax_partials   : optional float
+ *                     [moe_w4a4_grouped_gemm_per_expert_amax_count(...)].
+ *   Other arguments as moe_w4a4_grouped_gemm.  Runs on the kernel for many
+ *   rows per expert at every size: QD_ERR_UNSUPPORTED where it does not
+ *   apply (K a multiple of 128 and >= 256, N a multiple of 128, Ks <= ~440).
+ * ------------------------------------------------------------------- */
+int64_t   moe_w4a4_grouped_gemm_per_expert_amax_count(int64_t rows, int64_t N, int64_t K,
+                                                      int32_t E, int32_t Ks, int32_t epilogue);
+qd_status moe_w4a4_grouped_gemm_per_expert(const qd_nvfp4 *a, const int32_t *row_token,
+                                           const int32_t *expert_offsets, int32_t E, int64_t rows,
+                                           const qd_nvfp4 *w, const qd_nvfp4 *rq,
+                                           const int32_t *sel_pe, int32_t Ks,
+                                           const void *rq_sel_rows, int32_t epilogue, void *out,
+                                           float *amax_partials, void *stream);
 
 /* ---------------------------------------------------------------------
  * nvfp4_pack_frag_scales -- a load-time re-layout of a weight tensor's
@@ -406,6 +458,23 @@ qd_status qd_moe_layer_forward(const void *x, const float *logits, int64_t T, in
                                int32_t renorm,
                                const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y,
                                void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------
+ * qd_moe_layer_forward_per_expert -- the layer with one RAC channel set per
+ * expert at the W13 input (rac_select_channels_per_expert,
+ * moe_w4a4_grouped_gemm_per_expert), composed of the boundary calls:
+ * route, quantise X, per-expert selection and residual, W13 with SwiGLU,
+ * quantise h, W2, combine.  Arguments as qd_moe_layer_forward (no W2-site
+ * residual); 1 <= Ks <= H; ws at least
+ * qd_moe_layer_per_expert_workspace(T, H, E, k, I, Ks) bytes.
+ * ------------------------------------------------------------------- */
+size_t    qd_moe_layer_per_expert_workspace(int64_t T, int64_t H, int32_t E, int32_t k,
+                                            int64_t I, int32_t Ks);
+qd_status qd_moe_layer_forward_per_expert(const void *x, const float *logits, int64_t T,
+                                          int64_t H, int32_t E, int32_t k, int64_t I, int32_t Ks,
+                                          int32_t renorm, const qd_nvfp4 *w13,
+                                          const qd_nvfp4 *w2, void *y, void *ws, size_t ws_bytes,
+                                          void *stream);
 
 /*
  * Same as qd_moe_layer_forward, recording HIP events at the stage

@@ -54,6 +54,10 @@ struct GemmArgs {
   uint16_t *out;
   float *amax_part;
   int64_t amax_n;          // entries of amax_part (>= the grid; the rest are zeroed)
+  // per-expert channel sets (tile kernel only): S of expert e at
+  // sel + e * sel_stride, and r_sel indexed by grouped row instead of token
+  int sel_stride;
+  int rsel_rows;
 };
 
 // one maximum of |out| per workgroup into amax_part; workgroups also zero
@@ -1078,7 +1082,8 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
       inv_c = -(a_dec / r_dec);
       res_on = r_dec > 0.0f && fabsf(inv_c) <= 0x1p60f;
       if (res_on) alpha = -r_dec * sw;
-      for (int i = tid; i < ksa; i += TL_THREADS) sel_l[i] = i < p.Ks ? p.sel[i] : 0;
+      for (int i = tid; i < ksa; i += TL_THREADS)
+        sel_l[i] = i < p.Ks ? p.sel[(int64_t)e * p.sel_stride + i] : 0;
       // pad columns of the compact table are zero (the residual's are too)
       const int pad = ksa - p.Ks;
       for (int i = tid; i < TL_N * pad; i += TL_THREADS)
@@ -1111,7 +1116,7 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
         for (int i = 0; i < MTV; ++i) {
           const int rr = 32 * (fa0 + i) + (lane & 31);
           const int rc = rr < nrows ? rr : 0;
-          tkr[i] = GATHER ? p.row_token[row0 + rc] : row0 + rc;
+          tkr[i] = (GATHER && !p.rsel_rows) ? p.row_token[row0 + rc] : row0 + rc;
         }
       }
 #pragma unroll
@@ -1870,6 +1875,15 @@ extern "C" int64_t moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int
                            grid_x(rows, E, true) * grid_y(N, epilogue));
 }
 
+extern "C" int64_t moe_w4a4_grouped_gemm_per_expert_amax_count(int64_t rows, int64_t N,
+                                                               int64_t K, int32_t E, int32_t Ks,
+                                                               int32_t epilogue) {
+  (void)epilogue;
+  if (rows < 0 || N <= 0 || K <= 0 || E < 1 || Ks < 1) return 0;
+  const TlPlan tp = tile_plan(rows, E, N, K, true, Ks);
+  return tp.ok ? tp.grid : 0;
+}
+
 // Fragment-ordered weight scales: one thread per output dword, i.e. per
 // (group e, 16-row fragment f, 256-column chunk c, lane l = 16 g + r); the
 // dword holds the scales of row 16 f + r, blocks 16 c + 4 g .. 16 c + 4 g + 3.
@@ -1917,7 +1931,8 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
                             const int32_t *expert_offsets, int32_t E, int64_t rows,
                             const qd_nvfp4 *w, const qd_nvfp4 *rq, const int32_t *sel_idx,
                             int32_t Ks, const void *rq_sel, const uint32_t *bitmap,
-                            int32_t epilogue, void *out, float *amax_partials, void *stream) {
+                            int32_t epilogue, void *out, float *amax_partials, void *stream,
+                            bool per_expert = false) {
   if (!a || !w || !out) return QD_ERR_NULL;
   if (epilogue != QD_EPI_NONE && epilogue != QD_EPI_SWIGLU) return QD_ERR_DTYPE;
   if (E < 1 || rows < 0) return QD_ERR_SHAPE;
@@ -1948,8 +1963,11 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
   if (N > 0x7fffffff || K > 0x7fffffff) return QD_ERR_UNSUPPORTED;
   const int64_t gx = grid_x(rows, E, true), gy = grid_y(N, epilogue);
   if (gx > 0x7fffffffLL || gy > 65535) return QD_ERR_UNSUPPORTED;
-  const SkPlan pl = skinny_plan(rows, E, N, K, rac ? Ks : 0, epilogue, bitmap != nullptr);
+  // per-expert channel sets run on the tile kernel alone
+  const SkPlan pl = per_expert ? SkPlan{} : skinny_plan(rows, E, N, K, rac ? Ks : 0, epilogue, bitmap != nullptr);
   if (bitmap && !pl.ok) return QD_ERR_UNSUPPORTED;
+  if (per_expert && (!rac || !rq_sel || !tile_plan(rows, E, N, K, true, Ks).ok))
+    return rac && rq_sel ? QD_ERR_UNSUPPORTED : QD_ERR_NULL;
   if (qdh::fault_injected()) return QD_ERR_HIP;
   if (rows == 0) return QD_OK;
 
@@ -1975,6 +1993,8 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
     p.Ks = Ks;
     p.r_sel = static_cast<const uint16_t *>(rq_sel);
     p.ksa = (Ks + 15) / 16 * 16;
+    p.sel_stride = per_expert ? Ks : 0;
+    p.rsel_rows = per_expert ? 1 : 0;
     if (bitmap) {
       p.r_bitmap = bitmap;
       p.sel_out = const_cast<int32_t *>(sel_idx);
@@ -1982,7 +2002,9 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
   }
   p.out = static_cast<uint16_t *>(out);
   p.amax_part = amax_partials;
-  p.amax_n = amax_partials ? moe_w4a4_grouped_gemm_amax_count(rows, N, K, E, rac ? Ks : 0, epilogue) : 0;
+  p.amax_n = !amax_partials ? 0
+             : per_expert ? moe_w4a4_grouped_gemm_per_expert_amax_count(rows, N, K, E, Ks, epilogue)
+                          : moe_w4a4_grouped_gemm_amax_count(rows, N, K, E, rac ? Ks : 0, epilogue);
   const TlPlan tp = tile_plan(rows, E, N, K, rac, Ks);
   const WdPlan wp = wide_plan(rows, E, N, K, rac, Ks, w->scales_frag != nullptr);
   // the tiled kernels take the residual in its compact form only
@@ -2001,6 +2023,16 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
 }
 
 }  // namespace
+
+extern "C" qd_status moe_w4a4_grouped_gemm_per_expert(
+    const qd_nvfp4 *a, const int32_t *row_token, const int32_t *expert_offsets, int32_t E,
+    int64_t rows, const qd_nvfp4 *w, const qd_nvfp4 *rq, const int32_t *sel_pe, int32_t Ks,
+    const void *rq_sel_rows, int32_t epilogue, void *out, float *amax_partials, void *stream) {
+  if (Ks < 1) return QD_ERR_SHAPE;
+  if (!sel_pe || !rq || !rq_sel_rows || !expert_offsets) return QD_ERR_NULL;
+  return grouped_gemm_impl(a, row_token, expert_offsets, E, rows, w, rq, sel_pe, Ks, rq_sel_rows,
+                           nullptr, epilogue, out, amax_partials, stream, true);
+}
 
 extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
                                            const int32_t *expert_offsets, int32_t E, int64_t rows,

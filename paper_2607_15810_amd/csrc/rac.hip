@@ -303,7 +303,185 @@ __global__ __launch_bounds__(256) void rac_gather_selected_kernel(
   }
 }
 
+// ---- per-expert channel sets (reading L7): Eq. (channel-score) over each
+// expert's own rows, Eq. (channel-select) per expert
+
+// Workgroup (column group of 256 channels, expert e): 16 column blocks x 16
+// row lanes walk the expert's rows (their tokens' x and x_hat codes), sum
+// the fixed-point squared residuals per channel, reduce over the row lanes
+// and write score_e once (no atomics: one workgroup owns each entry); the
+// maximum |r| over all rows (every token is some expert's row) goes to
+// ramax.
+__global__ __launch_bounds__(256) void rac_scores_pe_kernel(
+    const uint16_t *__restrict__ x, const uint8_t *__restrict__ codes,
+    const uint8_t *__restrict__ scales, const float *__restrict__ gscale, int64_t K,
+    const float *__restrict__ part, int n_part, const int32_t *__restrict__ row_token,
+    const int32_t *__restrict__ offsets, uint64_t *__restrict__ scores_pe,
+    float *__restrict__ ramax) {
+  __shared__ float red[16];
+  __shared__ uint64_t acc_s[16][256];
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const int e = blockIdx.y;
+  float a = 0.0f;
+  for (int i = threadIdx.x; i < n_part; i += blockDim.x) a = fmaxf(a, part[i]);
+  const float amax = block_max(a, red);
+  int ex;
+  frexpf(amax, &ex);
+  const int F = 36 - 2 * ex;
+  const float s_dec = gscale[1];
+  const int64_t nbc = K >> 4;
+  const int64_t cb = (int64_t)blockIdx.x * 16 + tx;
+  uint64_t acc[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc[i] = 0ull;
+  float rmax = 0.0f;
+  if (cb < nbc) {
+    const int r1 = offsets[e + 1];
+    for (int row = offsets[e] + ty; row < r1; row += 16) {
+      const int64_t t = row_token[row];
+      float v[16], r[16];
+      load_bf16x16(x + t * K + cb * 16, v);
+      const uint2 cw = reinterpret_cast<const uint2 *>(codes + t * (K >> 1))[cb];
+      block_residual(v, cw, scales[t * nbc + cb], s_dec, r);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        rmax = fmaxf(rmax, fabsf(r[i]));
+        const float sq = r[i] * r[i];
+        acc[i] += (uint64_t)ldexp((double)sq, F);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) acc_s[ty][tx * 16 + i] = acc[i];
+  __syncthreads();
+  uint64_t sum = 0;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) sum += acc_s[j][threadIdx.x];
+  const int64_t ch = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (ch < K) scores_pe[(int64_t)e * K + ch] = sum;
+  const float m = block_max(rmax, red);
+  if (threadIdx.x == 0 && m > 0.0f)
+    atomicMax(reinterpret_cast<unsigned int *>(ramax), __float_as_uint(m));
+}
+
+// one workgroup per expert: the selection of rac_select_channels on score_e
+template <int PER>
+__global__ __launch_bounds__(qdc::kSelThreads) void rac_select_pe_kernel(
+    const uint64_t *__restrict__ scores_pe, int K, int Ks, int32_t *__restrict__ sel_pe,
+    uint32_t *__restrict__ bitmaps) {
+  const int e = blockIdx.x;
+  qdc::rac_select_body<PER>(scores_pe + (int64_t)e * K, K, Ks, sel_pe + (int64_t)e * Ks,
+                            bitmaps + (int64_t)e * ((K + 31) / 32));
+}
+
+// the residual (quantised over all channels) at the channels of each
+// permuted row's expert, compacted per row as f16 without the tensor scale
+// (exact); columns past Ks are zero
+__global__ __launch_bounds__(256) void rac_gather_rows_pe_kernel(
+    const uint8_t *__restrict__ codes, const uint8_t *__restrict__ scales, int64_t K,
+    const int32_t *__restrict__ sel_pe, int Ks, int width, const int32_t *__restrict__ row_token,
+    const int32_t *__restrict__ offsets, int E, int64_t rows, uint16_t *__restrict__ out) {
+  const int64_t n = rows * width;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const int64_t r = i / width;
+    const int j = (int)(i - r * width);
+    float v = 0.0f;
+    if (j < Ks) {
+      int lo = 0, hi = E;                 // the expert e with offsets[e] <= r < offsets[e + 1]
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (offsets[mid] <= r) lo = mid; else hi = mid;
+      }
+      const int64_t t = row_token[r];
+      const int64_t c = sel_pe[(int64_t)lo * Ks + j];
+      const uint32_t byte = codes[t * (K >> 1) + (c >> 1)];
+      const uint32_t code = (c & 1) ? byte >> 4 : byte & 15u;
+      v = e2m1_value(code) * e4m3_to_f32(scales[t * (K >> 4) + (c >> 4)]);
+      if (code & 8u) v = -v;
+    }
+    out[i] = __builtin_bit_cast(uint16_t, (_Float16)v);
+  }
+}
+
 }  // namespace
+
+extern "C" size_t rac_select_channels_per_expert_workspace(int64_t T, int64_t K, int32_t E) {
+  (void)T;
+  if (K <= 0 || E < 1) return 0;
+  return qdh::align_up((size_t)E * ((K + 31) / 32) * 4) + qdh::align_up((size_t)((K + 31) / 32) * 4) +
+         256 * sizeof(float) + 256;
+}
+
+extern "C" qd_status rac_select_channels_per_expert(
+    const void *x, const qd_nvfp4 *xq, int32_t Ks, const int32_t *row_token,
+    const int32_t *expert_offsets, int32_t E, int64_t rows, uint64_t *scores_pe, float *ramax,
+    int32_t *sel_pe, const qd_nvfp4 *rq, void *rq_sel_rows, void *ws, size_t ws_bytes,
+    void *stream) {
+  if (!x || !xq || !row_token || !expert_offsets || !scores_pe || !ramax || !rq) return QD_ERR_NULL;
+  const int64_t T = xq->rows, K = xq->cols;
+  qd_status st = qdh::check_nvfp4(xq, 1, T, K);
+  if (st) return st;
+  st = qdh::check_nvfp4(rq, 1, T, K);
+  if (st) return st;
+  if (E < 1 || rows < 0 || Ks < 0 || Ks > K) return QD_ERR_SHAPE;
+  if (K > qdc::kSelMaxK || (K / 256 + 1) > 65535 || E > 65535) return QD_ERR_UNSUPPORTED;
+  if (Ks > 0 && (!sel_pe || !rq_sel_rows)) return QD_ERR_NULL;
+  if (!ws || ws_bytes < rac_select_channels_per_expert_workspace(T, K, E)) return QD_ERR_WORKSPACE;
+  if (!qdh::aligned16(x) || !qdh::aligned16(scores_pe) || !qdh::aligned16(ws) ||
+      (sel_pe && !qdh::aligned16(sel_pe)) || (rq_sel_rows && !qdh::aligned16(rq_sel_rows)))
+    return QD_ERR_ALIGN;
+  if (qdh::fault_injected()) return QD_ERR_HIP;
+  if (T == 0) return QD_OK;
+  hipStream_t s = qdh::S(stream);
+  char *w = static_cast<char *>(ws);
+  uint32_t *bitmaps = reinterpret_cast<uint32_t *>(w);
+  uint32_t *ones = reinterpret_cast<uint32_t *>(w + qdh::align_up((size_t)E * ((K + 31) / 32) * 4));
+  float *part = reinterpret_cast<float *>(reinterpret_cast<char *>(ones) +
+                                          qdh::align_up((size_t)((K + 31) / 32) * 4));
+  const uint16_t *xb = static_cast<const uint16_t *>(x);
+  // amax of X (the fixed point of the scores) and ramax = 0
+  const int64_t n16 = T * K / 16;
+  int g = (int)((n16 + 255) / 256);
+  if (g > 256) g = 256;
+  if (g < 1) g = 1;
+  hipLaunchKernelGGL(rac_amax_kernel, dim3(g), dim3(256), 0, s, xb, n16, part, scores_pe, K, ramax);
+  // the per-expert scores (and max |r|)
+  hipLaunchKernelGGL(rac_scores_pe_kernel, dim3((unsigned)((K + 255) / 256), (unsigned)E),
+                     dim3(256), 0, s, xb, xq->codes, xq->scales, xq->gscale, K, part, g, row_token,
+                     expert_offsets, scores_pe, ramax);
+  if (Ks > 0) {
+    if (K <= 2048)
+      hipLaunchKernelGGL(rac_select_pe_kernel<8>, dim3((unsigned)E), dim3(qdc::kSelThreads), 0, s,
+                         scores_pe, (int)K, Ks, sel_pe, bitmaps);
+    else if (K <= 4096)
+      hipLaunchKernelGGL(rac_select_pe_kernel<16>, dim3((unsigned)E), dim3(qdc::kSelThreads), 0, s,
+                         scores_pe, (int)K, Ks, sel_pe, bitmaps);
+    else
+      hipLaunchKernelGGL(rac_select_pe_kernel<64>, dim3((unsigned)E), dim3(qdc::kSelThreads), 0, s,
+                         scores_pe, (int)K, Ks, sel_pe, bitmaps);
+  }
+  // the residual quantised over all channels (every channel in the mask)
+  qdi::launch_fill_i32(reinterpret_cast<int32_t *>(ones), (K + 31) / 32, -1, s);
+  {
+    const int64_t total = T * (K / 16);
+    int64_t gq = (total + 255) / 256;
+    if (gq > 4096) gq = 4096;
+    if (gq < 1) gq = 1;
+    hipLaunchKernelGGL(rac_resq_kernel, dim3((unsigned)gq), dim3(256), 0, s, xb, xq->codes,
+                       xq->scales, xq->gscale, T, K, ramax, ones, rq->codes, rq->scales,
+                       rq->gscale);
+  }
+  if (Ks > 0 && rows > 0) {
+    const int width = rac_selected_width(Ks);
+    const int64_t n = rows * width;
+    int64_t gg = (n + 255) / 256;
+    if (gg > 8192) gg = 8192;
+    hipLaunchKernelGGL(rac_gather_rows_pe_kernel, dim3((unsigned)gg), dim3(256), 0, s, rq->codes,
+                       rq->scales, K, sel_pe, Ks, width, row_token, expert_offsets, E, rows,
+                       static_cast<uint16_t *>(rq_sel_rows));
+  }
+  return qdh::check_launch();
+}
 
 extern "C" size_t rac_select_channels_workspace(int64_t T, int64_t K) {
   (void)T;

@@ -167,6 +167,48 @@ def select_channels(x, xq, Ks, scores=None, ramax=None):
     return sel[:Ks], rq, scores, ramax
 
 
+def select_channels_per_expert(x, xq, Ks, row_token, offsets):
+    """Per-expert RAC sets over the permuted rows (row_token, offsets from
+    route_permute): returns (sel_pe [E][Ks], rq (all channels), rq_rows
+    [rows][width] f16, scores_pe [E][K] as int64, ramax [1])."""
+    _require_cuda(x)
+    T, K = x.shape
+    dev = x.device
+    E = int(offsets.numel()) - 1
+    rows = int(row_token.numel())
+    scores = torch.empty((E, K), dtype=torch.int64, device=dev)
+    ramax = torch.empty(1, dtype=torch.float32, device=dev)
+    sel = torch.empty((E, max(Ks, 1)), dtype=torch.int32, device=dev)
+    rq = NVFP4Tensor.empty(1, T, K, dev)
+    width = Q.lib().rac_selected_width(Ks)
+    rows_out = torch.empty((max(rows, 1), max(width, 8)), dtype=torch.float16, device=dev)
+    ws = _ws(Q.lib().rac_select_channels_per_expert_workspace(T, K, E), dev)
+    Q.call("rac_select_channels_per_expert", x.data_ptr(), _nv(xq), Ks, row_token.data_ptr(),
+           offsets.data_ptr(), E, rows, scores.data_ptr(), ramax.data_ptr(), sel.data_ptr(),
+           _nv(rq), rows_out.data_ptr(), ws.data_ptr(), ws.numel(), _stream())
+    return sel[:, :Ks], rq, rows_out[:rows, :width], scores, ramax
+
+
+def grouped_gemm_per_expert(a, w, rows, row_token, offsets, rq, sel_pe, rq_rows,
+                            epilogue=Q.QD_EPI_NONE, want_amax=False):
+    """The grouped GEMM with one RAC channel set per expert (sel_pe [E][Ks],
+    rq_rows from select_channels_per_expert)."""
+    dev = a.codes.device
+    E, N, Ks = w.groups, w.rows, int(sel_pe.shape[1])
+    ncol = N // 2 if epilogue == Q.QD_EPI_SWIGLU else N
+    out = torch.empty((rows, ncol), dtype=torch.bfloat16, device=dev)
+    amax = None
+    if want_amax:
+        cnt = Q.lib().moe_w4a4_grouped_gemm_per_expert_amax_count(rows, N, a.cols, E, Ks, epilogue)
+        amax = torch.empty(max(cnt, 1), dtype=torch.float32, device=dev)
+    sel_c = sel_pe.contiguous()
+    rr = rq_rows.contiguous()
+    Q.call("moe_w4a4_grouped_gemm_per_expert", _nv(a), _ptr(row_token), offsets.data_ptr(), E,
+           rows, _nv(w), _nv(rq), sel_c.data_ptr(), Ks, rr.data_ptr(), epilogue, out.data_ptr(),
+           _ptr(amax), _stream())
+    return out, amax
+
+
 def gather_selected(rq, sel):
     """The masked residual at the selected channels, compacted per row: f16
     [rows][rac_selected_width(Ks)] (no tensor scale; zero past Ks)."""
@@ -297,6 +339,32 @@ class MoELayer:
             hr_sel=self.view("hr_sel", torch.float16,
                              (R, Q.lib().rac_selected_width(self.Ks2))),
         )
+
+
+class MoELayerPerExpert:
+    """The layer with one RAC channel set per expert at the W13 input
+    (qd_moe_layer_forward_per_expert), with a reusable workspace."""
+
+    def __init__(self, w13, w2, T, k, Ks, renorm=True):
+        self.w13, self.w2 = w13, w2
+        self.E = w13.groups
+        self.I = w13.rows // 2
+        self.H = w13.cols
+        self.T, self.k, self.Ks, self.renorm = T, k, Ks, renorm
+        n = Q.lib().qd_moe_layer_per_expert_workspace(T, self.H, self.E, k, self.I, Ks)
+        self.ws = _ws(n, w13.codes.device)
+        self._s13 = w13.struct()
+        self._s2 = w2.struct()
+
+    def __call__(self, x, logits, y=None):
+        import ctypes
+        if y is None:
+            y = torch.empty((self.T, self.H), dtype=torch.bfloat16, device=x.device)
+        Q.call("qd_moe_layer_forward_per_expert", x.data_ptr(), logits.data_ptr(), self.T,
+               self.H, self.E, self.k, self.I, self.Ks, int(self.renorm),
+               ctypes.byref(self._s13), ctypes.byref(self._s2), y.data_ptr(),
+               self.ws.data_ptr(), self.ws.numel(), _stream())
+        return y
 
 
 # ---------------------------------------------------------------- W4A16 (trainer-side forward)

@@ -60,6 +60,10 @@ SIGNATURES = {
     "rac_select_channels_workspace": (c_size_t, [c_int64, c_int64]),
     "rac_select_channels": (c_int, [c_void_p, PN, c_int32, c_void_p, c_void_p, c_int32,
                                     c_void_p, PN, c_void_p, c_size_t, c_void_p]),
+    "rac_select_channels_per_expert_workspace": (c_size_t, [c_int64, c_int64, c_int32]),
+    "rac_select_channels_per_expert": (c_int, [c_void_p, PN, c_int32, c_void_p, c_void_p,
+                                               c_int32, c_int64, c_void_p, c_void_p, c_void_p,
+                                               PN, c_void_p, c_void_p, c_size_t, c_void_p]),
     "rac_selected_width": (c_int32, [c_int32]),
     "rac_gather_selected": (c_int, [PN, c_void_p, c_int32, c_void_p, c_void_p]),
     "rac_residual_gemm": (c_int, [PN, c_void_p, c_int32, c_void_p, c_void_p, c_int64, PN,
@@ -71,6 +75,11 @@ SIGNATURES = {
     "moe_w4a4_grouped_gemm": (c_int, [PN, c_void_p, c_void_p, c_int32, c_int64, PN, PN,
                                       c_void_p, c_int32, c_void_p, c_int32, c_void_p, c_void_p,
                                       c_void_p]),
+    "moe_w4a4_grouped_gemm_per_expert_amax_count": (c_int64, [c_int64, c_int64, c_int64,
+                                                              c_int32, c_int32, c_int32]),
+    "moe_w4a4_grouped_gemm_per_expert": (c_int, [PN, c_void_p, c_void_p, c_int32, c_int64, PN,
+                                                 PN, c_void_p, c_int32, c_void_p, c_int32,
+                                                 c_void_p, c_void_p, c_void_p]),
     "moe_unpermute_combine": (c_int, [c_void_p, c_void_p, c_void_p, c_int64, c_int32, c_int64,
                                       c_void_p, c_void_p]),
     "fp8_quantize_rows": (c_int, [c_void_p, c_int32, c_int64, c_int64, c_void_p, c_void_p,
@@ -103,6 +112,11 @@ SIGNATURES = {
                                            c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]),
     "qd_moe_layer_views": (c_int, [c_int64, c_int64, c_int32, c_int32, c_int64,
                                    POINTER(c_int64)]),
+    "qd_moe_layer_per_expert_workspace": (c_size_t, [c_int64, c_int64, c_int32, c_int32,
+                                                     c_int64, c_int32]),
+    "qd_moe_layer_forward_per_expert": (c_int, [c_void_p, c_void_p, c_int64, c_int64, c_int32,
+                                                c_int32, c_int64, c_int32, c_int32, PN, PN,
+                                                c_void_p, c_void_p, c_size_t, c_void_p]),
     "qd_probe_hbm_read_out_count": (c_int64, []),
     "qd_probe_hbm_read": (c_int, [c_void_p, c_int64, c_void_p, c_void_p]),
     "qd_probe_mfma_f16_flops": (ctypes.c_double, [c_int64, c_int32]),

@@ -261,3 +261,47 @@ def test_w4a16_validation(lib):
     assert g(F + 2, 16, None, F, 2, 16, ctypes.byref(w), 0, F, None) == Q.QD_ERR_ALIGN
     assert g(None, 0, None, F, 2, 0, ctypes.byref(w), 0, None, None) == Q.QD_OK   # no rows
 
+
+
+def test_per_expert_validation(lib):
+    """Per-expert RAC sets: argument checks before any launch."""
+    xq = _nv(1, 8, 256, FAKE)
+    rq = _nv(1, 8, 256, FAKE)
+    ws = lib.rac_select_channels_per_expert_workspace(8, 256, 4)
+    assert ws > 0
+    r = lambda *x: Q.raw("rac_select_channels_per_expert", *x)
+    # (x, xq, Ks, row_token, offsets, E, rows, scores_pe, ramax, sel_pe, rq, rq_rows, ws, ws_bytes, stream)
+    assert r(FAKE, ctypes.byref(xq), 257, FAKE, FAKE, 4, 16, FAKE, FAKE, FAKE, ctypes.byref(rq),
+             FAKE, FAKE, ws, None) == Q.QD_ERR_SHAPE          # K_s > K
+    assert r(FAKE, ctypes.byref(xq), 4, None, FAKE, 4, 16, FAKE, FAKE, FAKE, ctypes.byref(rq),
+             FAKE, FAKE, ws, None) == Q.QD_ERR_NULL           # no routing
+    assert r(FAKE, ctypes.byref(xq), 4, FAKE, FAKE, 4, 16, FAKE, FAKE, None, ctypes.byref(rq),
+             FAKE, FAKE, ws, None) == Q.QD_ERR_NULL           # K_s > 0 without the sets
+    assert r(FAKE, ctypes.byref(xq), 4, FAKE, FAKE, 4, 16, FAKE, FAKE, FAKE, ctypes.byref(rq),
+             FAKE, FAKE, 8, None) == Q.QD_ERR_WORKSPACE
+    assert r(FAKE, ctypes.byref(xq), 4, FAKE, FAKE, 4, 16, FAKE, FAKE, FAKE, ctypes.byref(rq),
+             FAKE + 8, FAKE, ws, None) == Q.QD_ERR_ALIGN
+    a = _nv(1, 64, 256, FAKE)
+    rq = _nv(1, 64, 256, FAKE)
+    w = _nv(4, 256, 256, FAKE)
+    g = lambda *x: Q.raw("moe_w4a4_grouped_gemm_per_expert", *x)
+    # (a, row_token, offsets, E, rows, w, rq, sel_pe, Ks, rq_rows, epilogue, out, amax, stream)
+    assert g(ctypes.byref(a), FAKE, FAKE, 4, 128, ctypes.byref(w), ctypes.byref(rq), FAKE, 0,
+             FAKE, 1, FAKE, None, None) == Q.QD_ERR_SHAPE       # K_s >= 1
+    assert g(ctypes.byref(a), FAKE, FAKE, 4, 128, ctypes.byref(w), ctypes.byref(rq), None, 4,
+             FAKE, 1, FAKE, None, None) == Q.QD_ERR_NULL
+    w_n = _nv(4, 80, 256, FAKE)                    # N not a multiple of 128: no tile kernel
+    assert g(ctypes.byref(a), FAKE, FAKE, 4, 128, ctypes.byref(w_n), ctypes.byref(rq), FAKE, 4,
+             FAKE, 0, FAKE, None, None) == Q.QD_ERR_UNSUPPORTED
+    assert lib.moe_w4a4_grouped_gemm_per_expert_amax_count(128, 256, 256, 4, 4, 1) > 0
+    assert lib.moe_w4a4_grouped_gemm_per_expert_amax_count(128, 80, 256, 4, 4, 1) == 0
+    assert lib.qd_moe_layer_per_expert_workspace(64, 256, 4, 2, 128, 8) > 0
+    lw = lambda *x: Q.raw("qd_moe_layer_forward_per_expert", *x)
+    w13 = _nv(4, 256, 256, FAKE)
+    w2 = _nv(4, 256, 128, FAKE)
+    assert lw(FAKE, FAKE, 64, 256, 4, 2, 128, 0, 1, ctypes.byref(w13), ctypes.byref(w2), FAKE,
+              FAKE, 1 << 30, None) == Q.QD_ERR_SHAPE           # K_s >= 1
+    assert lw(FAKE, FAKE, 64, 256, 4, 2, 128, 8, 1, ctypes.byref(w13), ctypes.byref(w2), FAKE,
+              FAKE, 16, None) == Q.QD_ERR_WORKSPACE
+    assert lw(None, None, 0, 256, 4, 2, 128, 8, 1, ctypes.byref(w13), ctypes.byref(w2), None,
+              None, 0, None) == Q.QD_OK                       # empty batch
