@@ -243,10 +243,13 @@ qd_status rac_residual_gemm(const qd_nvfp4 *rq, const int32_t *sel_idx, int32_t 
  *   rq, sel_idx, Ks : the masked residual (NULL / 0: plain W4A4; Ks > 0
  *                     needs rq).
  *   rq_sel          : rac_gather_selected(rq, sel_idx, Ks) (f16, 16-byte
- *                     aligned).  The kernel for many rows per expert
- *                     contracts the residual in this compact form and
- *                     returns QD_ERR_NULL without it; other shapes ignore
- *                     it (NULL allowed).
+ *                     aligned).  Where moe_w4a4_grouped_gemm_residual_form
+ *                     is 2 (many rows per expert, K_s small enough for the
+ *                     compact weight table in LDS) the kernel contracts the
+ *                     residual in this compact form and returns QD_ERR_NULL
+ *                     without it; where it is 1 the kernel reads the masked
+ *                     residual rq (a second pass over K for many rows) and
+ *                     ignores rq_sel (NULL allowed).
  *   epilogue        : QD_EPI_NONE: out bf16 [rows][N] = bf16(v);
  *                     QD_EPI_SWIGLU: N = 2I, gate rows [0,I), up rows
  *                     [I,2I); out bf16 [rows][I] = bf16(silu(g)*u).
@@ -257,6 +260,11 @@ qd_status rac_residual_gemm(const qd_nvfp4 *rq, const int32_t *sel_idx, int32_t 
  * ------------------------------------------------------------------- */
 int64_t   moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int64_t K, int32_t E,
                                            int32_t Ks, int32_t epilogue);
+/* which form of the residual moe_w4a4_grouped_gemm reads for these sizes:
+ * 0 none (Ks = 0 or empty), 1 the masked residual rq, 2 the compact rq_sel
+ * (with rq's tensor scale).  Pure host function, no error path. */
+int32_t   moe_w4a4_grouped_gemm_residual_form(int64_t rows, int64_t N, int64_t K, int32_t E,
+                                              int32_t Ks, int32_t epilogue);
 qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row_token,
                                 const int32_t *expert_offsets, int32_t E, int64_t rows,
                                 const qd_nvfp4 *w, const qd_nvfp4 *rq,

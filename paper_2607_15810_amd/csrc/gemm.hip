@@ -993,9 +993,13 @@ __device__ __forceinline__ float swiglu_fast(float g, float u) {
   return g * __builtin_amdgcn_rcpf(1.0f + e) * u;
 }
 
-template <bool GATHER, bool RAC, int EPI>
+// DENSE (with RAC): the residual as a second pass over K on the masked
+// residual codes (for K_s too large for the compact table)
+template <bool GATHER, bool RAC, int EPI, bool DENSE = false>
 __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, int ntn, int grp) {
-  constexpr int NS = tl_ns(RAC);
+  static_assert(RAC || !DENSE, "the dense residual mode needs RAC");
+  constexpr bool CMP = RAC && !DENSE;      // compact residual table
+  constexpr int NS = tl_ns(CMP);
   extern __shared__ __align__(16) unsigned char lds[];
   __shared__ int sh_w[4];
   __shared__ int sh_t[4];
@@ -1033,14 +1037,17 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
     const int bsstep = sfrag ? 64 : 4;
     const int nst = K / TL_K;
     // the A-scale ring (grp): after the stage ring and the compact table
-    const uint32_t agrp = lds0 + (uint32_t)tl_lds_bytes(RAC, RAC ? p.ksa : 0);
+    const uint32_t agrp = lds0 + (uint32_t)tl_lds_bytes(CMP, CMP ? p.ksa : 0);
     const uint32_t oag = arow(64 * w + lane) * (uint32_t)kb16;
     // five loads per wave and stage (waves 0 / 2 and 1 / 3 load the same B
     // scale half: equal bytes to equal places)
+    // the A operand of the pass: the activations, then (DENSE) the masked
+    // residual, same layout
+    const uint8_t *a_cod = p.a_codes, *a_scl = p.a_scales;
     auto issue = [&](int s, int q) __attribute__((always_inline)) {
       s = min(s, nst - 1);
       const uint32_t sb = uni(lds0 + q * TL_STAGE);
-      const uint8_t *ac = uni_ptr(p.a_codes + s * 32), *as_ = uni_ptr(p.a_scales + s * 4);
+      const uint8_t *ac = uni_ptr(a_cod + s * 32), *as_ = uni_ptr(a_scl + s * 4);
       const uint8_t *bc = uni_ptr(wc + s * 32), *bs_ = uni_ptr(ws + s * bsstep);
       dma16s(ac, oa0, sb + TL_ACODE + (2 * w) * 1024);
       dma16s(ac, oa1, sb + TL_ACODE + (2 * w + 1) * 1024);
@@ -1052,10 +1059,10 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
         // never one line for the whole chip) into the unused A-scale area of
         // their stage slot
         if ((s & 3) == 0)
-          dma16s(uni_ptr(p.a_scales + (s >> 2) * 16), oag,
+          dma16s(uni_ptr(a_scl + (s >> 2) * 16), oag,
                  uni(agrp + ((s >> 2) & 1) * (TL_AGRP / 2) + w * 1024));
         else
-          dma16s(uni_ptr(p.a_scales + (s >> 2) * 16), uni(oag), sb + TL_ASCL);
+          dma16s(uni_ptr(a_scl + (s >> 2) * 16), uni(oag), sb + TL_ASCL);
       } else {
         dma4s(as_, oas, sb + TL_ASCL + w * 256);
       }
@@ -1074,7 +1081,7 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
     // left out (its share of any output is far below f32 resolution).
     float inv_c = 0.0f;
     bool res_on = false;
-    const int ksa = RAC ? p.ksa : 0, ksp = ksa + 8;
+    const int ksa = CMP ? p.ksa : 0, ksp = ksa + 8;
     unsigned char *bres = lds + NS * TL_STAGE;
     int32_t *sel_l = reinterpret_cast<int32_t *>(bres + TL_N * ksp * 2);
     if (RAC) {
@@ -1082,12 +1089,15 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
       inv_c = -(a_dec / r_dec);
       res_on = r_dec > 0.0f && fabsf(inv_c) <= 0x1p60f;
       if (res_on) alpha = -r_dec * sw;
-      for (int i = tid; i < ksa; i += TL_THREADS)
-        sel_l[i] = i < p.Ks ? p.sel[(int64_t)e * p.sel_stride + i] : 0;
-      // pad columns of the compact table are zero (the residual's are too)
-      const int pad = ksa - p.Ks;
-      for (int i = tid; i < TL_N * pad; i += TL_THREADS)
-        *reinterpret_cast<_Float16 *>(bres + ((i / pad) * ksp + p.Ks + i % pad) * 2) = (_Float16)0.0f;
+      if constexpr (CMP) {
+        for (int i = tid; i < ksa; i += TL_THREADS)
+          sel_l[i] = i < p.Ks ? p.sel[(int64_t)e * p.sel_stride + i] : 0;
+        // pad columns of the compact table are zero (the residual's are too)
+        const int pad = ksa - p.Ks;
+        for (int i = tid; i < TL_N * pad; i += TL_THREADS)
+          *reinterpret_cast<_Float16 *>(bres + ((i / pad) * ksp + p.Ks + i % pad) * 2) =
+              (_Float16)0.0f;
+      }
     }
     const int wm = w & 1, wn = w >> 1;
     const bool wide = nrows > 128;
@@ -1111,7 +1121,7 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
       // RAC: the tokens of this lane's residual rows, loaded before the K
       // loop so the residual steps after it wait for one load, not two
       int32_t tkr[MTV > 0 ? MTV : 1];
-      if constexpr (RAC && MTV > 0) {
+      if constexpr (CMP && MTV > 0) {
 #pragma unroll
         for (int i = 0; i < MTV; ++i) {
           const int rr = 32 * (fa0 + i) + (lane & 31);
@@ -1119,17 +1129,12 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
           tkr[i] = (GATHER && !p.rsel_rows) ? p.row_token[row0 + rc] : row0 + rc;
         }
       }
-#pragma unroll
-      for (int t = 0; t < NS - 1; ++t) issue(t, t);
-      wait_vm<(NS - 2) * 5>();
-      __syncthreads();
-      if constexpr (MTV > 0) tl_read<MTV>(R0, lds, a_src(0), astr, fa0, fb0, fbs, lane);
       // RAC: the next selected channel this wave copies (waves 0, 1 take the
       // even entries of S, waves 2, 3 the odd ones; S is ascending), held in a
       // register so a stage without one of its channels costs one compare
+      // (read after the prologue's barrier: other threads wrote sel_l)
       int nk = tid >> 7;
       int nsel = 0x7fffffff;
-      if constexpr (RAC) nsel = nk < p.Ks ? (int)uni((uint32_t)sel_l[nk]) : 0x7fffffff;
       auto body = [&](const TlRaw &Rc, TlRaw &Rn, int s) __attribute__((always_inline)) {
         auto mid = [&]() __attribute__((always_inline)) {
           wait_vm<(NS - 3) * 5>();
@@ -1138,7 +1143,7 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
           if constexpr (MTV > 0)
             tl_read<MTV>(Rn, lds + ((s + 1) % NS) * TL_STAGE, a_src(s + 1), astr, fa0, fb0, fbs,
                          lane);
-          if constexpr (RAC) {
+          if constexpr (CMP) {
             // selected channels of stage s (slot s % NS holds it until the
             // next barrier): decoded weight values into the compact table
             // (the hardware FP4 conversion with a power-of-two scale and one
@@ -1163,12 +1168,40 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
         if constexpr (MTV > 0) tl_stage<MTV>(Rc, acc, lane, mid);
         else mid();
       };
-      for (int s = 0; s < nst; s += 2) {     // nst is even
-        body(R0, R1, s);
-        body(R1, R0, s + 1);
+      // one pass over K: the ring's prologue, then the stages
+      auto kpass = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int t = 0; t < NS - 1; ++t) issue(t, t);
+        wait_vm<(NS - 2) * 5>();
+        __syncthreads();
+        if constexpr (CMP) nsel = nk < p.Ks ? (int)uni((uint32_t)sel_l[nk]) : 0x7fffffff;
+        if constexpr (MTV > 0) tl_read<MTV>(R0, lds, a_src(0), astr, fa0, fb0, fbs, lane);
+        for (int s = 0; s < nst; s += 2) {     // nst is even
+          body(R0, R1, s);
+          body(R1, R0, s + 1);
+        }
+        wait_vm<0>();
+      };
+      kpass();
+      if constexpr (DENSE) {
+        // the residual: acc -> acc * inv_c, then a second pass over K with
+        // the masked residual codes as the A operand (zero outside S), so the
+        // epilogue's scale -s_dec_r * s_dec_w yields
+        // s_dec_x s_dec_w acc - s_dec_r s_dec_w accr
+        if (res_on) {
+          __syncthreads();                     // every wave is done with the ring
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+              for (int q = 0; q < 16; ++q) acc[i][j][q] *= inv_c;
+          a_cod = p.r_codes;
+          a_scl = p.r_scales;
+          kpass();
+        }
       }
-      wait_vm<0>();
-      if constexpr (RAC) {
+      if constexpr (CMP) {
         if (res_on) {
           __syncthreads();                     // the compact table is complete
           if constexpr (MTV > 0) {
@@ -1748,11 +1781,16 @@ void launch_skinny(const GemmArgs &p, const SkPlan &pl, hipStream_t s) {
 // host-side plan of the prefill kernel
 struct TlPlan {
   bool ok;
+  bool dense;   // RAC as a second pass over K on the masked residual
   int ntn, grid, lds, grp;
 };
 
-// rac: the residual is fused (needs its compact form, rq_sel)
-inline TlPlan tile_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac, int Ks) {
+// rac: the residual is fused, in its compact form (rq_sel) while the compact
+// weight table leaves LDS for two workgroups per CU, else as the dense second
+// pass over the masked residual (faster than the table at one workgroup per
+// CU); compact_only: the table wherever it fits at all
+inline TlPlan tile_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac, int Ks,
+                        bool compact_only = false) {
   TlPlan pl{};
   if (K < 4 * TL_K || K % (2 * TL_K) != 0 || N % TL_N != 0 || E > TL_EMAX) return pl;
   // byte offsets inside one activation matrix or one expert's weights, and
@@ -1760,6 +1798,10 @@ inline TlPlan tile_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac, int
   if (N * K / 2 >= (1LL << 32) || (rows + 1) * K / 2 >= (1LL << 32)) return pl;
   if ((rows + TL_M) * N * 2 >= (1LL << 32)) return pl;
   pl.lds = tl_lds_bytes(rac, rac ? (Ks + 15) / 16 * 16 : 0);
+  if (rac && !compact_only && pl.lds > TL_LDS_2WG) {
+    pl.dense = true;
+    pl.lds = tl_lds_bytes(false, 0);
+  }
   if (pl.lds > TL_LDS_MAX) return pl;
   // the A-scale ring where it keeps the workgroups per CU (groups of four
   // stages: K a multiple of 256, so no group reads past a row's scales)
@@ -1776,9 +1818,9 @@ inline TlPlan tile_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac, int
   return pl;
 }
 
-template <bool GATHER, bool RAC, int EPI>
+template <bool GATHER, bool RAC, int EPI, bool DENSE = false>
 void launch_tile(const GemmArgs &p, const TlPlan &pl, hipStream_t s) {
-  auto kern = gemm_tile_kernel<GATHER, RAC, EPI>;
+  auto kern = gemm_tile_kernel<GATHER, RAC, EPI, DENSE>;
   static const bool attr = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize,
                                                TL_LDS_MAX) == hipSuccess;
@@ -1838,6 +1880,13 @@ void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, const SkPl
     }
   }
   if (tp.ok) {
+    if constexpr (RAC) {
+      if (tp.dense) {
+        if (epi == QD_EPI_SWIGLU) launch_tile<GATHER, true, QD_EPI_SWIGLU, true>(p, tp, s);
+        else launch_tile<GATHER, true, QD_EPI_NONE, true>(p, tp, s);
+        return;
+      }
+    }
     if (epi == QD_EPI_SWIGLU) launch_tile<GATHER, RAC, QD_EPI_SWIGLU>(p, tp, s);
     else launch_tile<GATHER, RAC, QD_EPI_NONE>(p, tp, s);
     return;
@@ -1853,13 +1902,21 @@ void launch_epi(const GemmArgs &p, int epi, dim3 grid, hipStream_t s, const SkPl
 bool qdi::gemm_wants_rq_sel(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
                             int32_t epilogue) {
   if (Ks <= 0 || rows <= 0 || E < 1 || N <= 0 || K <= 0) return false;
-  return !skinny_plan(rows, E, N, K, Ks, epilogue).ok && tile_plan(rows, E, N, K, true, Ks).ok;
+  if (skinny_plan(rows, E, N, K, Ks, epilogue).ok) return false;
+  const TlPlan tp = tile_plan(rows, E, N, K, true, Ks);
+  return tp.ok && !tp.dense;
 }
 
 bool qdi::gemm_takes_bitmap(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
                             int32_t epilogue) {
   if (Ks <= 0 || rows <= 0 || E < 1 || N <= 0 || K <= 0) return false;
   return skinny_plan(rows, E, N, K, Ks, epilogue, true).ok;
+}
+
+extern "C" int32_t moe_w4a4_grouped_gemm_residual_form(int64_t rows, int64_t N, int64_t K,
+                                                       int32_t E, int32_t Ks, int32_t epilogue) {
+  if (Ks <= 0 || rows <= 0 || E < 1 || N <= 0 || K <= 0) return 0;
+  return qdi::gemm_wants_rq_sel(rows, E, N, K, Ks, epilogue) ? 2 : 1;
 }
 
 extern "C" int64_t moe_w4a4_grouped_gemm_amax_count(int64_t rows, int64_t N, int64_t K,
@@ -1880,7 +1937,7 @@ extern "C" int64_t moe_w4a4_grouped_gemm_per_expert_amax_count(int64_t rows, int
                                                                int32_t epilogue) {
   (void)epilogue;
   if (rows < 0 || N <= 0 || K <= 0 || E < 1 || Ks < 1) return 0;
-  const TlPlan tp = tile_plan(rows, E, N, K, true, Ks);
+  const TlPlan tp = tile_plan(rows, E, N, K, true, Ks, true);
   return tp.ok ? tp.grid : 0;
 }
 
@@ -1966,8 +2023,12 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
   // per-expert channel sets run on the tile kernel alone
   const SkPlan pl = per_expert ? SkPlan{} : skinny_plan(rows, E, N, K, rac ? Ks : 0, epilogue, bitmap != nullptr);
   if (bitmap && !pl.ok) return QD_ERR_UNSUPPORTED;
-  if (per_expert && (!rac || !rq_sel || !tile_plan(rows, E, N, K, true, Ks).ok))
-    return rac && rq_sel ? QD_ERR_UNSUPPORTED : QD_ERR_NULL;
+  if (per_expert) {
+    // per-expert sets take the compact residual (one per grouped row)
+    const TlPlan pp = tile_plan(rows, E, N, K, true, Ks, true);
+    if (!rac || !rq_sel || !pp.ok)
+      return rac && rq_sel ? QD_ERR_UNSUPPORTED : QD_ERR_NULL;
+  }
   if (qdh::fault_injected()) return QD_ERR_HIP;
   if (rows == 0) return QD_OK;
 
@@ -2005,10 +2066,11 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
   p.amax_n = !amax_partials ? 0
              : per_expert ? moe_w4a4_grouped_gemm_per_expert_amax_count(rows, N, K, E, Ks, epilogue)
                           : moe_w4a4_grouped_gemm_amax_count(rows, N, K, E, rac ? Ks : 0, epilogue);
-  const TlPlan tp = tile_plan(rows, E, N, K, rac, Ks);
+  const TlPlan tp = tile_plan(rows, E, N, K, rac, Ks, per_expert);
   const WdPlan wp = wide_plan(rows, E, N, K, rac, Ks, w->scales_frag != nullptr);
-  // the tiled kernels take the residual in its compact form only
-  if (rac && !pl.ok && (tp.ok || wp.ok) && (!rq_sel || !qdh::aligned16(rq_sel)))
+  // the tile kernel takes the residual in its compact form unless its plan
+  // is the dense second pass (which reads the masked residual rq)
+  if (rac && !pl.ok && tp.ok && !tp.dense && (!rq_sel || !qdh::aligned16(rq_sel)))
     return rq_sel ? QD_ERR_ALIGN : QD_ERR_NULL;
   dim3 grid((unsigned)gx, (unsigned)gy);
   hipStream_t s = qdh::S(stream);

@@ -230,7 +230,7 @@ def residual_gemm(rq, sel, w, rows, row_token=None, offsets=None):
 def grouped_gemm(a, w, rows, row_token=None, offsets=None, rq=None, sel=None,
                  epilogue=Q.QD_EPI_NONE, want_amax=False, rq_sel=None):
     """rq_sel: the compact residual (gather_selected(rq, sel)); formed here
-    when the residual is given without it."""
+    when the kernel for these sizes reads it and it is not given."""
     dev = a.codes.device
     E = w.groups
     N = w.rows
@@ -241,7 +241,8 @@ def grouped_gemm(a, w, rows, row_token=None, offsets=None, rq=None, sel=None,
     if want_amax:
         cnt = Q.lib().moe_w4a4_grouped_gemm_amax_count(rows, N, a.cols, E, Ks, epilogue)
         amax = torch.empty(max(cnt, 1), dtype=torch.float32, device=dev)
-    if Ks and rq_sel is None:
+    if Ks and rq_sel is None and Q.lib().moe_w4a4_grouped_gemm_residual_form(
+            rows, N, a.cols, E, Ks, epilogue) == 2:
         rq_sel = gather_selected(rq, sel)
     Q.call("moe_w4a4_grouped_gemm", _nv(a), _ptr(row_token), _ptr(offsets), E, rows, _nv(w),
            _nv(rq) if Ks else None, _ptr(sel) if Ks else None, Ks,

@@ -70,6 +70,8 @@ SIGNATURES = {
                                   c_void_p, c_void_p]),
     "moe_w4a4_grouped_gemm_amax_count": (c_int64, [c_int64, c_int64, c_int64, c_int32, c_int32,
                                                    c_int32]),
+    "moe_w4a4_grouped_gemm_residual_form": (c_int32, [c_int64, c_int64, c_int64, c_int32,
+                                                      c_int32, c_int32]),
     "nvfp4_frag_scales_bytes": (c_int64, [c_int64, c_int64, c_int64]),
     "nvfp4_pack_frag_scales": (c_int, [PN, c_void_p, c_void_p]),
     "moe_w4a4_grouped_gemm": (c_int, [PN, c_void_p, c_void_p, c_int32, c_int64, PN, PN,

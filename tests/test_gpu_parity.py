@@ -61,6 +61,15 @@ SMALL = [
     ("tile_rac_zipf_edges", 300, 512, 8, 2, 128, 40,
      dict(routing="zipf", acts="student_t3", edge_cases=True, outlier_frac=0.0)),
     ("tile_rac_all", 256, 256, 4, 2, 64, 256, {}),
+    # the largest K_s the compact table takes at two workgroups per CU
+    ("tile_rac_compact_max", 256, 512, 4, 2, 128, 144, {}),
+    # K_s beyond it: the residual as a second pass over K on the masked
+    # residual (K_s = 145, K_s = H/2, and a ragged K_s near K with skewed
+    # routing and edge values; tile_rac_all above is K_s = K)
+    ("tile_rac_dense_145", 256, 512, 4, 2, 128, 145, {}),
+    ("tile_rac_dense", 256, 1024, 4, 2, 128, 512, {}),
+    ("tile_rac_dense_zipf_edges", 300, 1024, 8, 2, 128, 1000,
+     dict(routing="zipf", acts="student_t3", edge_cases=True, outlier_frac=0.0)),
     # H > 4096 at decode shapes: the one-workgroup selection and the separate
     # masked-residual pass instead of the fused selection by rank
     ("wide_h_resq", 16, 5120, 4, 2, 64, 40, {}),
@@ -133,6 +142,12 @@ def test_layer_stagewise_small(case):
     assert np.array_equal(sel2.cpu().numpy(), sel.cpu().numpy())
     # A6 without the epilogue: [g; u] against the float64 contraction
     R = T * k
+    if name.startswith("tile_rac"):
+        # the tile kernel's dense residual mode reads the masked residual, the
+        # compact one rq_sel
+        form = Q.lib().moe_w4a4_grouped_gemm_residual_form(R, 2 * I, H, E, Ks, Q.QD_EPI_SWIGLU)
+        dense = name.startswith("tile_rac_dense") or name == "tile_rac_all"
+        assert form == (1 if dense else 2)
     gu, _ = ops.grouped_gemm(xq, w13, R, row_token, offs, rq if Ks else None,
                              sel if Ks else None, Q.QD_EPI_NONE)
     ref_gu, mag_gu = OL.w13_stage(act["xq"], act["rq"] if Ks else None, perm["row_token"],
@@ -195,6 +210,8 @@ W2RAC = [
      dict(routing="zipf", acts="student_t3", edge_cases=True, outlier_frac=0.0)),
     # many rows per expert at W2 (the tile kernel with the compact residual)
     ("w2rac_prefill_tile", 512, 256, 2, 2, 256, 8, 24, {}),
+    # K_s2 = I/2 at W2 with many rows: the tile kernel's dense residual pass
+    ("w2rac_prefill_dense", 512, 256, 2, 2, 1024, 8, 512, {}),
 ]
 
 
@@ -238,9 +255,11 @@ def test_layer_w2_site_rac(case):
     assert torch.equal(v["hq_codes"], hq_g.codes[0])
     assert torch.equal(v["h_scores"], sc_g)
     assert torch.equal(v["sel2"], sel_g)
-    # the W2 residual: in full, or compacted to S for the tile kernel (many
-    # rows per expert, I and H multiples of 128, I >= 256)
-    tile_w2 = R > E * 48 and I >= 256 and I % 128 == 0 and H % 128 == 0
+    # the W2 residual: in full, or compacted to S where the tile kernel takes
+    # it in that form (many rows per expert, I and H multiples of 128,
+    # I >= 256, K_s2 small enough for the compact table)
+    tile_w2 = Q.lib().moe_w4a4_grouped_gemm_residual_form(R, H, I, E, Ks2, Q.QD_EPI_NONE) == 2
+    assert tile_w2 == (name == "w2rac_prefill_tile")
     if tile_w2:
         assert torch.equal(v["hr_sel"], ops.gather_selected(hr_g, sel_g))
     else:
@@ -435,14 +454,17 @@ def test_empty_batch():
 
 FULL = [
     # workload, token count (None: the workload's), experts with real weights
-    # ("all": every expert that receives a row; "sampled": three of them)
-    ("moe_decode_t256_h2048", None, "all"),
-    ("moe_zipf_decode_t64_h4096", None, "all"),
-    ("moe_prefill_t8192_h2048", None, "sampled"),
-    ("moe_prefill_t4096_h4096", None, "sampled"),
+    # ("all": every expert that receives a row; "sampled": three of them),
+    # K_s (None: the workload's)
+    ("moe_decode_t256_h2048", None, "all", None),
+    ("moe_zipf_decode_t64_h4096", None, "all", None),
+    ("moe_prefill_t8192_h2048", None, "sampled", None),
+    ("moe_prefill_t4096_h4096", None, "sampled", None),
     # a single token (single-sequence decode) at the decode workloads' sizes
-    ("moe_decode_t256_h2048", 1, "all"),
-    ("moe_zipf_decode_t64_h4096", 1, "all"),
+    ("moe_decode_t256_h2048", 1, "all", None),
+    ("moe_zipf_decode_t64_h4096", 1, "all", None),
+    # K_s = H/2 on the prefill workload (the tile kernel's dense residual pass)
+    ("moe_prefill_t8192_h2048", None, "sampled", 1024),
 ]
 
 
@@ -453,9 +475,10 @@ def _sampled_experts(counts):
     return sorted({int(order[-1]), int(order[0]), int(order[len(order) // 2])})
 
 
-@pytest.mark.parametrize("name,T,which", FULL,
-                         ids=[f"{n}-T{T or 'full'}-{w}" for n, T, w in FULL])
-def test_full_size(name, T, which):
+@pytest.mark.parametrize("name,T,which,ks", FULL,
+                         ids=[f"{n}-T{T or 'full'}-{w}" + (f"-ks{ks}" if ks else "")
+                              for n, T, w, ks in FULL])
+def test_full_size(name, T, which, ks):
     """A MoE workload at its full size (or a single token at its sizes)
     through the whole-layer call the benchmark times (same shapes, hence the
     same kernels and grids).
@@ -479,7 +502,7 @@ def test_full_size(name, T, which):
     zero_e = next((e for e in range(wl.E) if e not in S), None)
     inp = synth.generate(name, T=T, experts=S)
     T = inp.x.shape[0]
-    H, E, k, I, Ks = wl.H, wl.E, wl.k, wl.I, wl.Ks
+    H, E, k, I, Ks = wl.H, wl.E, wl.k, wl.I, (wl.Ks if ks is None else ks)
     R = T * k
     print(f"{name} T={T}: {len(S)} experts with weights, rows "
           f"{sorted(int(counts[e]) for e in S)[-3:]} (largest)", flush=True)
@@ -516,7 +539,10 @@ def test_full_size(name, T, which):
     # (prefill kernel), with its tensor scale either way
     assert v["rq_gscale"].cpu().numpy().view(np.uint32).tolist() == \
         np.array([act["rq"]["s_enc"], act["rq"]["s_dec"]], np.float32).view(np.uint32).tolist()
-    if Q.lib().moe_w4a4_grouped_gemm_amax_count(R, 2 * I, H, E, Ks, Q.QD_EPI_SWIGLU) <= 1024:
+    form = Q.lib().moe_w4a4_grouped_gemm_residual_form(R, 2 * I, H, E, Ks, Q.QD_EPI_SWIGLU)
+    if ks is not None:
+        assert form == 1       # the dense residual pass reads the masked residual
+    if form == 1:
         assert_nvfp4_equal(dict(packed=v["rq_codes"].cpu().numpy(),
                                 scales=v["rq_scales"].cpu().numpy(),
                                 gscale=v["rq_gscale"].cpu().numpy()), act["rq"], "rq")
