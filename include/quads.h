@@ -524,6 +524,48 @@ qd_status qd_moe_layer_views(int64_t T, int64_t H, int32_t E, int32_t k, int64_t
                              int64_t *off /* host, QD_VIEW_COUNT */);
 
 /* ---------------------------------------------------------------------
+ * qd_moe_block_forward -- the layer fed straight from the transformer's
+ * hidden state: RMSNorm and the router folded into the layer's first launch
+ * (the MoE block of Sec. 4.1's model; the paper names neither step, the
+ * readings are: x = bf16(h / sqrt(mean_j h_j^2 + eps) * gamma), logits =
+ * f32(x w_router^T)).  One pass over h gives x, the router logits (bf16
+ * MFMAs, f32 accumulation), the top-k routing and the amax partials of x;
+ * the rest is qd_moe_layer_forward on that x and those logits, bit for bit.
+ *   h        : bf16 [T][H] (the hidden state before the norm);
+ *   gamma    : bf16 [H] (the norm's gain); eps >= 0 (finite);
+ *   w_router : bf16 [E][H] (row-major, one row per expert); E <= 256;
+ *   other arguments as qd_moe_layer_forward; ws at least
+ *   qd_moe_block_workspace(T, H, E, k, I) bytes (the layer's workspace, then
+ *   x bf16 [T][H] and the logits f32 [T][E] at the offsets
+ *   qd_moe_block_views gives in off[QD_BLOCK_VIEW_X] and
+ *   off[QD_BLOCK_VIEW_LOGITS]; off has QD_BLOCK_VIEW_COUNT entries, the
+ *   first QD_VIEW_COUNT as qd_moe_layer_views).
+ * x and the logits are float32 arithmetic on the GPU (squares summed per
+ * lane, then across the wave; 1 / sqrt correctly rounded): within one bf16
+ * ulp of the float64 reading for x, and within float32 accumulation error
+ * for the logits.
+ * Errors: as qd_moe_layer_forward; QD_ERR_UNSUPPORTED for E > 256;
+ * QD_ERR_SHAPE for a negative or non-finite eps.
+ * ------------------------------------------------------------------- */
+enum { QD_BLOCK_VIEW_X = QD_VIEW_COUNT, QD_BLOCK_VIEW_LOGITS, QD_BLOCK_VIEW_COUNT };
+size_t    qd_moe_block_workspace(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I);
+qd_status qd_moe_block_views(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I,
+                             int64_t *off /* host, QD_BLOCK_VIEW_COUNT */);
+qd_status qd_moe_block_forward(const void *h, const void *gamma, float eps, const void *w_router,
+                               int64_t T, int64_t H, int32_t E, int32_t k, int64_t I, int32_t Ks,
+                               int32_t Ks2, int32_t renorm, const qd_nvfp4 *w13,
+                               const qd_nvfp4 *w2, void *y, void *ws, size_t ws_bytes,
+                               void *stream);
+/* the same with stage events as qd_moe_layer_forward_timed (ROUTE holds the
+ * norm, the router and the top-k) */
+qd_status qd_moe_block_forward_timed(const void *h, const void *gamma, float eps,
+                                     const void *w_router, int64_t T, int64_t H, int32_t E,
+                                     int32_t k, int64_t I, int32_t Ks, int32_t Ks2,
+                                     int32_t renorm, const qd_nvfp4 *w13, const qd_nvfp4 *w2,
+                                     void *y, void *ws, size_t ws_bytes, void *const *events,
+                                     void *stream);
+
+/* ---------------------------------------------------------------------
  * qd_moe_layer_forward_noalloc -- qd_moe_layer_forward without a caller
  * workspace, for callers that cannot allocate device memory: code under
  * HIP graph capture, serving loops and harnesses that forbid hipMalloc.

@@ -9,6 +9,8 @@
 
 namespace {
 
+using namespace qd;
+
 // The steps before the W13 GEMM form two independent chains -- routing
 // (top-k, ranks, scatter) and X (amax, quantise + RAC scores, channel
 // select) -- so each launch below runs one step of each chain side by side
@@ -24,6 +26,144 @@ __global__ __launch_bounds__(256) void layer_pre1_kernel(
   const int b = blockIdx.x;
   if (b < ntopk) qdr::route_topk_body(b, logits, T, E, k, renorm, ids, wts);
   else qdq::amax_partial_body<uint16_t>(b - ntopk, ga, x, n16, part, scores, scores ? H : 0, ramax);
+}
+
+// ---- The block's input path folded ahead of the layer: RMSNorm of the
+// hidden state h, the router logits of the normalised state, top-k and the
+// amax partials of the normalised state, in one pass over h (it replaces
+// layer_pre1_kernel, and a separate normalisation and router launch with
+// their round trip of x).  Token blocks of 32 rows: per block, 1/RMS per row
+// (wave w: rows 8 w .. 8 w + 7), then per 128-column chunk the normalised
+// bf16 values go to x and to LDS, and the router contraction runs on bf16
+// MFMAs (32 tokens x 32 experts per 32x32x16 step: wave w takes expert
+// blocks w and w + 4, so E <= 256); the logits go out, and each wave takes
+// the top-k of four of the block's tokens in turn.
+constexpr int kBlkTok = 32;
+constexpr int kBlkKC = 128;
+constexpr int kBlkXS = kBlkKC + 8;     // LDS row stride of a chunk (bf16)
+constexpr int kBlkMaxE = 256;
+
+typedef __bf16 blk_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float blk_f32x16 __attribute__((ext_vector_type(16)));
+
+template <int PER>
+__global__ __launch_bounds__(256) void block_pre0_kernel(
+    const uint16_t *__restrict__ hin, const uint16_t *__restrict__ gamma, float eps,
+    const uint16_t *__restrict__ wr, int64_t T, int64_t H, int E, int k, int renorm,
+    uint16_t *__restrict__ x, float *__restrict__ logits, int32_t *__restrict__ ids,
+    float *__restrict__ wts, float *__restrict__ part, uint64_t *__restrict__ scores,
+    float *__restrict__ ramax) {
+  __shared__ __align__(16) uint16_t xs[kBlkTok * kBlkXS];
+  __shared__ float rinv[kBlkTok];
+  __shared__ float red[16];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int64_t ntb = (T + kBlkTok - 1) / kBlkTok;
+  const int neb = (E + 31) >> 5;
+  float m = 0.0f;
+  for (int64_t tb = blockIdx.x; tb < ntb; tb += gridDim.x) {
+    const int64_t t0 = tb * kBlkTok;
+    const int nt = (int)(T - t0 < kBlkTok ? T - t0 : kBlkTok);
+    // 1 / RMS: squares summed per lane over its 8-column pieces, then across
+    // the wave
+    for (int j = 8 * w; j < 8 * w + 8 && j < nt; ++j) {
+      const uint16_t *hr = hin + (t0 + j) * H;
+      float ss = 0.0f;
+      for (int64_t c = 8 * lane; c < H; c += 512) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(hr + c);
+        const uint32_t q[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float a = bf16_bits_to_f32(q[i] & 0xFFFFu), b = bf16_bits_to_f32(q[i] >> 16);
+          ss += a * a;
+          ss += b * b;
+        }
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+      if (lane == 0) rinv[j] = 1.0f / sqrtf(ss / (float)H + eps);
+    }
+    __syncthreads();
+    blk_f32x16 acc[2];
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[bi][q] = 0.0f;
+    for (int64_t kc = 0; kc < H; kc += kBlkKC) {
+      const int kw = (int)(H - kc < kBlkKC ? H - kc : kBlkKC);   // a multiple of 16
+      // x = bf16((h * (1 / RMS)) * gamma) for the chunk; rows past the
+      // batch and columns past H are zero in LDS
+      for (int q = tid; q < kBlkTok * (kBlkKC / 8); q += 256) {
+        const int j = q >> 4, c8 = (q & 15) * 8;
+        uint32_t o[4] = {0u, 0u, 0u, 0u};
+        if (j < nt && c8 < kw) {
+          const uint4 hv = *reinterpret_cast<const uint4 *>(hin + (t0 + j) * H + kc + c8);
+          const uint4 gv = *reinterpret_cast<const uint4 *>(gamma + kc + c8);
+          const uint32_t hq[4] = {hv.x, hv.y, hv.z, hv.w}, gq[4] = {gv.x, gv.y, gv.z, gv.w};
+          const float r = rinv[j];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const uint32_t lo = f32_to_bf16_bits(
+                (bf16_bits_to_f32(hq[i] & 0xFFFFu) * r) * bf16_bits_to_f32(gq[i] & 0xFFFFu));
+            const uint32_t hi = f32_to_bf16_bits(
+                (bf16_bits_to_f32(hq[i] >> 16) * r) * bf16_bits_to_f32(gq[i] >> 16));
+            m = fmaxf(m, fmaxf(fabsf(bf16_bits_to_f32(lo)), fabsf(bf16_bits_to_f32(hi))));
+            o[i] = lo | (hi << 16);
+          }
+          *reinterpret_cast<uint4 *>(x + (t0 + j) * H + kc + c8) = make_uint4(o[0], o[1], o[2], o[3]);
+        }
+        *reinterpret_cast<uint4 *>(xs + j * kBlkXS + c8) = make_uint4(o[0], o[1], o[2], o[3]);
+      }
+      __syncthreads();
+      // router: lane l holds token row l % 32 of x and expert row l % 32 of
+      // the block, columns 8 (l / 32) .. + 7 of each 16-column step
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi) {
+        const int eb = w + 4 * bi;
+        if (eb < neb) {
+          const int e = 32 * eb + (lane & 31);
+          const bool ev = e < E;
+          const uint16_t *wrow = wr + (int64_t)(ev ? e : 0) * H + kc + 8 * (lane >> 5);
+          const uint16_t *xrow = xs + (lane & 31) * kBlkXS + 8 * (lane >> 5);
+          for (int kk = 0; kk < kw; kk += 16) {
+            const uint4 av = *reinterpret_cast<const uint4 *>(xrow + kk);
+            uint4 bv = *reinterpret_cast<const uint4 *>(wrow + kk);
+            if (!ev) bv = make_uint4(0u, 0u, 0u, 0u);
+            acc[bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(blk_bf16x8, av),
+                                                             __builtin_bit_cast(blk_bf16x8, bv),
+                                                             acc[bi], 0, 0, 0);
+          }
+        }
+      }
+      __syncthreads();
+    }
+    // logits: lane l holds expert 32 eb + l % 32 for token rows
+    // 8 (q / 4) + 4 (l / 32) + q % 4
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+      const int e = 32 * (w + 4 * bi) + (lane & 31);
+      if (w + 4 * bi < neb && e < E) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int j = 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+          if (j < nt) logits[(t0 + j) * E + e] = acc[bi][q];
+        }
+      }
+    }
+    __syncthreads();
+    // top-k: wave w takes tokens t0 + 4 i + w (the wave routing body, same
+    // arithmetic as the layer's)
+#pragma unroll 1
+    for (int i = 0; i < kBlkTok / 4; ++i)
+      qdr::route_topk_wave_body<PER>((int)(tb * (kBlkTok / 4) + i), logits, T, E, k, renorm, ids,
+                                     wts);
+  }
+  // the RAC accumulators the quantiser that follows adds into
+  if (scores)
+    for (int64_t i = (int64_t)blockIdx.x * 256 + tid; i < H; i += (int64_t)gridDim.x * 256)
+      scores[i] = 0ull;
+  if (ramax && blockIdx.x == 0 && tid == 0) ramax[0] = 0.0f;
+  m = block_max(m, red);
+  if (tid == 0) part[blockIdx.x] = m;
 }
 
 // routing ranks (nr workgroups) | X quantiser (+ RAC scores) on a (gx, gy) grid
@@ -123,6 +263,9 @@ __global__ __launch_bounds__(qdc::kRankSelThreads) void layer_pre3r_kernel(
 struct Layout {
   int64_t off[QD_VIEW_COUNT];
   int64_t route_ws, q1_ws, sel_ws, q2_ws, sel2_ws, total;
+  // the block entry point's extra views after the layer's workspace: the
+  // normalised state x and the router logits
+  int64_t xn, lg, block_total;
 };
 
 Layout make_layout(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I) {
@@ -179,6 +322,9 @@ Layout make_layout(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I) {
   put(QD_VIEW_HR_GSCALE, 8);
   put(QD_VIEW_HR_SEL, R * (int64_t)rac_selected_width((int32_t)I) * 2);
   L.total = o;
+  L.xn = blob(T * H * 2);
+  L.lg = blob(T * (int64_t)E * 4);
+  L.block_total = o;
   return L;
 }
 
@@ -207,12 +353,18 @@ extern "C" qd_status qd_moe_layer_forward(const void *x, const float *logits, in
                                     ws_bytes, nullptr, stream);
 }
 
-extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logits, int64_t T,
-                                                int64_t H, int32_t E, int32_t k, int64_t I,
-                                                int32_t Ks, int32_t Ks2, int32_t renorm,
-                                                const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y,
-                                                void *ws, size_t ws_bytes,
-                                                void *const *events, void *stream) {
+namespace {
+
+// the block entry point's input path (RMSNorm + router ahead of the layer)
+struct BlockIn {
+  const void *h, *gamma, *w_router;
+  float eps;
+};
+
+qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, int32_t E,
+                     int32_t k, int64_t I, int32_t Ks, int32_t Ks2, int32_t renorm,
+                     const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y, void *ws, size_t ws_bytes,
+                     void *const *events, void *stream, const BlockIn *blk) {
   if (!w13 || !w2) return QD_ERR_NULL;
   if (T < 0 || H <= 0 || H % 16 || I <= 0 || I % 16 || E < 1 || k < 1 || k > E) return QD_ERR_SHAPE;
   if (Ks < 0 || Ks > H || Ks2 < 0 || Ks2 > I) return QD_ERR_SHAPE;
@@ -223,15 +375,25 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   if (st) return st;
   st = qdh::check_nvfp4(w2, E, H, I);
   if (st) return st;
+  if (blk && E > kBlkMaxE) return QD_ERR_UNSUPPORTED;
   if (T == 0) return QD_OK;
-  if (!x || !logits || !y) return QD_ERR_NULL;
+  if (blk ? (!blk->h || !blk->gamma || !blk->w_router || !y) : (!x || !logits || !y))
+    return QD_ERR_NULL;
+  if (blk && !(blk->eps >= 0.0f && blk->eps < INFINITY)) return QD_ERR_SHAPE;
   if (!ws) return QD_ERR_WORKSPACE;
   Layout L = make_layout(T, H, E, k, I);
-  if (ws_bytes < (size_t)L.total) return QD_ERR_WORKSPACE;
-  if (!qdh::aligned16(ws) || !qdh::aligned16(x) || !qdh::aligned16(y) || !qdh::aligned16(logits))
+  if (ws_bytes < (size_t)(blk ? L.block_total : L.total)) return QD_ERR_WORKSPACE;
+  if (!qdh::aligned16(ws) || !qdh::aligned16(y)) return QD_ERR_ALIGN;
+  if (blk ? (!qdh::aligned16(blk->h) || !qdh::aligned16(blk->gamma) ||
+             !qdh::aligned16(blk->w_router))
+          : (!qdh::aligned16(x) || !qdh::aligned16(logits)))
     return QD_ERR_ALIGN;
   if (qdh::fault_injected()) return QD_ERR_HIP;
   char *b = static_cast<char *>(ws);
+  if (blk) {
+    x = b + L.xn;
+    logits = reinterpret_cast<const float *>(b + L.lg);
+  }
   auto P = [&](int idx) { return b + L.off[idx]; };
   const int64_t R = T * k;
   auto mark = [&](int i) {
@@ -280,17 +442,37 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   qdq::quant_grid(T, H, rac, gx, gy);
 
   mark(QD_STAGE_ROUTE);
-  hipLaunchKernelGGL(layer_pre1_kernel, dim3((unsigned)(ntopk + ga)), dim3(256), 0, s, logits, T,
-                     E, k, renorm, ids, wts, ntopk, x, n16, part, ga, rac ? scores : nullptr, H,
-                     rac ? ramax : nullptr);
+  int np = ga;      // amax partials of X
+  if (blk) {
+    const int64_t ntb = (T + kBlkTok - 1) / kBlkTok;
+    np = (int)(ntb < qdq::kAmaxPartials ? ntb : qdq::kAmaxPartials);
+    auto pre0 = block_pre0_kernel<4>;
+    switch ((E + 63) >> 6) {
+      case 1: pre0 = block_pre0_kernel<1>; break;
+      case 2: pre0 = block_pre0_kernel<2>; break;
+      case 3: pre0 = block_pre0_kernel<3>; break;
+      default: break;
+    }
+    hipLaunchKernelGGL(pre0, dim3((unsigned)np), dim3(256), 0, s,
+                       static_cast<const uint16_t *>(blk->h),
+                       static_cast<const uint16_t *>(blk->gamma), blk->eps,
+                       static_cast<const uint16_t *>(blk->w_router), T, H, E, k, renorm,
+                       static_cast<uint16_t *>(const_cast<void *>(x)),
+                       const_cast<float *>(logits), ids, wts, part, rac ? scores : nullptr,
+                       rac ? ramax : nullptr);
+  } else {
+    hipLaunchKernelGGL(layer_pre1_kernel, dim3((unsigned)(ntopk + ga)), dim3(256), 0, s, logits,
+                       T, E, k, renorm, ids, wts, ntopk, x, n16, part, ga,
+                       rac ? scores : nullptr, H, rac ? ramax : nullptr);
+  }
   mark(QD_STAGE_QUANT_X);
   if (rac)
     hipLaunchKernelGGL(layer_pre2_kernel<true>, dim3((unsigned)(nr + gx * gy)), dim3(256), 0, s,
-                       T, E, k, ids, counts, ranks, nr, x, H, part, ga, xq.codes, xq.scales,
+                       T, E, k, ids, counts, ranks, nr, x, H, part, np, xq.codes, xq.scales,
                        xq.gscale, scores, ramax, gx, gy);
   else
     hipLaunchKernelGGL(layer_pre2_kernel<false>, dim3((unsigned)(nr + gx * gy)), dim3(256), 0, s,
-                       T, E, k, ids, counts, ranks, nr, x, H, part, ga, xq.codes, xq.scales,
+                       T, E, k, ids, counts, ranks, nr, x, H, part, np, xq.codes, xq.scales,
                        xq.gscale, nullptr, nullptr, gx, gy);
   mark(QD_STAGE_SELECT);
   if (rac) {
@@ -423,4 +605,53 @@ extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logi
   if (st) return st;
   mark(QD_STAGE_COUNT);
   return qdh::check_launch();
+}
+
+}  // namespace
+
+extern "C" qd_status qd_moe_layer_forward_timed(const void *x, const float *logits, int64_t T,
+                                                int64_t H, int32_t E, int32_t k, int64_t I,
+                                                int32_t Ks, int32_t Ks2, int32_t renorm,
+                                                const qd_nvfp4 *w13, const qd_nvfp4 *w2, void *y,
+                                                void *ws, size_t ws_bytes,
+                                                void *const *events, void *stream) {
+  return layer_impl(x, logits, T, H, E, k, I, Ks, Ks2, renorm, w13, w2, y, ws, ws_bytes, events,
+                    stream, nullptr);
+}
+
+extern "C" size_t qd_moe_block_workspace(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I) {
+  if (T < 0 || H <= 0 || E < 1 || k < 1 || I <= 0) return 0;
+  return (size_t)make_layout(T, H, E, k, I).block_total;
+}
+
+extern "C" qd_status qd_moe_block_views(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I,
+                                        int64_t *off) {
+  if (!off) return QD_ERR_NULL;
+  if (T < 0 || H <= 0 || E < 1 || k < 1 || I <= 0) return QD_ERR_SHAPE;
+  Layout L = make_layout(T, H, E, k, I);
+  for (int i = 0; i < QD_VIEW_COUNT; ++i) off[i] = L.off[i];
+  off[QD_BLOCK_VIEW_X] = L.xn;
+  off[QD_BLOCK_VIEW_LOGITS] = L.lg;
+  return QD_OK;
+}
+
+extern "C" qd_status qd_moe_block_forward_timed(const void *h, const void *gamma, float eps,
+                                                const void *w_router, int64_t T, int64_t H,
+                                                int32_t E, int32_t k, int64_t I, int32_t Ks,
+                                                int32_t Ks2, int32_t renorm, const qd_nvfp4 *w13,
+                                                const qd_nvfp4 *w2, void *y, void *ws,
+                                                size_t ws_bytes, void *const *events,
+                                                void *stream) {
+  const BlockIn blk{h, gamma, w_router, eps};
+  return layer_impl(nullptr, nullptr, T, H, E, k, I, Ks, Ks2, renorm, w13, w2, y, ws, ws_bytes,
+                    events, stream, &blk);
+}
+
+extern "C" qd_status qd_moe_block_forward(const void *h, const void *gamma, float eps,
+                                          const void *w_router, int64_t T, int64_t H, int32_t E,
+                                          int32_t k, int64_t I, int32_t Ks, int32_t Ks2,
+                                          int32_t renorm, const qd_nvfp4 *w13, const qd_nvfp4 *w2,
+                                          void *y, void *ws, size_t ws_bytes, void *stream) {
+  return qd_moe_block_forward_timed(h, gamma, eps, w_router, T, H, E, k, I, Ks, Ks2, renorm, w13,
+                                    w2, y, ws, ws_bytes, nullptr, stream);
 }

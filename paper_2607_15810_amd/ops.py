@@ -342,6 +342,60 @@ class MoELayer:
         )
 
 
+class MoEBlock(MoELayer):
+    """The layer fed from the hidden state through qd_moe_block_forward:
+    RMSNorm (gamma, eps) and the router (w_router [E][H] bf16) folded into
+    the layer's first launch; `views()` adds x (the normalised state) and the
+    router logits."""
+
+    def __init__(self, w13, w2, T, k, Ks, gamma, w_router, eps=1e-6, renorm=True, Ks2=0):
+        import ctypes
+        self.w13, self.w2 = w13, w2
+        self.E = w13.groups
+        self.I = w13.rows // 2
+        self.H = w13.cols
+        self.T, self.k, self.Ks, self.Ks2, self.renorm = T, k, Ks, Ks2, renorm
+        _require_cuda(gamma, w_router)
+        if gamma.dtype != torch.bfloat16 or w_router.dtype != torch.bfloat16:
+            raise TypeError("gamma and w_router must be bfloat16")
+        self.gamma = gamma.contiguous()
+        self.w_router = w_router.contiguous()
+        self.eps = float(eps)
+        n = Q.lib().qd_moe_block_workspace(T, self.H, self.E, k, self.I)
+        self.ws = _ws(n, w13.codes.device)
+        off = (ctypes.c_int64 * (len(Q.VIEW_NAMES) + 2))()
+        Q.call("qd_moe_block_views", T, self.H, self.E, k, self.I, off)
+        self.off = list(off)
+        self._s13 = w13.struct()
+        self._s2 = w2.struct()
+
+    def __call__(self, h, y=None, events=None):
+        import ctypes
+        _require_cuda(h)
+        if h.dtype != torch.bfloat16:
+            raise TypeError("h must be bfloat16")
+        h = h.contiguous()
+        if y is None:
+            y = torch.empty((self.T, self.H), dtype=torch.bfloat16, device=h.device)
+        evp = None
+        if events is not None:
+            evp = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+        Q.call("qd_moe_block_forward_timed", h.data_ptr(), self.gamma.data_ptr(), self.eps,
+               self.w_router.data_ptr(), self.T, self.H, self.E, self.k, self.I, self.Ks,
+               self.Ks2, int(self.renorm), ctypes.byref(self._s13), ctypes.byref(self._s2),
+               y.data_ptr(), self.ws.data_ptr(), self.ws.numel(), evp, _stream())
+        return y
+
+    def views(self):
+        v = super().views()
+        n = len(Q.VIEW_NAMES)
+        T, H, E = self.T, self.H, self.E
+        v["x"] = self.ws[self.off[n]:self.off[n] + T * H * 2].view(torch.bfloat16).view(T, H)
+        v["logits"] = self.ws[self.off[n + 1]:self.off[n + 1] + T * E * 4].view(
+            torch.float32).view(T, E)
+        return v
+
+
 class MoELayerPerExpert:
     """The layer with one RAC channel set per expert at the W13 input
     (qd_moe_layer_forward_per_expert), with a reusable workspace."""

@@ -114,6 +114,16 @@ SIGNATURES = {
                                            c_void_p, c_void_p, c_size_t, c_void_p, c_void_p]),
     "qd_moe_layer_views": (c_int, [c_int64, c_int64, c_int32, c_int32, c_int64,
                                    POINTER(c_int64)]),
+    "qd_moe_block_workspace": (c_size_t, [c_int64, c_int64, c_int32, c_int32, c_int64]),
+    "qd_moe_block_views": (c_int, [c_int64, c_int64, c_int32, c_int32, c_int64,
+                                   POINTER(c_int64)]),
+    "qd_moe_block_forward": (c_int, [c_void_p, c_void_p, ctypes.c_float, c_void_p, c_int64,
+                                     c_int64, c_int32, c_int32, c_int64, c_int32, c_int32,
+                                     c_int32, PN, PN, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "qd_moe_block_forward_timed": (c_int, [c_void_p, c_void_p, ctypes.c_float, c_void_p,
+                                           c_int64, c_int64, c_int32, c_int32, c_int64, c_int32,
+                                           c_int32, c_int32, PN, PN, c_void_p, c_void_p,
+                                           c_size_t, c_void_p, c_void_p]),
     "qd_moe_layer_per_expert_workspace": (c_size_t, [c_int64, c_int64, c_int32, c_int32,
                                                      c_int64, c_int32]),
     "qd_moe_layer_forward_per_expert": (c_int, [c_void_p, c_void_p, c_int64, c_int64, c_int32,

@@ -220,3 +220,14 @@ def small_moe(name, T, H, E, k, I, Ks, seed=0, acts="normal", routing="normal",
     w13 = make_bank(s_w13, E, 2 * I, H, wl.w_std)
     w2 = make_bank(s_w2, E, H, I, wl.w_std)
     return Inputs(wl, x, logits=logits, w13=w13, w2=w2)
+
+
+def block_params(H, E, seed=0, gamma_std=0.1, router_std=0.02):
+    """The block input path's parameters: the RMSNorm gain gamma [H] (about
+    1, N(1, gamma_std)) and the router weights [E][H] (N(0, router_std)),
+    both bf16, from their own seeded stream (the hidden state h is drawn
+    like a workload's activations)."""
+    rng = np.random.default_rng(np.random.SeedSequence([BASE_SEED, 7919, seed, H, E]))
+    gamma = to_bf16(1.0 + gamma_std * rng.standard_normal(H))
+    w_router = to_bf16(router_std * rng.standard_normal((E, H)))
+    return gamma, w_router

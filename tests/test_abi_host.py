@@ -305,3 +305,40 @@ def test_per_expert_validation(lib):
               FAKE, 16, None) == Q.QD_ERR_WORKSPACE
     assert lw(None, None, 0, 256, 4, 2, 128, 8, 1, ctypes.byref(w13), ctypes.byref(w2), None,
               None, 0, None) == Q.QD_OK                       # empty batch
+
+
+def test_block_validation(lib):
+    """The block entry point (RMSNorm + router folded ahead of the layer):
+    argument checks before any launch, and its workspace and views."""
+    T, H, E, k, I = 64, 256, 4, 2, 128
+    n = lib.qd_moe_block_workspace(T, H, E, k, I)
+    assert n > lib.qd_moe_layer_workspace(T, H, E, k, I) + T * H * 2
+    off = (ctypes.c_int64 * (len(Q.VIEW_NAMES) + 2))()
+    assert lib.qd_moe_block_views(T, H, E, k, I, off) == Q.QD_OK
+    lo = (ctypes.c_int64 * len(Q.VIEW_NAMES))()
+    assert lib.qd_moe_layer_views(T, H, E, k, I, lo) == Q.QD_OK
+    assert list(off)[:len(Q.VIEW_NAMES)] == list(lo)
+    nv = len(Q.VIEW_NAMES)
+    assert off[nv] >= lib.qd_moe_layer_workspace(T, H, E, k, I)
+    assert off[nv + 1] >= off[nv] + T * H * 2 and off[nv + 1] + T * E * 4 <= n
+    w13 = _nv(E, 2 * I, H, FAKE)
+    w2 = _nv(E, H, I, FAKE)
+    b = lambda *x: Q.raw("qd_moe_block_forward", *x)
+    # (h, gamma, eps, w_router, T, H, E, k, I, Ks, Ks2, renorm, w13, w2, y, ws, ws_bytes, stream)
+    assert b(FAKE, FAKE, ctypes.c_float(1e-6), None, T, H, E, k, I, 8, 0, 1, ctypes.byref(w13),
+             ctypes.byref(w2), FAKE, FAKE, n, None) == Q.QD_ERR_NULL     # no router
+    assert b(FAKE, FAKE, ctypes.c_float(-1.0), FAKE, T, H, E, k, I, 8, 0, 1, ctypes.byref(w13),
+             ctypes.byref(w2), FAKE, FAKE, n, None) == Q.QD_ERR_SHAPE    # eps < 0
+    assert b(FAKE, FAKE, ctypes.c_float(float("inf")), FAKE, T, H, E, k, I, 8, 0, 1,
+             ctypes.byref(w13), ctypes.byref(w2), FAKE, FAKE, n, None) == Q.QD_ERR_SHAPE
+    assert b(FAKE, FAKE, ctypes.c_float(1e-6), FAKE, T, H, E, k, I, 8, 0, 1, ctypes.byref(w13),
+             ctypes.byref(w2), FAKE, FAKE, n - 16, None) == Q.QD_ERR_WORKSPACE
+    assert b(FAKE + 8, FAKE, ctypes.c_float(1e-6), FAKE, T, H, E, k, I, 8, 0, 1,
+             ctypes.byref(w13), ctypes.byref(w2), FAKE, FAKE, n, None) == Q.QD_ERR_ALIGN
+    w13b = _nv(300, 2 * I, H, FAKE)
+    w2b = _nv(300, H, I, FAKE)
+    assert b(FAKE, FAKE, ctypes.c_float(1e-6), FAKE, T, H, 300, k, I, 8, 0, 1,
+             ctypes.byref(w13b), ctypes.byref(w2b), FAKE, FAKE, 1 << 40,
+             None) == Q.QD_ERR_UNSUPPORTED                               # E > 256
+    assert b(None, None, ctypes.c_float(1e-6), None, 0, H, E, k, I, 8, 0, 1, ctypes.byref(w13),
+             ctypes.byref(w2), None, None, 0, None) == Q.QD_OK          # empty batch
