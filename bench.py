@@ -478,7 +478,9 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
     routing and shapes, per-token / per-channel E4M3, no residual), the
     MXFP4 W4A4 layer (the hardware's native FP4 format, no residual), the
     plain NVFP4 W4A4 layer (K_s = 0), RAC at K_s = 50% of the channels, RAC
-    at both the W13 and the W2 inputs, and the trainer-side W4A16 forward."""
+    at both the W13 and the W2 inputs, per-expert channel sets, the block
+    entry point with RMSNorm and router folded in, and the trainer-side
+    W4A16 forward."""
     import torch
     from paper_2607_15810_amd import ops
     dev = "cuda"
@@ -529,6 +531,32 @@ def comparisons(args, wl, inp, banks, xs, lgs, ms_step, ws):
                                       value=round(wl.T / (mspe * 1e-3), 1), unit="tokens/s",
                                       rac_channels=wl.Ks,
                                       time_vs_headline=round(mspe / ms_step, 3))
+    # the block input path: RMSNorm and the router folded into the layer's
+    # first launch (qd_moe_block_forward, the workload's activations as the
+    # hidden state) against the same steps as separate launches (torch's
+    # RMSNorm arithmetic and bf16 router product, then the layer)
+    from paper_2607_15810_amd import synth
+    gamma, w_r = synth.block_params(wl.H, wl.E, seed=wl.index)
+    gamma, w_r = gamma.to(dev), w_r.to(dev)
+    w_rt = w_r.t().contiguous()
+    gf = gamma.float()
+    blks = [ops.MoEBlock(b13, b2, wl.T, wl.k, wl.Ks, gamma, w_r) for b13, b2 in banks]
+    msb = time_steps([lambda c=c: blks[c](xs[c], y) for c in range(len(blks))], steps, warm)
+    lays = [ops.MoELayer(b13, b2, wl.T, wl.k, wl.Ks, ws=ws) for b13, b2 in banks]
+
+    def unfused(c):
+        hf = xs[c].float()
+        xn = (hf * torch.rsqrt(hf.pow(2).mean(-1, keepdim=True) + 1e-6) * gf).to(torch.bfloat16)
+        lg = torch.mm(xn, w_rt).float()
+        lays[c](xn, lg, y)
+
+    msu = time_steps([lambda c=c: unfused(c) for c in range(len(lays))], steps, warm)
+    res["block_norm_router_fused"] = dict(ms_per_step=round(msb, 5),
+                                          value=round(wl.T / (msb * 1e-3), 1), unit="tokens/s",
+                                          unfused_ms_per_step=round(msu, 5),
+                                          speedup_vs_unfused=round(msu / msb, 3),
+                                          time_vs_headline=round(msb / ms_step, 3))
+    del blks, lays
     # the trainer-side forward on the same weights (Sec. 3.2: bf16
     # activations, fake-quantised NVFP4 weights, no activation quantiser)
     lay16 = [ops.W4A16MoELayer(b13, b2, wl.k) for b13, b2 in banks]

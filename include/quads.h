@@ -544,7 +544,8 @@ qd_status qd_moe_layer_views(int64_t T, int64_t H, int32_t E, int32_t k, int64_t
  * lane, then across the wave; 1 / sqrt correctly rounded): within one bf16
  * ulp of the float64 reading for x, and within float32 accumulation error
  * for the logits.
- * Errors: as qd_moe_layer_forward; QD_ERR_UNSUPPORTED for E > 256;
+ * Errors: as qd_moe_layer_forward; QD_ERR_UNSUPPORTED for E > 256 or
+ * H > 9208 (eight normalised rows must fit 144 KiB of LDS);
  * QD_ERR_SHAPE for a negative or non-finite eps.
  * ------------------------------------------------------------------- */
 enum { QD_BLOCK_VIEW_X = QD_VIEW_COUNT, QD_BLOCK_VIEW_LOGITS, QD_BLOCK_VIEW_COUNT };

@@ -32,40 +32,49 @@ __global__ __launch_bounds__(256) void layer_pre1_kernel(
 // hidden state h, the router logits of the normalised state, top-k and the
 // amax partials of the normalised state, in one pass over h (it replaces
 // layer_pre1_kernel, and a separate normalisation and router launch with
-// their round trip of x).  Token blocks of 32 rows: per block, 1/RMS per row
-// (wave w: rows 8 w .. 8 w + 7), then per 128-column chunk the normalised
-// bf16 values go to x and to LDS, and the router contraction runs on bf16
-// MFMAs (32 tokens x 32 experts per 32x32x16 step: wave w takes expert
-// blocks w and w + 4, so E <= 256); the logits go out, and each wave takes
-// the top-k of four of the block's tokens in turn.
-constexpr int kBlkTok = 32;
-constexpr int kBlkKC = 128;
-constexpr int kBlkXS = kBlkKC + 8;     // LDS row stride of a chunk (bf16)
+// their round trip of x).  Token blocks of TOK rows (8, 16 or 32: the
+// largest that leaves the chip 256 blocks and fits LDS): 1/RMS per row
+// (wave w: rows TOK/4 w ..), then the block's normalised bf16 rows go to x
+// and to LDS whole, then the router contraction on bf16 MFMAs (32 token
+// rows, zero past TOK, x 32 experts per 32x32x16 step; wave w takes expert
+// blocks w and w + 4, so E <= 256), its router weights streamed in groups
+// of steps with the next group in flight during the current one's MFMAs;
+// the logits go out, and each wave takes the top-k of TOK/4 of the block's
+// tokens in turn.
 constexpr int kBlkMaxE = 256;
+constexpr int kBlkLds = 144 * 1024;    // the normalised rows of one block
 
 typedef __bf16 blk_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float blk_f32x16 __attribute__((ext_vector_type(16)));
 
-template <int PER>
+inline int64_t block_lds(int tok, int64_t H) { return (int64_t)tok * (H + 8) * 2; }
+
+template <int PER, int TOK>
 __global__ __launch_bounds__(256) void block_pre0_kernel(
     const uint16_t *__restrict__ hin, const uint16_t *__restrict__ gamma, float eps,
     const uint16_t *__restrict__ wr, int64_t T, int64_t H, int E, int k, int renorm,
     uint16_t *__restrict__ x, float *__restrict__ logits, int32_t *__restrict__ ids,
     float *__restrict__ wts, float *__restrict__ part, uint64_t *__restrict__ scores,
     float *__restrict__ ramax) {
-  __shared__ __align__(16) uint16_t xs[kBlkTok * kBlkXS];
-  __shared__ float rinv[kBlkTok];
+  static_assert(TOK == 8 || TOK == 16 || TOK == 32, "token block");
+  constexpr int NB = PER > 2 ? 2 : 1;    // expert blocks per wave
+  constexpr int G = NB == 1 ? 16 : 8;    // MFMA steps per group of loads
+  extern __shared__ __align__(16) uint16_t xs[];     // [TOK][H + 8]
+  __shared__ float rinv[TOK];
   __shared__ float red[16];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int64_t ntb = (T + kBlkTok - 1) / kBlkTok;
+  const int64_t XS = H + 8, n8 = H >> 3;
+  const int64_t ntb = (T + TOK - 1) / TOK;
   const int neb = (E + 31) >> 5;
+  const int nst = (int)(H >> 4), ngr = (nst + G - 1) / G;
   float m = 0.0f;
   for (int64_t tb = blockIdx.x; tb < ntb; tb += gridDim.x) {
-    const int64_t t0 = tb * kBlkTok;
-    const int nt = (int)(T - t0 < kBlkTok ? T - t0 : kBlkTok);
+    const int64_t t0 = tb * TOK;
+    const int nt = (int)(T - t0 < TOK ? T - t0 : TOK);
     // 1 / RMS: squares summed per lane over its 8-column pieces, then across
     // the wave
-    for (int j = 8 * w; j < 8 * w + 8 && j < nt; ++j) {
+    constexpr int RPW = TOK / 4;
+    for (int j = RPW * w; j < RPW * w + RPW && j < nt; ++j) {
       const uint16_t *hr = hin + (t0 + j) * H;
       float ss = 0.0f;
       for (int64_t c = 8 * lane; c < H; c += 512) {
@@ -83,63 +92,86 @@ __global__ __launch_bounds__(256) void block_pre0_kernel(
       if (lane == 0) rinv[j] = 1.0f / sqrtf(ss / (float)H + eps);
     }
     __syncthreads();
-    blk_f32x16 acc[2];
+    // x = bf16((h * (1 / RMS)) * gamma), to x and to LDS (rows past the
+    // batch zero in LDS)
+    const int n8i = (int)n8;
+#pragma unroll 4
+    for (int q = tid; q < TOK * n8i; q += 256) {
+      const int j = q / n8i;
+      const int c = (q - j * n8i) * 8;
+      uint32_t o[4] = {0u, 0u, 0u, 0u};
+      if (j < nt) {
+        const uint4 hv = *reinterpret_cast<const uint4 *>(hin + (t0 + j) * H + c);
+        const uint4 gv = *reinterpret_cast<const uint4 *>(gamma + c);
+        const uint32_t hq[4] = {hv.x, hv.y, hv.z, hv.w}, gq[4] = {gv.x, gv.y, gv.z, gv.w};
+        const float r = rinv[j];
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t lo = f32_to_bf16_bits(
+              (bf16_bits_to_f32(hq[i] & 0xFFFFu) * r) * bf16_bits_to_f32(gq[i] & 0xFFFFu));
+          const uint32_t hi = f32_to_bf16_bits(
+              (bf16_bits_to_f32(hq[i] >> 16) * r) * bf16_bits_to_f32(gq[i] >> 16));
+          m = fmaxf(m, fmaxf(fabsf(bf16_bits_to_f32(lo)), fabsf(bf16_bits_to_f32(hi))));
+          o[i] = lo | (hi << 16);
+        }
+        *reinterpret_cast<uint4 *>(x + (t0 + j) * H + c) = make_uint4(o[0], o[1], o[2], o[3]);
+      }
+      *reinterpret_cast<uint4 *>(xs + j * XS + c) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+    __syncthreads();
+    // router: lane l holds token row l % 32 (zero past TOK) and expert row
+    // l % 32 of its block, columns 8 (l / 32) .. + 7 of each 16-column step
+    blk_f32x16 acc[NB];
+    const uint16_t *wrow[NB];
+    bool ev[NB];
+#pragma unroll
+    for (int bi = 0; bi < NB; ++bi) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[bi][q] = 0.0f;
-    for (int64_t kc = 0; kc < H; kc += kBlkKC) {
-      const int kw = (int)(H - kc < kBlkKC ? H - kc : kBlkKC);   // a multiple of 16
-      // x = bf16((h * (1 / RMS)) * gamma) for the chunk; rows past the
-      // batch and columns past H are zero in LDS
-      for (int q = tid; q < kBlkTok * (kBlkKC / 8); q += 256) {
-        const int j = q >> 4, c8 = (q & 15) * 8;
-        uint32_t o[4] = {0u, 0u, 0u, 0u};
-        if (j < nt && c8 < kw) {
-          const uint4 hv = *reinterpret_cast<const uint4 *>(hin + (t0 + j) * H + kc + c8);
-          const uint4 gv = *reinterpret_cast<const uint4 *>(gamma + kc + c8);
-          const uint32_t hq[4] = {hv.x, hv.y, hv.z, hv.w}, gq[4] = {gv.x, gv.y, gv.z, gv.w};
-          const float r = rinv[j];
+      const int e = 32 * (w + 4 * bi) + (lane & 31);
+      ev[bi] = w + 4 * bi < neb && e < E;
+      wrow[bi] = wr + (int64_t)(ev[bi] ? e : 0) * H + 8 * (lane >> 5);
+    }
+    const bool arow = (lane & 31) < TOK;
+    const uint16_t *xrow = xs + (arow ? (lane & 31) : 0) * XS + 8 * (lane >> 5);
+    uint4 bA[NB][G], bB[NB][G];
+    auto load = [&](uint4 (&b)[NB][G], int g) __attribute__((always_inline)) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const uint32_t lo = f32_to_bf16_bits(
-                (bf16_bits_to_f32(hq[i] & 0xFFFFu) * r) * bf16_bits_to_f32(gq[i] & 0xFFFFu));
-            const uint32_t hi = f32_to_bf16_bits(
-                (bf16_bits_to_f32(hq[i] >> 16) * r) * bf16_bits_to_f32(gq[i] >> 16));
-            m = fmaxf(m, fmaxf(fabsf(bf16_bits_to_f32(lo)), fabsf(bf16_bits_to_f32(hi))));
-            o[i] = lo | (hi << 16);
-          }
-          *reinterpret_cast<uint4 *>(x + (t0 + j) * H + kc + c8) = make_uint4(o[0], o[1], o[2], o[3]);
+      for (int bi = 0; bi < NB; ++bi)
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+          const int st = g * G + i;
+          b[bi][i] = ev[bi] && st < nst ? *reinterpret_cast<const uint4 *>(wrow[bi] + 16 * st)
+                                        : make_uint4(0u, 0u, 0u, 0u);
         }
-        *reinterpret_cast<uint4 *>(xs + j * kBlkXS + c8) = make_uint4(o[0], o[1], o[2], o[3]);
-      }
-      __syncthreads();
-      // router: lane l holds token row l % 32 of x and expert row l % 32 of
-      // the block, columns 8 (l / 32) .. + 7 of each 16-column step
+    };
+    auto mfmas = [&](const uint4 (&b)[NB][G], int g) __attribute__((always_inline)) {
 #pragma unroll
-      for (int bi = 0; bi < 2; ++bi) {
-        const int eb = w + 4 * bi;
-        if (eb < neb) {
-          const int e = 32 * eb + (lane & 31);
-          const bool ev = e < E;
-          const uint16_t *wrow = wr + (int64_t)(ev ? e : 0) * H + kc + 8 * (lane >> 5);
-          const uint16_t *xrow = xs + (lane & 31) * kBlkXS + 8 * (lane >> 5);
-          for (int kk = 0; kk < kw; kk += 16) {
-            const uint4 av = *reinterpret_cast<const uint4 *>(xrow + kk);
-            uint4 bv = *reinterpret_cast<const uint4 *>(wrow + kk);
-            if (!ev) bv = make_uint4(0u, 0u, 0u, 0u);
-            acc[bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(blk_bf16x8, av),
-                                                             __builtin_bit_cast(blk_bf16x8, bv),
-                                                             acc[bi], 0, 0, 0);
-          }
+      for (int i = 0; i < G; ++i) {
+        const int st = g * G + i;
+        if (st < nst) {
+          uint4 av = *reinterpret_cast<const uint4 *>(xrow + 16 * st);
+          if (!arow) av = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+          for (int bi = 0; bi < NB; ++bi)
+            if (w + 4 * bi < neb)
+              acc[bi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                  __builtin_bit_cast(blk_bf16x8, av), __builtin_bit_cast(blk_bf16x8, b[bi][i]),
+                  acc[bi], 0, 0, 0);
         }
       }
-      __syncthreads();
+    };
+    load(bA, 0);
+    for (int g = 0; g < ngr; g += 2) {
+      load(bB, g + 1);
+      mfmas(bA, g);
+      load(bA, g + 2);
+      mfmas(bB, g + 1);
     }
     // logits: lane l holds expert 32 eb + l % 32 for token rows
     // 8 (q / 4) + 4 (l / 32) + q % 4
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi) {
+    for (int bi = 0; bi < NB; ++bi) {
       const int e = 32 * (w + 4 * bi) + (lane & 31);
       if (w + 4 * bi < neb && e < E) {
 #pragma unroll
@@ -153,8 +185,8 @@ __global__ __launch_bounds__(256) void block_pre0_kernel(
     // top-k: wave w takes tokens t0 + 4 i + w (the wave routing body, same
     // arithmetic as the layer's)
 #pragma unroll 1
-    for (int i = 0; i < kBlkTok / 4; ++i)
-      qdr::route_topk_wave_body<PER>((int)(tb * (kBlkTok / 4) + i), logits, T, E, k, renorm, ids,
+    for (int i = 0; i < TOK / 4; ++i)
+      qdr::route_topk_wave_body<PER>((int)(tb * (TOK / 4) + i), logits, T, E, k, renorm, ids,
                                      wts);
   }
   // the RAC accumulators the quantiser that follows adds into
@@ -164,6 +196,37 @@ __global__ __launch_bounds__(256) void block_pre0_kernel(
   if (ramax && blockIdx.x == 0 && tid == 0) ramax[0] = 0.0f;
   m = block_max(m, red);
   if (tid == 0) part[blockIdx.x] = m;
+}
+
+// token rows per block of the block pre-kernel: the largest of 32, 16, 8
+// that leaves at least 256 blocks and whose rows fit LDS (0: none fits)
+inline int block_tok(int64_t T, int64_t H) {
+  for (int tok = 32; tok >= 8; tok >>= 1)
+    if ((T >= (int64_t)tok * 256 || tok == 8) && block_lds(tok, H) <= kBlkLds) return tok;
+  return 0;
+}
+
+template <int TOK>
+void launch_pre0(int E, int np, hipStream_t s, const void *h, const void *gamma, float eps,
+                 const void *wr, int64_t T, int64_t H, int k, int renorm, void *x, float *logits,
+                 int32_t *ids, float *wts, float *part, uint64_t *scores, float *ramax) {
+  auto kern = block_pre0_kernel<4, TOK>;
+  switch ((E + 63) >> 6) {
+    case 1: kern = block_pre0_kernel<1, TOK>; break;
+    case 2: kern = block_pre0_kernel<2, TOK>; break;
+    case 3: kern = block_pre0_kernel<3, TOK>; break;
+    default: break;
+  }
+  static bool attr[4] = {false, false, false, false};
+  const int pi = ((E + 63) >> 6) - 1;
+  if (!attr[pi])
+    attr[pi] = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                   hipFuncAttributeMaxDynamicSharedMemorySize,
+                                   kBlkLds) == hipSuccess;
+  hipLaunchKernelGGL(kern, dim3((unsigned)np), dim3(256), (size_t)block_lds(TOK, H), s,
+                     static_cast<const uint16_t *>(h), static_cast<const uint16_t *>(gamma), eps,
+                     static_cast<const uint16_t *>(wr), T, H, E, k, renorm,
+                     static_cast<uint16_t *>(x), logits, ids, wts, part, scores, ramax);
 }
 
 // routing ranks (nr workgroups) | X quantiser (+ RAC scores) on a (gx, gy) grid
@@ -375,7 +438,7 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
   if (st) return st;
   st = qdh::check_nvfp4(w2, E, H, I);
   if (st) return st;
-  if (blk && E > kBlkMaxE) return QD_ERR_UNSUPPORTED;
+  if (blk && (E > kBlkMaxE || block_tok(T, H) == 0)) return QD_ERR_UNSUPPORTED;
   if (T == 0) return QD_OK;
   if (blk ? (!blk->h || !blk->gamma || !blk->w_router || !y) : (!x || !logits || !y))
     return QD_ERR_NULL;
@@ -444,22 +507,22 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
   mark(QD_STAGE_ROUTE);
   int np = ga;      // amax partials of X
   if (blk) {
-    const int64_t ntb = (T + kBlkTok - 1) / kBlkTok;
+    const int tok = block_tok(T, H);
+    const int64_t ntb = (T + tok - 1) / tok;
     np = (int)(ntb < qdq::kAmaxPartials ? ntb : qdq::kAmaxPartials);
-    auto pre0 = block_pre0_kernel<4>;
-    switch ((E + 63) >> 6) {
-      case 1: pre0 = block_pre0_kernel<1>; break;
-      case 2: pre0 = block_pre0_kernel<2>; break;
-      case 3: pre0 = block_pre0_kernel<3>; break;
-      default: break;
-    }
-    hipLaunchKernelGGL(pre0, dim3((unsigned)np), dim3(256), 0, s,
-                       static_cast<const uint16_t *>(blk->h),
-                       static_cast<const uint16_t *>(blk->gamma), blk->eps,
-                       static_cast<const uint16_t *>(blk->w_router), T, H, E, k, renorm,
-                       static_cast<uint16_t *>(const_cast<void *>(x)),
-                       const_cast<float *>(logits), ids, wts, part, rac ? scores : nullptr,
-                       rac ? ramax : nullptr);
+    void *xw = const_cast<void *>(x);
+    float *lw = const_cast<float *>(logits);
+    uint64_t *sc = rac ? scores : nullptr;
+    float *ra = rac ? ramax : nullptr;
+    if (tok == 32)
+      launch_pre0<32>(E, np, s, blk->h, blk->gamma, blk->eps, blk->w_router, T, H, k, renorm, xw,
+                      lw, ids, wts, part, sc, ra);
+    else if (tok == 16)
+      launch_pre0<16>(E, np, s, blk->h, blk->gamma, blk->eps, blk->w_router, T, H, k, renorm, xw,
+                      lw, ids, wts, part, sc, ra);
+    else
+      launch_pre0<8>(E, np, s, blk->h, blk->gamma, blk->eps, blk->w_router, T, H, k, renorm, xw,
+                     lw, ids, wts, part, sc, ra);
   } else {
     hipLaunchKernelGGL(layer_pre1_kernel, dim3((unsigned)(ntopk + ga)), dim3(256), 0, s, logits,
                        T, E, k, renorm, ids, wts, ntopk, x, n16, part, ga,

@@ -340,5 +340,10 @@ def test_block_validation(lib):
     assert b(FAKE, FAKE, ctypes.c_float(1e-6), FAKE, T, H, 300, k, I, 8, 0, 1,
              ctypes.byref(w13b), ctypes.byref(w2b), FAKE, FAKE, 1 << 40,
              None) == Q.QD_ERR_UNSUPPORTED                               # E > 256
+    w13w = _nv(E, 2 * I, 9216, FAKE)
+    w2w = _nv(E, 9216, I, FAKE)
+    assert b(FAKE, FAKE, ctypes.c_float(1e-6), FAKE, T, 9216, E, k, I, 8, 0, 1,
+             ctypes.byref(w13w), ctypes.byref(w2w), FAKE, FAKE, 1 << 40,
+             None) == Q.QD_ERR_UNSUPPORTED                               # rows past LDS
     assert b(None, None, ctypes.c_float(1e-6), None, 0, H, E, k, I, 8, 0, 1, ctypes.byref(w13),
              ctypes.byref(w2), None, None, 0, None) == Q.QD_OK          # empty batch

@@ -78,6 +78,8 @@ CASES = [
     # heavy tails, edge values, zero rows (RMS = sqrt(eps))
     ("blk_edges", 48, 256, 16, 4, 64, 16, 0, True,
      dict(acts="student_t3", edge_cases=True, outlier_frac=0.0)),
+    # the widest hidden state the block's LDS rows take (8 tokens x 9200)
+    ("blk_h9200", 16, 9200, 8, 2, 32, 8, 0, True, {}),
     # many rows per expert: the tile GEMM
     ("blk_tile", 256, 256, 4, 2, 128, 8, 0, True, {}),
 ]
