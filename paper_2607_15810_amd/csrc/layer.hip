@@ -71,40 +71,58 @@ __global__ __launch_bounds__(256) void block_pre0_kernel(
   for (int64_t tb = blockIdx.x; tb < ntb; tb += gridDim.x) {
     const int64_t t0 = tb * TOK;
     const int nt = (int)(T - t0 < TOK ? T - t0 : TOK);
-    // 1 / RMS: squares summed per lane over its 8-column pieces, then across
-    // the wave
+    // the block's rows of h into LDS, and 1 / RMS: squares summed per lane
+    // over its 8-column pieces, then across the wave (wave w: rows RPW w ..;
+    // rows past the batch repeat the block's first row, so the loads need no
+    // branch and several rows' loads are in flight together)
     constexpr int RPW = TOK / 4;
-    for (int j = RPW * w; j < RPW * w + RPW && j < nt; ++j) {
-      const uint16_t *hr = hin + (t0 + j) * H;
-      float ss = 0.0f;
-      for (int64_t c = 8 * lane; c < H; c += 512) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(hr + c);
-        const uint32_t q[4] = {v.x, v.y, v.z, v.w};
+    {
+      float ss[RPW];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float a = bf16_bits_to_f32(q[i] & 0xFFFFu), b = bf16_bits_to_f32(q[i] >> 16);
-          ss += a * a;
-          ss += b * b;
+      for (int jj = 0; jj < RPW; ++jj) ss[jj] = 0.0f;
+#pragma unroll 2
+      for (int64_t c = 8 * lane; c < H; c += 512) {
+        uint4 v[RPW];
+#pragma unroll
+        for (int jj = 0; jj < RPW; ++jj) {
+          const int j = RPW * w + jj;
+          v[jj] = *reinterpret_cast<const uint4 *>(hin + (t0 + (j < nt ? j : 0)) * H + c);
+        }
+#pragma unroll
+        for (int jj = 0; jj < RPW; ++jj) {
+          *reinterpret_cast<uint4 *>(xs + (RPW * w + jj) * XS + c) = v[jj];
+          const uint32_t q[4] = {v[jj].x, v[jj].y, v[jj].z, v[jj].w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float a = bf16_bits_to_f32(q[i] & 0xFFFFu), b = bf16_bits_to_f32(q[i] >> 16);
+            ss[jj] += a * a;
+            ss[jj] += b * b;
+          }
         }
       }
 #pragma unroll
-      for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
-      if (lane == 0) rinv[j] = 1.0f / sqrtf(ss / (float)H + eps);
+      for (int jj = 0; jj < RPW; ++jj) {
+        float t = ss[jj];
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o, 64);
+        if (lane == 0) rinv[RPW * w + jj] = 1.0f / sqrtf(t / (float)H + eps);
+      }
     }
     __syncthreads();
-    // x = bf16((h * (1 / RMS)) * gamma), to x and to LDS (rows past the
-    // batch zero in LDS)
+    // x = bf16((h * (1 / RMS)) * gamma) in place in LDS, and to x (rows past
+    // the batch stay as loaded: their MFMA rows are never stored)
     const int n8i = (int)n8;
 #pragma unroll 4
     for (int q = tid; q < TOK * n8i; q += 256) {
       const int j = q / n8i;
       const int c = (q - j * n8i) * 8;
-      uint32_t o[4] = {0u, 0u, 0u, 0u};
       if (j < nt) {
-        const uint4 hv = *reinterpret_cast<const uint4 *>(hin + (t0 + j) * H + c);
+        uint4 *px = reinterpret_cast<uint4 *>(xs + j * XS + c);
+        const uint4 hv = *px;
         const uint4 gv = *reinterpret_cast<const uint4 *>(gamma + c);
         const uint32_t hq[4] = {hv.x, hv.y, hv.z, hv.w}, gq[4] = {gv.x, gv.y, gv.z, gv.w};
         const float r = rinv[j];
+        uint32_t o[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const uint32_t lo = f32_to_bf16_bits(
@@ -114,9 +132,10 @@ __global__ __launch_bounds__(256) void block_pre0_kernel(
           m = fmaxf(m, fmaxf(fabsf(bf16_bits_to_f32(lo)), fabsf(bf16_bits_to_f32(hi))));
           o[i] = lo | (hi << 16);
         }
-        *reinterpret_cast<uint4 *>(x + (t0 + j) * H + c) = make_uint4(o[0], o[1], o[2], o[3]);
+        const uint4 ov = make_uint4(o[0], o[1], o[2], o[3]);
+        *px = ov;
+        *reinterpret_cast<uint4 *>(x + (t0 + j) * H + c) = ov;
       }
-      *reinterpret_cast<uint4 *>(xs + j * XS + c) = make_uint4(o[0], o[1], o[2], o[3]);
     }
     __syncthreads();
     // router: lane l holds token row l % 32 (zero past TOK) and expert row
