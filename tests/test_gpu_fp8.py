@@ -114,10 +114,12 @@ def test_fp8_layer_stagewise(case):
     assert rel <= REL_L2_FP8_LAYER, f"fp8 layer rel-L2 {rel:.3e}"
 
 
-def test_fp8_full_size_decode():
-    """The decode workload at full size (T=256, H=2048, E=128, I=768) through
-    the layer call the benchmark times; three experts carry real weights."""
-    name = "moe_decode_t256_h2048"
+@pytest.mark.parametrize("name", ["moe_decode_t256_h2048", "moe_zipf_decode_t64_h4096"])
+def test_fp8_full_size_decode(name):
+    """A decode workload at full size (T=256, H=2048, E=128, I=768; and the
+    Zipf-routed T=64, H=4096, I=1536 one with heavy tails and edge values)
+    through the layer call the benchmark times; three experts carry real
+    weights."""
     wl = synth.WORKLOADS[name]
     lg = synth.generate(name, with_weights=False).logits.numpy()
     perm = ORt.permute(ORt.topk_fast(lg, wl.k), wl.E)
