@@ -225,27 +225,49 @@ inline int block_tok(int64_t T, int64_t H) {
   return 0;
 }
 
+// the dynamic LDS limit of one instantiation, raised once (thread-safe
+// static initialisation)
+template <int PER, int TOK>
+const void *pre0_kernel() {
+  static const bool attr =
+      hipFuncSetAttribute(reinterpret_cast<const void *>(block_pre0_kernel<PER, TOK>),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, kBlkLds) == hipSuccess;
+  (void)attr;
+  return reinterpret_cast<const void *>(block_pre0_kernel<PER, TOK>);
+}
+
 template <int TOK>
 void launch_pre0(int E, int np, hipStream_t s, const void *h, const void *gamma, float eps,
                  const void *wr, int64_t T, int64_t H, int k, int renorm, void *x, float *logits,
                  int32_t *ids, float *wts, float *part, uint64_t *scores, float *ramax) {
-  auto kern = block_pre0_kernel<4, TOK>;
+  const uint16_t *hh = static_cast<const uint16_t *>(h);
+  const uint16_t *gg = static_cast<const uint16_t *>(gamma);
+  const uint16_t *ww = static_cast<const uint16_t *>(wr);
+  uint16_t *xx = static_cast<uint16_t *>(x);
+  const dim3 grid((unsigned)np), block(256);
+  const size_t lds = (size_t)block_lds(TOK, H);
   switch ((E + 63) >> 6) {
-    case 1: kern = block_pre0_kernel<1, TOK>; break;
-    case 2: kern = block_pre0_kernel<2, TOK>; break;
-    case 3: kern = block_pre0_kernel<3, TOK>; break;
-    default: break;
+    case 1:
+      (void)pre0_kernel<1, TOK>();
+      hipLaunchKernelGGL((block_pre0_kernel<1, TOK>), grid, block, lds, s, hh, gg, eps, ww, T, H,
+                         E, k, renorm, xx, logits, ids, wts, part, scores, ramax);
+      break;
+    case 2:
+      (void)pre0_kernel<2, TOK>();
+      hipLaunchKernelGGL((block_pre0_kernel<2, TOK>), grid, block, lds, s, hh, gg, eps, ww, T, H,
+                         E, k, renorm, xx, logits, ids, wts, part, scores, ramax);
+      break;
+    case 3:
+      (void)pre0_kernel<3, TOK>();
+      hipLaunchKernelGGL((block_pre0_kernel<3, TOK>), grid, block, lds, s, hh, gg, eps, ww, T, H,
+                         E, k, renorm, xx, logits, ids, wts, part, scores, ramax);
+      break;
+    default:
+      (void)pre0_kernel<4, TOK>();
+      hipLaunchKernelGGL((block_pre0_kernel<4, TOK>), grid, block, lds, s, hh, gg, eps, ww, T, H,
+                         E, k, renorm, xx, logits, ids, wts, part, scores, ramax);
+      break;
   }
-  static bool attr[4] = {false, false, false, false};
-  const int pi = ((E + 63) >> 6) - 1;
-  if (!attr[pi])
-    attr[pi] = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                   hipFuncAttributeMaxDynamicSharedMemorySize,
-                                   kBlkLds) == hipSuccess;
-  hipLaunchKernelGGL(kern, dim3((unsigned)np), dim3(256), (size_t)block_lds(TOK, H), s,
-                     static_cast<const uint16_t *>(h), static_cast<const uint16_t *>(gamma), eps,
-                     static_cast<const uint16_t *>(wr), T, H, E, k, renorm,
-                     static_cast<uint16_t *>(x), logits, ids, wts, part, scores, ramax);
 }
 
 // routing ranks (nr workgroups) | X quantiser (+ RAC scores) on a (gx, gy) grid
