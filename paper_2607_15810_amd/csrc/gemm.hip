@@ -888,8 +888,12 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(GemmArgs p, int
 // fragment-ordered copy when present (64 contiguous bytes per 16 rows), and
 // when LDS allows, the A scales of four stages at a time (16 contiguous
 // bytes per row, one load per 16-byte piece) go into a two-slot ring of their
-// own; the three stages between those loads issue a one-line dummy load in
-// their place so every stage issues the same number of loads.
+// own.  With the four-slot ring the three stages between those loads issue a
+// one-line placeholder load instead, so every stage issues the same number of
+// loads; with the three-slot ring (RAC) the wait before each stage covers
+// every outstanding load, so those stages issue none, and the stage slot
+// drops its A-scale area (B scales right after the codes), which leaves the
+// A-scale ring room beside the compact table.
 // Lane l of a fragment holds row l % 32, elements 32 (l / 32) .. +31 of the
 // stage; MFMA k-step s (0..3) takes elements 8s .. 8s+7 of each half, for A
 // and B alike.
@@ -902,16 +906,26 @@ constexpr int TL_BCODE = 8192;
 constexpr int TL_ASCL = 12288;
 constexpr int TL_BSCL = 13312;
 constexpr int TL_STAGE = 13824;
+constexpr int TL_BSCL_G = 12288;         // three-slot ring with the A-scale ring
+constexpr int TL_STAGE_G = 12800;
+constexpr int TL_PAD = 4;                // f16 columns past each compact table row
 constexpr int TL_EMAX = 1024;            // experts handled by the tile scan (4 per thread)
 constexpr int TL_LDS_MAX = 160 * 1024 - 1024;   // dynamic LDS beside the static arrays
 
 // ring depth: four slots, or three with RAC, which leaves LDS room for the
 // compact table (three slots measured 1-3% slower without RAC)
 __host__ __device__ constexpr int tl_ns(bool rac) { return rac ? 3 : 4; }
-// LDS: ring, then (RAC) the compact weight table [128][ksa + 8] f16 and the
-// selected channels [ksa]
-__host__ __device__ inline int tl_lds_bytes(bool rac, int ksa) {
-  return tl_ns(rac) * TL_STAGE + (rac ? TL_N * (ksa + 8) * 2 + ksa * 4 : 0);
+// stage slot size and the B-scale offset inside it (grp: the A-scale ring is on)
+__host__ __device__ constexpr int tl_stage(bool rac, bool grp) {
+  return tl_ns(rac) == 3 && grp ? TL_STAGE_G : TL_STAGE;
+}
+__host__ __device__ constexpr int tl_bscl(bool rac, bool grp) {
+  return tl_ns(rac) == 3 && grp ? TL_BSCL_G : TL_BSCL;
+}
+// LDS: ring, then (RAC) the compact weight table [128][ksa + TL_PAD] f16 and
+// the selected channels [ksa], then (grp) the A-scale ring
+__host__ __device__ inline int tl_lds_bytes(bool rac, int ksa, bool grp) {
+  return tl_ns(rac) * tl_stage(rac, grp) + (rac ? TL_N * (ksa + TL_PAD) * 2 + ksa * 4 : 0);
 }
 constexpr int TL_AGRP = 2 * TL_M * 16;   // the A-scale ring: 2 slots x 256 rows x 16 B
 constexpr int TL_LDS_2WG = TL_LDS_MAX / 2;   // two workgroups per CU
@@ -945,13 +959,13 @@ struct TlRaw {
 // ascl / astr: the A scale dword of row r of this stage is at ascl + r * astr
 template <int MTV>
 __device__ __forceinline__ void tl_read(TlRaw &R, const unsigned char *sl, const unsigned char *ascl,
-                                        int astr, int fa0, int fb0, int fbs, int lane) {
+                                        int astr, int bscl, int fa0, int fb0, int fbs, int lane) {
   const int r = lane & 31;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int fb = fb0 + j * fbs;
     R.b[j] = *reinterpret_cast<const uint4 *>(sl + TL_BCODE + (fb * 64 + lane) * 16);
-    R.bs[j] = *reinterpret_cast<const uint32_t *>(sl + TL_BSCL + (fb * 32 + r) * 4);
+    R.bs[j] = *reinterpret_cast<const uint32_t *>(sl + bscl + (fb * 32 + r) * 4);
   }
 #pragma unroll
   for (int i = 0; i < MTV; ++i) {
@@ -1036,8 +1050,9 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
     const uint8_t *ws = uni_ptr((sfrag ? p.w_sfrag : p.w_scales) + (int64_t)e * N * kb16);
     const int bsstep = sfrag ? 64 : 4;
     const int nst = K / TL_K;
-    // the A-scale ring (grp): after the stage ring and the compact table
-    const uint32_t agrp = lds0 + (uint32_t)tl_lds_bytes(CMP, CMP ? p.ksa : 0);
+    // stage slots, and the A-scale ring (grp) after them and the compact table
+    const int tls = tl_stage(CMP, grp != 0), bsc = tl_bscl(CMP, grp != 0);
+    const uint32_t agrp = lds0 + (uint32_t)tl_lds_bytes(CMP, CMP ? p.ksa : 0, grp != 0);
     const uint32_t oag = arow(64 * w + lane) * (uint32_t)kb16;
     // five loads per wave and stage (waves 0 / 2 and 1 / 3 load the same B
     // scale half: equal bytes to equal places)
@@ -1046,7 +1061,7 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
     const uint8_t *a_cod = p.a_codes, *a_scl = p.a_scales;
     auto issue = [&](int s, int q) __attribute__((always_inline)) {
       s = min(s, nst - 1);
-      const uint32_t sb = uni(lds0 + q * TL_STAGE);
+      const uint32_t sb = uni(lds0 + q * tls);
       const uint8_t *ac = uni_ptr(a_cod + s * 32), *as_ = uni_ptr(a_scl + s * 4);
       const uint8_t *bc = uni_ptr(wc + s * 32), *bs_ = uni_ptr(ws + s * bsstep);
       dma16s(ac, oa0, sb + TL_ACODE + (2 * w) * 1024);
@@ -1054,24 +1069,24 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
       dma16s(bc, ob, sb + TL_BCODE + w * 1024);
       if (grp) {
         // stage 4G brings group G's A scales (rows 64 w .. 64 w + 63, 16 B
-        // each) into ring slot G % 2; other stages load one line (the group
-        // scales of the wave's first row: a different line per workgroup,
-        // never one line for the whole chip) into the unused A-scale area of
-        // their stage slot
+        // each) into ring slot G % 2; with four slots other stages load one
+        // line (the group scales of the wave's first row: a different line
+        // per workgroup, never one line for the whole chip) into the unused
+        // A-scale area of their stage slot
         if ((s & 3) == 0)
           dma16s(uni_ptr(a_scl + (s >> 2) * 16), oag,
                  uni(agrp + ((s >> 2) & 1) * (TL_AGRP / 2) + w * 1024));
-        else
+        else if constexpr (NS != 3)
           dma16s(uni_ptr(a_scl + (s >> 2) * 16), uni(oag), sb + TL_ASCL);
       } else {
         dma4s(as_, oas, sb + TL_ASCL + w * 256);
       }
-      dma4s(bs_, obs, sb + TL_BSCL + (w & 1) * 256);
+      dma4s(bs_, obs, sb + bsc + (w & 1) * 256);
     };
     // where tl_read finds stage s's A scales
     auto a_src = [&](int s) __attribute__((always_inline)) -> const unsigned char * {
       return grp ? lds + (agrp - lds0) + ((s >> 2) & 1) * (TL_AGRP / 2) + (s & 3) * 4
-                 : lds + (s % NS) * TL_STAGE + TL_ASCL;
+                 : lds + (s % NS) * tls + TL_ASCL;
     };
     const int astr = grp ? 16 : 4;
     const float a_dec = p.a_gs[1], sw = p.w_gs[2 * e + 1];
@@ -1081,8 +1096,8 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
     // left out (its share of any output is far below f32 resolution).
     float inv_c = 0.0f;
     bool res_on = false;
-    const int ksa = CMP ? p.ksa : 0, ksp = ksa + 8;
-    unsigned char *bres = lds + NS * TL_STAGE;
+    const int ksa = CMP ? p.ksa : 0, ksp = ksa + TL_PAD;
+    unsigned char *bres = lds + NS * tls;
     int32_t *sel_l = reinterpret_cast<int32_t *>(bres + TL_N * ksp * 2);
     if (RAC) {
       const float r_dec = p.r_gs[1];
@@ -1141,7 +1156,7 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
           __syncthreads();
           issue(s + NS - 1, (s + NS - 1) % NS);
           if constexpr (MTV > 0)
-            tl_read<MTV>(Rn, lds + ((s + 1) % NS) * TL_STAGE, a_src(s + 1), astr, fa0, fb0, fbs,
+            tl_read<MTV>(Rn, lds + ((s + 1) % NS) * tls, a_src(s + 1), astr, bsc, fa0, fb0, fbs,
                          lane);
           if constexpr (CMP) {
             // selected channels of stage s (slot s % NS holds it until the
@@ -1149,14 +1164,14 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
             // (the hardware FP4 conversion with a power-of-two scale and one
             // f16 multiply by the E4M3 scale, as in the operand decode: exact;
             // the next channel of the wave is fetched before this one's work)
-            const unsigned char *sl = lds + (s % NS) * TL_STAGE;
+            const unsigned char *sl = lds + (s % NS) * tls;
             const int tb = tid & 127, f = tb >> 5, r = tb & 31;
             while (nsel < TL_K * (s + 1)) {     // wave-uniform
               const int el = nsel - TL_K * s;   // >= 0: S is ascending
               const int nk2 = nk + 2;
               const int nxt = nk2 < p.Ks ? sel_l[nk2] : 0x7fffffff;
               const uint32_t byte = sl[TL_BCODE + ((f * 64 + (el >> 5) * 32 + r) * 16) + ((el & 31) >> 1)];
-              const uint32_t sbyte = sl[TL_BSCL + tb * 4 + (el >> 4)];
+              const uint32_t sbyte = sl[bsc + tb * 4 + (el >> 4)];
               const f16x2 v2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(byte, 256.0f, 0);
               const f16x2 sc = __builtin_bit_cast(f16x2, sbyte << 7);
               *reinterpret_cast<_Float16 *>(bres + (tb * ksp + nk) * 2) = (el & 1 ? v2[1] : v2[0]) * sc[0];
@@ -1172,10 +1187,13 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
       auto kpass = [&]() __attribute__((always_inline)) {
 #pragma unroll
         for (int t = 0; t < NS - 1; ++t) issue(t, t);
-        wait_vm<(NS - 2) * 5>();
+        // stage 0 has landed once at most stage NS - 2's loads are in flight
+        // (three slots with the A-scale ring: stage 1 issues four)
+        if (NS == 3 && grp) wait_vm<4>();
+        else wait_vm<(NS - 2) * 5>();
         __syncthreads();
         if constexpr (CMP) nsel = nk < p.Ks ? (int)uni((uint32_t)sel_l[nk]) : 0x7fffffff;
-        if constexpr (MTV > 0) tl_read<MTV>(R0, lds, a_src(0), astr, fa0, fb0, fbs, lane);
+        if constexpr (MTV > 0) tl_read<MTV>(R0, lds, a_src(0), astr, bsc, fa0, fb0, fbs, lane);
         for (int s = 0; s < nst; s += 2) {     // nst is even
           body(R0, R1, s);
           body(R1, R0, s + 1);
@@ -1228,7 +1246,11 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
 #pragma unroll
               for (int j = 0; j < 2; ++j) {
                 const int fb = fb0 + j * fbs;
-                bfr[j] = *reinterpret_cast<const f16x8 *>(bres + ((32 * fb + (lane & 31)) * ksp + c + 8 * h) * 2);
+                // rows are 8-byte aligned: two 8-byte reads
+                const uint2 *q = reinterpret_cast<const uint2 *>(
+                    bres + ((32 * fb + (lane & 31)) * ksp + c + 8 * h) * 2);
+                const uint2 lo = q[0], hi = q[1];
+                bfr[j] = __builtin_bit_cast(f16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
               }
 #pragma unroll
               for (int i = 0; i < MTV; ++i)
@@ -1797,17 +1819,21 @@ inline TlPlan tile_plan(int64_t rows, int E, int64_t N, int64_t K, bool rac, int
   // output offsets, fit 32 bits
   if (N * K / 2 >= (1LL << 32) || (rows + 1) * K / 2 >= (1LL << 32)) return pl;
   if ((rows + TL_M) * N * 2 >= (1LL << 32)) return pl;
-  pl.lds = tl_lds_bytes(rac, rac ? (Ks + 15) / 16 * 16 : 0);
-  if (rac && !compact_only && pl.lds > TL_LDS_2WG) {
+  bool cmp = rac;
+  int ksa = rac ? (Ks + 15) / 16 * 16 : 0;
+  if (rac && !compact_only && tl_lds_bytes(true, ksa, false) > TL_LDS_2WG) {
     pl.dense = true;
-    pl.lds = tl_lds_bytes(false, 0);
+    cmp = false;
+    ksa = 0;
   }
+  pl.lds = tl_lds_bytes(cmp, ksa, false);
   if (pl.lds > TL_LDS_MAX) return pl;
   // the A-scale ring where it keeps the workgroups per CU (groups of four
   // stages: K a multiple of 256, so no group reads past a row's scales)
-  if (K % 256 == 0 && ((pl.lds <= TL_LDS_2WG && pl.lds + TL_AGRP <= TL_LDS_2WG) ||
-                       (pl.lds > TL_LDS_2WG && pl.lds + TL_AGRP <= TL_LDS_MAX))) {
-    pl.lds += TL_AGRP;
+  const int lg = tl_lds_bytes(cmp, ksa, true) + TL_AGRP;
+  if (K % 256 == 0 && ((pl.lds <= TL_LDS_2WG && lg <= TL_LDS_2WG) ||
+                       (pl.lds > TL_LDS_2WG && lg <= TL_LDS_MAX))) {
+    pl.lds = lg;
     pl.grp = 1;
   }
   pl.ntn = (int)(N / TL_N);
