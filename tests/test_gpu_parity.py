@@ -70,6 +70,11 @@ SMALL = [
     ("tile_rac_dense", 256, 1024, 4, 2, 128, 512, {}),
     ("tile_rac_dense_zipf_edges", 300, 1024, 8, 2, 128, 1000,
      dict(routing="zipf", acts="student_t3", edge_cases=True, outlier_frac=0.0)),
+    # K = 384, not a multiple of 256: no A-scale ring (every stage loads its
+    # own activation scales) in each tile form
+    ("tile_k384", 300, 384, 4, 2, 128, 0, {}),
+    ("tile_rac_k384", 300, 384, 4, 2, 128, 12, {}),
+    ("tile_rac_dense_k384", 300, 384, 4, 2, 128, 200, {}),
     # H > 4096 at decode shapes: the one-workgroup selection and the separate
     # masked-residual pass instead of the fused selection by rank
     ("wide_h_resq", 16, 5120, 4, 2, 64, 40, {}),
