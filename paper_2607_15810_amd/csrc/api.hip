@@ -53,18 +53,7 @@ namespace {
 __global__ __launch_bounds__(1024) void reduce_max_kernel(const float *__restrict__ in,
                                                           int64_t n, float *__restrict__ out) {
   __shared__ float red[16];
-  float m = 0.0f;
-  // eight independent loads in flight per thread: one round trip to memory
-  // per 8192 values instead of one per 1024 (the values are >= 0)
-  const int64_t st = blockDim.x;
-  for (int64_t i = threadIdx.x; i < n; i += 8 * st) {
-    float v[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = i + j * st < n ? in[i + j * st] : 0.0f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) m = fmaxf(m, v[j]);
-  }
-  m = qd::block_max(m, red);
+  const float m = qd::block_max(qd::partials_max(in, n), red);
   if (threadIdx.x == 0) out[0] = m;
 }
 

@@ -60,9 +60,7 @@ __global__ __launch_bounds__(256) void quantize_weight_kernel(
     float *__restrict__ gscale) {
   __shared__ float red[16];
   const int64_t g = blockIdx.y;
-  float a = 0.0f;
-  for (int i = threadIdx.x; i < n_part; i += blockDim.x) a = fmaxf(a, part[g * n_part + i]);
-  const float amax = block_max(a, red);
+  const float amax = block_max(partials_max(part + g * n_part, n_part), red);
   float s_enc, s_dec;
   tensor_scale(amax, s_enc, s_dec);
   const bool zero_tensor = !(amax >= kZeroAmax);

@@ -88,9 +88,7 @@ __device__ __forceinline__ void quantize_act_body(
   __shared__ float red[16];
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   // tensor amax from the partial maxima
-  float a = 0.0f;
-  for (int i = threadIdx.x; i < n_part; i += blockDim.x) a = fmaxf(a, amax_part[i]);
-  const float amax = block_max(a, red);
+  const float amax = block_max(partials_max(amax_part, n_part), red);
   float s_enc, s_dec;
   tensor_scale(amax, s_enc, s_dec);
   const bool zero_tensor = !(amax >= kZeroAmax);

@@ -55,9 +55,7 @@ __global__ __launch_bounds__(256) void rac_scores_kernel(
   __shared__ float red[16];
   __shared__ uint64_t acc_s[16][256];
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  float a = 0.0f;
-  for (int i = threadIdx.x; i < n_part; i += blockDim.x) a = fmaxf(a, part[i]);
-  const float amax = block_max(a, red);
+  const float amax = block_max(partials_max(part, n_part), red);
   int e;
   frexpf(amax, &e);
   const int F = 36 - 2 * e;
@@ -322,9 +320,7 @@ __global__ __launch_bounds__(256) void rac_scores_pe_kernel(
   __shared__ uint64_t acc_s[16][256];
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const int e = blockIdx.y;
-  float a = 0.0f;
-  for (int i = threadIdx.x; i < n_part; i += blockDim.x) a = fmaxf(a, part[i]);
-  const float amax = block_max(a, red);
+  const float amax = block_max(partials_max(part, n_part), red);
   int ex;
   frexpf(amax, &ex);
   const int F = 36 - 2 * ex;
