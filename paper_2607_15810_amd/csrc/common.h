@@ -259,4 +259,19 @@ qd_status grouped_gemm_bitmap(const qd_nvfp4 *a, const int32_t *row_token,
                               const qd_nvfp4 *w, const qd_nvfp4 *rq, const uint32_t *bitmap,
                               int32_t Ks, int32_t *sel_out, int32_t epilogue, void *out,
                               float *amax_partials, hipStream_t stream);
+// Bytes of the staged A operand the grouped GEMM reads on these sizes (the
+// tile kernel with the residual, gathered rows and the A-scale ring): codes
+// [K / 64][rows][32 B] then scales [K / 256][rows][16 B]; 0 where it reads the
+// gathered rows directly.  gemm_stage_reserve: an upper bound over K_s >= 1.
+int64_t gemm_stage_bytes(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
+                         int32_t epilogue);
+int64_t gemm_stage_reserve(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t epilogue);
+// moe_w4a4_grouped_gemm with the A operand also given staged (a_stg, as
+// gemm_stage_bytes describes; the kernel falls back to the gathered rows
+// where it does not use it).
+qd_status grouped_gemm_staged(const qd_nvfp4 *a, const int32_t *row_token,
+                              const int32_t *expert_offsets, int32_t E, int64_t rows,
+                              const qd_nvfp4 *w, const qd_nvfp4 *rq, const int32_t *sel_idx,
+                              int32_t Ks, const void *rq_sel, int32_t epilogue, void *out,
+                              float *amax_partials, const uint8_t *a_stg, hipStream_t stream);
 }  // namespace qdi

@@ -58,6 +58,11 @@ struct GemmArgs {
   // sel + e * sel_stride, and r_sel indexed by grouped row instead of token
   int sel_stride;
   int rsel_rows;
+  // optional (tile kernel, gathered rows, A-scale ring on): the A operand
+  // staged by grouped row, stage-major -- codes [K / 64][rows][32 B], then
+  // the scales of four stages at a time [K / 256][rows][16 B] -- so that a
+  // tile's loads of one stage are contiguous
+  const uint8_t *a_stg;
 };
 
 // one maximum of |out| per workgroup into amax_part; workgroups also zero
@@ -1062,6 +1067,15 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
     const int tls = tl_stage(CMP, grp != 0), bsc = tl_bscl(CMP, grp != 0);
     const uint32_t agrp = lds0 + (uint32_t)tl_lds_bytes(CMP, CMP ? p.ksa : 0, grp != 0);
     const uint32_t oag = arow(64 * w + lane) * (uint32_t)kb16;
+    // the staged A operand (first pass only): row offsets within a stage's
+    // [rows][32 B] and a group's [rows][16 B] record
+    bool stg = GATHER && grp && p.a_stg != nullptr;
+    auto srow = [&](int r) __attribute__((always_inline)) -> uint32_t {
+      return (uint32_t)(row0 + (r < nrows ? r : 0));
+    };
+    const uint32_t os0 = srow(64 * w + (lane & 31)) * 32u + hb;
+    const uint32_t os1 = srow(64 * w + 32 + (lane & 31)) * 32u + hb;
+    const uint32_t osg = srow(64 * w + lane) * 16u;
     // five loads per wave and stage (waves 0 / 2 and 1 / 3 load the same B
     // scale half: equal bytes to equal places)
     // the A operand of the pass: the activations, then (DENSE) the masked
@@ -1072,8 +1086,14 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
       const uint32_t sb = uni(lds0 + q * tls);
       const uint8_t *ac = uni_ptr(a_cod + s * 32), *as_ = uni_ptr(a_scl + s * 4);
       const uint8_t *bc = uni_ptr(wc + s * 32), *bs_ = uni_ptr(ws + s * bsstep);
-      dma16s(ac, oa0, sb + TL_ACODE + (2 * w) * 1024);
-      dma16s(ac, oa1, sb + TL_ACODE + (2 * w + 1) * 1024);
+      if (stg) {
+        const uint8_t *sc = uni_ptr(p.a_stg + (int64_t)s * p.rows * 32);
+        dma16s(sc, os0, sb + TL_ACODE + (2 * w) * 1024);
+        dma16s(sc, os1, sb + TL_ACODE + (2 * w + 1) * 1024);
+      } else {
+        dma16s(ac, oa0, sb + TL_ACODE + (2 * w) * 1024);
+        dma16s(ac, oa1, sb + TL_ACODE + (2 * w + 1) * 1024);
+      }
       dma16s(bc, ob, sb + TL_BCODE + w * 1024);
       if (grp) {
         // stage 4G brings group G's A scales (rows 64 w .. 64 w + 63, 16 B
@@ -1081,9 +1101,14 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
         // line (the group scales of the wave's first row: a different line
         // per workgroup, never one line for the whole chip) into the unused
         // A-scale area of their stage slot
-        if ((s & 3) == 0)
-          dma16s(uni_ptr(a_scl + (s >> 2) * 16), oag,
-                 uni(agrp + ((s >> 2) & 1) * (TL_AGRP / 2) + w * 1024));
+        if ((s & 3) == 0) {
+          if (stg)
+            dma16s(uni_ptr(p.a_stg + (int64_t)p.rows * kb2 + (int64_t)(s >> 2) * p.rows * 16), osg,
+                   uni(agrp + ((s >> 2) & 1) * (TL_AGRP / 2) + w * 1024));
+          else
+            dma16s(uni_ptr(a_scl + (s >> 2) * 16), oag,
+                   uni(agrp + ((s >> 2) & 1) * (TL_AGRP / 2) + w * 1024));
+        }
         else if constexpr (NS != 3)
           dma16s(uni_ptr(a_scl + (s >> 2) * 16), uni(oag), sb + TL_ASCL);
       } else {
@@ -1224,6 +1249,7 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
               for (int q = 0; q < 16; ++q) acc[i][j][q] *= inv_c;
           a_cod = p.r_codes;
           a_scl = p.r_scales;
+          stg = false;
           kpass();
         }
       }
@@ -2023,7 +2049,7 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
                             const qd_nvfp4 *w, const qd_nvfp4 *rq, const int32_t *sel_idx,
                             int32_t Ks, const void *rq_sel, const uint32_t *bitmap,
                             int32_t epilogue, void *out, float *amax_partials, void *stream,
-                            bool per_expert = false) {
+                            bool per_expert = false, const uint8_t *a_stg = nullptr) {
   if (!a || !w || !out) return QD_ERR_NULL;
   if (epilogue != QD_EPI_NONE && epilogue != QD_EPI_SWIGLU) return QD_ERR_DTYPE;
   if (E < 1 || rows < 0) return QD_ERR_SHAPE;
@@ -2096,6 +2122,7 @@ qd_status grouped_gemm_impl(const qd_nvfp4 *a, const int32_t *row_token,
     }
   }
   p.out = static_cast<uint16_t *>(out);
+  p.a_stg = row_token && !per_expert ? a_stg : nullptr;
   p.amax_part = amax_partials;
   p.amax_n = !amax_partials ? 0
              : per_expert ? moe_w4a4_grouped_gemm_per_expert_amax_count(rows, N, K, E, Ks, epilogue)
@@ -2138,6 +2165,38 @@ extern "C" qd_status moe_w4a4_grouped_gemm(const qd_nvfp4 *a, const int32_t *row
                                            void *stream) {
   return grouped_gemm_impl(a, row_token, expert_offsets, E, rows, w, rq, sel_idx, Ks, rq_sel,
                            nullptr, epilogue, out, amax_partials, stream);
+}
+
+// Staging costs rows x K x 9/16 bytes written and read once, and saves time in
+// proportion to N (the n-tiles that re-read each stage): measured at N = 3072,
+// K = 4096 the tile GEMM gains 2.5x the copy's time, at N = 1536, K = 2048
+// 0.8x, so it is taken from N = 2048 on.
+constexpr int64_t kStageMinN = 2048;
+
+int64_t qdi::gemm_stage_bytes(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
+                              int32_t epilogue) {
+  if (Ks <= 0 || rows <= 0 || E < 1 || N < kStageMinN || K <= 0) return 0;
+  if (skinny_plan(rows, E, N, K, Ks, epilogue).ok) return 0;
+  const TlPlan tp = tile_plan(rows, E, N, K, true, Ks);
+  if (!tp.ok || !tp.grp) return 0;
+  return rows * (K / 2 + K / 16);
+}
+
+int64_t qdi::gemm_stage_reserve(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t epilogue) {
+  if (rows <= 0 || E < 1 || N < kStageMinN || K <= 0 || K % 256 != 0) return 0;
+  if (skinny_plan(rows, E, N, K, 1, epilogue).ok) return 0;
+  return tile_plan(rows, E, N, K, true, 1).ok ? rows * (K / 2 + K / 16) : 0;
+}
+
+qd_status qdi::grouped_gemm_staged(const qd_nvfp4 *a, const int32_t *row_token,
+                                   const int32_t *expert_offsets, int32_t E, int64_t rows,
+                                   const qd_nvfp4 *w, const qd_nvfp4 *rq, const int32_t *sel_idx,
+                                   int32_t Ks, const void *rq_sel, int32_t epilogue, void *out,
+                                   float *amax_partials, const uint8_t *a_stg, hipStream_t stream) {
+  if (!a_stg || !row_token) return QD_ERR_NULL;
+  if (!qdh::aligned16(a_stg)) return QD_ERR_ALIGN;
+  return grouped_gemm_impl(a, row_token, expert_offsets, E, rows, w, rq, sel_idx, Ks, rq_sel,
+                           nullptr, epilogue, out, amax_partials, stream, false, a_stg);
 }
 
 qd_status qdi::grouped_gemm_bitmap(const qd_nvfp4 *a, const int32_t *row_token,

@@ -364,9 +364,38 @@ __global__ __launch_bounds__(qdc::kRankSelThreads) void layer_pre3r_kernel(
                               rcodes, rscales, rgs);
 }
 
+// The quantised activations of every grouped row copied stage-major for the
+// W13 tile GEMM (its A loads of one stage then read one contiguous 8 KB
+// piece per tile instead of 32 bytes from each of 256 gathered rows): codes
+// [K / 64][R][32 B], then the scales of four stages at a time [K / 256][R][16 B].
+// Grid (ceil(2R / 256), K / 64 + K / 256): row y < K / 64 is code stage y,
+// thread x its 16-byte piece x % 2 of grouped row x / 2; the rows after are
+// scale group y - K / 64, thread x grouped row x.  Consecutive threads write
+// consecutive 16-byte pieces.
+__global__ __launch_bounds__(256) void layer_stage_kernel(const int32_t *__restrict__ row_token,
+                                                          const uint8_t *__restrict__ codes,
+                                                          const uint8_t *__restrict__ scales,
+                                                          int64_t R, int64_t K,
+                                                          uint8_t *__restrict__ out) {
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t y = blockIdx.y, nst = K / 64;
+  uint4 *o = reinterpret_cast<uint4 *>(out);
+  if (y < nst) {
+    if (x >= 2 * R) return;
+    const int64_t r = x >> 1, half = x & 1;
+    const int64_t t = row_token[r];
+    o[y * 2 * R + x] = *reinterpret_cast<const uint4 *>(codes + t * (K / 2) + 32 * y + 16 * half);
+  } else {
+    if (x >= R) return;
+    const int64_t g = y - nst;
+    const int64_t t = row_token[x];
+    o[R * (K / 32) + g * R + x] = *reinterpret_cast<const uint4 *>(scales + t * (K / 16) + 16 * g);
+  }
+}
+
 struct Layout {
   int64_t off[QD_VIEW_COUNT];
-  int64_t route_ws, q1_ws, sel_ws, q2_ws, sel2_ws, total;
+  int64_t route_ws, q1_ws, sel_ws, q2_ws, sel2_ws, stg, stg_bytes, total;
   // the block entry point's extra views after the layer's workspace: the
   // normalised state x and the router logits
   int64_t xn, lg, block_total;
@@ -425,6 +454,9 @@ Layout make_layout(int64_t T, int64_t H, int32_t E, int32_t k, int64_t I) {
   put(QD_VIEW_HR_SCALES, R * I / 16);
   put(QD_VIEW_HR_GSCALE, 8);
   put(QD_VIEW_HR_SEL, R * (int64_t)rac_selected_width((int32_t)I) * 2);
+  // the staged W13 operand, where the tile GEMM may take it
+  L.stg_bytes = qdi::gemm_stage_reserve(R, E, 2 * I, H, QD_EPI_SWIGLU);
+  L.stg = blob(L.stg_bytes);
   L.total = o;
   L.xn = blob(T * H * 2);
   L.lg = blob(T * (int64_t)E * 4);
@@ -627,12 +659,22 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
   uint16_t *h = (uint16_t *)P(QD_VIEW_H);
   float *hamax = (float *)P(QD_VIEW_H_AMAX);
   mark(QD_STAGE_W13);
-  if (rank_sel)
+  const int64_t stg_bytes = rank_sel ? 0 : qdi::gemm_stage_bytes(R, E, 2 * I, H, Ks, QD_EPI_SWIGLU);
+  if (rank_sel) {
     st = qdi::grouped_gemm_bitmap(&xq, row_token, offs, E, R, w13, &rq, bitmap, Ks, sel,
                                   QD_EPI_SWIGLU, h, hamax, s);
-  else
+  } else if (stg_bytes > 0 && stg_bytes <= L.stg_bytes) {
+    uint8_t *stg = reinterpret_cast<uint8_t *>(b + L.stg);
+    const int64_t gxs = (2 * R + 255) / 256, gys = H / 64 + H / 256;
+    if (gxs > 0x7fffffffLL || gys > 65535) return QD_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL(layer_stage_kernel, dim3((unsigned)gxs, (unsigned)gys), dim3(256), 0, s,
+                       row_token, xq.codes, xq.scales, R, H, stg);
+    st = qdi::grouped_gemm_staged(&xq, row_token, offs, E, R, w13, &rq, sel, Ks, rq_sel,
+                                  QD_EPI_SWIGLU, h, hamax, stg, s);
+  } else {
     st = moe_w4a4_grouped_gemm(&xq, row_token, offs, E, R, w13, rac ? &rq : nullptr,
                                rac ? sel : nullptr, Ks, rq_sel, QD_EPI_SWIGLU, h, hamax, stream);
+  }
   if (st) return st;
   qd_nvfp4 hq{(uint8_t *)P(QD_VIEW_HQ_CODES), (uint8_t *)P(QD_VIEW_HQ_SCALES),
               (float *)P(QD_VIEW_HQ_GSCALE), 1, R, I};

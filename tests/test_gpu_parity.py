@@ -70,6 +70,11 @@ SMALL = [
     ("tile_rac_dense", 256, 1024, 4, 2, 128, 512, {}),
     ("tile_rac_dense_zipf_edges", 300, 1024, 8, 2, 128, 1000,
      dict(routing="zipf", acts="student_t3", edge_cases=True, outlier_frac=0.0)),
+    # N = 2I >= 2048 with the residual in compact form: the layer stages the
+    # activations stage-major for the W13 tile GEMM (its h is compared bit for
+    # bit with the gathered-row GEMM below)
+    ("tile_rac_staged", 256, 256, 4, 2, 1024, 8, {}),
+    ("tile_rac_staged_zipf", 300, 512, 8, 2, 1024, 40, dict(routing="zipf")),
     # K = 384, not a multiple of 256: no A-scale ring (every stage loads its
     # own activation scales) in each tile form
     ("tile_k384", 300, 384, 4, 2, 128, 0, {}),
