@@ -658,17 +658,22 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
   if (st) return st;
   uint16_t *h = (uint16_t *)P(QD_VIEW_H);
   float *hamax = (float *)P(QD_VIEW_H_AMAX);
-  mark(QD_STAGE_W13);
+  // the staged W13 operand (timed with the steps before the GEMM, so that
+  // the W13 stage is the GEMM launch alone)
   const int64_t stg_bytes = rank_sel ? 0 : qdi::gemm_stage_bytes(R, E, 2 * I, H, Ks, QD_EPI_SWIGLU);
-  if (rank_sel) {
-    st = qdi::grouped_gemm_bitmap(&xq, row_token, offs, E, R, w13, &rq, bitmap, Ks, sel,
-                                  QD_EPI_SWIGLU, h, hamax, s);
-  } else if (stg_bytes > 0 && stg_bytes <= L.stg_bytes) {
-    uint8_t *stg = reinterpret_cast<uint8_t *>(b + L.stg);
+  const bool staged = stg_bytes > 0 && stg_bytes <= L.stg_bytes;
+  uint8_t *stg = reinterpret_cast<uint8_t *>(b + L.stg);
+  if (staged) {
     const int64_t gxs = (2 * R + 255) / 256, gys = H / 64 + H / 256;
     if (gxs > 0x7fffffffLL || gys > 65535) return QD_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(layer_stage_kernel, dim3((unsigned)gxs, (unsigned)gys), dim3(256), 0, s,
                        row_token, xq.codes, xq.scales, R, H, stg);
+  }
+  mark(QD_STAGE_W13);
+  if (rank_sel) {
+    st = qdi::grouped_gemm_bitmap(&xq, row_token, offs, E, R, w13, &rq, bitmap, Ks, sel,
+                                  QD_EPI_SWIGLU, h, hamax, s);
+  } else if (staged) {
     st = qdi::grouped_gemm_staged(&xq, row_token, offs, E, R, w13, &rq, sel, Ks, rq_sel,
                                   QD_EPI_SWIGLU, h, hamax, stg, s);
   } else {
