@@ -1076,8 +1076,9 @@ __global__ __launch_bounds__(TL_THREADS, 2) void gemm_tile_kernel(GemmArgs p, in
     const uint32_t os0 = srow(64 * w + (lane & 31)) * 32u + hb;
     const uint32_t os1 = srow(64 * w + 32 + (lane & 31)) * 32u + hb;
     const uint32_t osg = srow(64 * w + lane) * 16u;
-    // five loads per wave and stage (waves 0 / 2 and 1 / 3 load the same B
-    // scale half: equal bytes to equal places)
+    // five loads per wave and stage, four between A-scale groups with the
+    // three-slot ring (waves 0 / 2 and 1 / 3 load the same B scale half:
+    // equal bytes to equal places)
     // the A operand of the pass: the activations, then (DENSE) the masked
     // residual, same layout
     const uint8_t *a_cod = p.a_codes, *a_scl = p.a_scales;
