@@ -132,9 +132,9 @@ __device__ __forceinline__ void route_topk_rank_body(int bid, const float *__res
 // (within rows of 16 lanes by DPP moves, across rows by two shuffles); all
 // keys differ, so each round's maximum sits in exactly one lane and slot, and
 // the expert found in round s takes slot s.  (Counting every expert's rank
-// against all E broadcast keys, the earlier form, took 2.5x the time at
-// E = 128, k = 8.)  Same arithmetic as the rank body above (softmax terms in
-// slot order).
+// against all E broadcast keys instead takes 2.5x the time at E = 128,
+// k = 8.)  Same arithmetic as the rank body above (softmax terms in slot
+// order).
 constexpr int64_t kTopkWaveMinT = 1024;
 // PER = ceil(E / 64) experts per lane
 template <int PER>
