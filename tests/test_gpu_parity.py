@@ -75,6 +75,9 @@ SMALL = [
     # bit with the gathered-row GEMM below)
     ("tile_rac_staged", 256, 256, 4, 2, 1024, 8, {}),
     ("tile_rac_staged_zipf", 300, 512, 8, 2, 1024, 40, dict(routing="zipf")),
+    # the dense residual pass after a staged first pass (the second pass reads
+    # the masked residual by gathered row)
+    ("tile_rac_dense_staged", 256, 256, 4, 2, 1024, 200, {}),
     # K = 384, not a multiple of 256: no A-scale ring (every stage loads its
     # own activation scales) in each tile form
     ("tile_k384", 300, 384, 4, 2, 128, 0, {}),
