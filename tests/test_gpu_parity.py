@@ -318,10 +318,12 @@ def test_route_topk_paths(T, E, k, renorm):
     assert np.array_equal(inv_row.cpu().numpy(), perm["inv_row"])
 
 
-@pytest.mark.parametrize("T,k,H", [(5, 1, 8), (64, 8, 2048), (7, 12, 4104), (3, 32, 136)])
+@pytest.mark.parametrize("T,k,H", [(5, 1, 8), (64, 8, 2048), (7, 12, 4104), (3, 32, 136),
+                                   (70001, 2, 24)])
 def test_combine_slot_counts(T, k, H):
     """A9 on its own: k <= 8 (all loads in flight) and the generic loop
-    (k > 8), column blocks past one workgroup's 2048 columns, ragged H."""
+    (k > 8), column blocks past one workgroup's 2048 columns, ragged H, and
+    more tokens than the grid's 65535 rows (workgroups loop over tokens)."""
     rng = np.random.default_rng(T + k + H)
     R = T * k
     zb = np_bf16(torch.from_numpy(rng.standard_normal((R, H)).astype(np.float32)).to(torch.bfloat16))
