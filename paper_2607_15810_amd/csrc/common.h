@@ -183,6 +183,17 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// max(*addr, m) for finite m >= 0 into a float >= 0 that many workgroups
+// update at the end of a kernel: the device-coherent value is read first and
+// the atomic is issued only when m exceeds it.  The stored value only grows
+// during the kernel, so a skipped update is already covered; at one address
+// this removes most of the serialised atomics.
+__device__ __forceinline__ void atomic_max_pos(float *addr, float m) {
+  unsigned int *a = reinterpret_cast<unsigned int *>(addr);
+  const unsigned int cur = __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (__float_as_uint(m) > cur) atomicMax(a, __float_as_uint(m));
+}
+
 // This thread's max over the n partial maxima (>= 0) at p, taken in steps of
 // blockDim.x: eight independent loads in flight per thread, so one round trip
 // to memory covers up to eight values per thread (the partials are read once

@@ -270,7 +270,11 @@ void launch_pre0(int E, int np, hipStream_t s, const void *h, const void *gamma,
   }
 }
 
-// routing ranks (nr workgroups) | X quantiser (+ RAC scores) on a (gx, gy) grid
+// routing ranks (nr workgroups) | X quantiser (+ RAC scores) on a (gx, gy) grid;
+// the two bodies run in different workgroups and share one LDS array, so the
+// kernel's LDS is the larger body's (40 KB: four workgroups per CU)
+constexpr int kPre2Lds =
+    qdr::kRankLdsBytes > qdq::kQuantLdsBytes ? qdr::kRankLdsBytes : qdq::kQuantLdsBytes;
 template <bool RAC>
 __global__ __launch_bounds__(256) void layer_pre2_kernel(
     int64_t T, int E, int k, const int32_t *__restrict__ ids, int32_t *__restrict__ counts,
@@ -278,13 +282,18 @@ __global__ __launch_bounds__(256) void layer_pre2_kernel(
     const float *__restrict__ part, int np, uint8_t *__restrict__ codes,
     uint8_t *__restrict__ scales, float *__restrict__ gscale, uint64_t *__restrict__ scores,
     float *__restrict__ ramax, int gx, int gy) {
+  __shared__ __align__(16) unsigned char lds[kPre2Lds];
   const int b = blockIdx.x;
   if (b < nr) {
-    qdr::route_rank_body(b, T, E, k, ids, counts, ranks);
+    constexpr int kw = qdr::kTokBlock / 32;
+    qdr::route_rank_rows(b, T, E, k, ids, counts, ranks, reinterpret_cast<uint32_t(*)[kw]>(lds),
+                         reinterpret_cast<uint8_t(*)[kw]>(lds + qdr::kMaxE * kw * 4));
   } else {
     const int q = b - nr;
-    qdq::quantize_act_body<uint16_t, RAC>(q % gx, q / gx, gy, x, T, H, part, np, codes, scales,
-                                          gscale, scores, ramax);
+    qdq::quantize_act_rows<uint16_t, RAC>(
+        q % gx, q / gx, gy, x, T, H, part, np, codes, scales, gscale, scores, ramax,
+        reinterpret_cast<uint64_t(*)[qdq::kQuantPartCols]>(lds),
+        reinterpret_cast<float *>(lds + 16 * qdq::kQuantPartCols * 8));
   }
 }
 

@@ -10,27 +10,52 @@ namespace qdq {
 using namespace qd;
 
 template <typename T> struct Loader;
+// load_raw brings 16 consecutive elements starting at element index i
+// (16-aligned) into registers as stored; unpack widens them to float, so a
+// caller can keep the next block's load in flight while it works on this one.
 template <> struct Loader<uint16_t> {   // bf16 storage
-  // 16 consecutive elements starting at element index i (16-aligned)
-  __device__ static void load16(const void *base, int64_t i, float (&x)[16]) {
+  struct Raw {
+    uint4 a, b;
+  };
+  __device__ static void load_raw(const void *base, int64_t i, Raw &r) {
     const uint4 *p = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(base) + i);
-    uint4 a = p[0], b = p[1];
-    uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    r.a = p[0];
+    r.b = p[1];
+  }
+  __device__ static void unpack(const Raw &r, float (&x)[16]) {
+    const uint32_t w[8] = {r.a.x, r.a.y, r.a.z, r.a.w, r.b.x, r.b.y, r.b.z, r.b.w};
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       x[2 * j] = __uint_as_float(w[j] << 16);
       x[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
     }
   }
+  __device__ static void load16(const void *base, int64_t i, float (&x)[16]) {
+    Raw r;
+    load_raw(base, i, r);
+    unpack(r, x);
+  }
 };
 template <> struct Loader<float> {
-  __device__ static void load16(const void *base, int64_t i, float (&x)[16]) {
+  struct Raw {
+    float4 q[4];
+  };
+  __device__ static void load_raw(const void *base, int64_t i, Raw &r) {
     const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(base) + i);
 #pragma unroll
+    for (int j = 0; j < 4; ++j) r.q[j] = p[j];
+  }
+  __device__ static void unpack(const Raw &r, float (&x)[16]) {
+#pragma unroll
     for (int j = 0; j < 4; ++j) {
-      float4 v = p[j];
-      x[4 * j] = v.x; x[4 * j + 1] = v.y; x[4 * j + 2] = v.z; x[4 * j + 3] = v.w;
+      x[4 * j] = r.q[j].x; x[4 * j + 1] = r.q[j].y; x[4 * j + 2] = r.q[j].z;
+      x[4 * j + 3] = r.q[j].w;
     }
+  }
+  __device__ static void load16(const void *base, int64_t i, float (&x)[16]) {
+    Raw r;
+    load_raw(base, i, r);
+    unpack(r, x);
   }
 };
 
@@ -62,16 +87,17 @@ __device__ __forceinline__ void amax_partial_body(int bid, int nblk, const void 
   if (threadIdx.x == 0) part[bid] = m;
 }
 
-// trunc(sq * 2^F) as uint64 for a finite float sq >= 0, exactly (what the
-// float64 product and truncation give): sq = m * 2^x with m the integer
-// significand, so the result is m shifted by x + F.
-__device__ __forceinline__ uint64_t fixed_point_term(float sq, int F) {
-  const uint32_t bits = __float_as_uint(sq);
-  const uint32_t be = bits >> 23;
-  const uint64_t m = be ? ((bits & 0x7FFFFFu) | 0x800000u) : (bits & 0x7FFFFFu);
-  const int sh = (be ? (int)be - 150 : -149) + F;
-  if (sh >= 0) return m << sh;
-  return sh > -64 ? m >> (-sh) : 0ull;
+// The channel-score term trunc(sq * 2^F) (what the float64 product and
+// truncation give), for a finite sq >= 0 whose term is below 2^37, computed in
+// floating point: sq * 2^F is exact in float wherever it is >= 1 (a
+// power-of-two scaling of a normal value into the normal range), anything
+// below 1 truncates to 0 either way, and the integer result is exact in
+// double, where sums of up to 2^16 such terms stay exact (the quantiser's grid
+// gives no thread more rows than that).  The clamp only keeps a non-finite
+// input's term bounded.
+constexpr int64_t kScoreMaxRows = 1 << 16;
+__device__ __forceinline__ double fixed_point_term_f64(float sq, int F) {
+  return (double)fminf(truncf(ldexpf(sq, F)), 137438953472.0f);   // 2^37
 }
 
 // Q_A over [rows][cols] on a (gx, gy) grid of workgroups; this is
@@ -79,13 +105,17 @@ __device__ __forceinline__ uint64_t fixed_point_term(float sq, int F) {
 // (bx*16 + tx) and rows ty, ty+16*gy, ...  With RAC the same pass forms
 // r = x_hat - x and accumulates the fixed-point channel scores (u64, order
 // independent) and max|r|.
+// The LDS it uses comes from the caller: red (16 floats) and, with RAC, part
+// (16 x 272 u64), so that a kernel fusing it with other work can overlay
+// the two bodies' arrays.
+constexpr int kQuantPartCols = 16 * 17;
+constexpr int kQuantLdsBytes = 16 * kQuantPartCols * 8 + 16 * 4;
 template <typename T, bool RAC>
-__device__ __forceinline__ void quantize_act_body(
+__device__ __forceinline__ void quantize_act_rows(
     int bx, int by, int gy, const void *__restrict__ x, int64_t rows, int64_t cols,
     const float *__restrict__ amax_part, int n_part, uint8_t *__restrict__ codes,
     uint8_t *__restrict__ scales, float *__restrict__ gscale, uint64_t *__restrict__ scores,
-    float *__restrict__ ramax) {
-  __shared__ float red[16];
+    float *__restrict__ ramax, uint64_t (*part)[kQuantPartCols], float *red) {
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   // tensor amax from the partial maxima
   const float amax = block_max(partials_max(amax_part, n_part), red);
@@ -106,15 +136,25 @@ __device__ __forceinline__ void quantize_act_body(
     frexpf(amax, &e);
     F = 36 - 2 * e;
   }
-  uint64_t acc[16];
+  // per-thread score sums: exact integer sums in double (cheaper per term
+  // than 64-bit integer shifts), at most kScoreMaxRows terms each
+  double accd[16];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc[i] = 0ull;
+  for (int i = 0; i < 16; ++i) accd[i] = 0.0;
   float rmax = 0.0f;
 
   if (active) {
-    for (int64_t r = (int64_t)by * 16 + ty; r < rows; r += (int64_t)gy * 16) {
+    const int64_t step = (int64_t)gy * 16;
+    int64_t r = (int64_t)by * 16 + ty;
+    // with RAC (the longer row body) the thread's next row is loaded while
+    // this one is quantised
+    typename Loader<T>::Raw cur = {}, nxt = {};
+    if (RAC && r < rows) Loader<T>::load_raw(x, r * cols + cb * 16, cur);
+    for (; r < rows; r += step) {
+      if (!RAC) Loader<T>::load_raw(x, r * cols + cb * 16, cur);
+      else if (r + step < rows) Loader<T>::load_raw(x, (r + step) * cols + cb * 16, nxt);
       float v[16];
-      Loader<T>::load16(x, r * cols + cb * 16, v);
+      Loader<T>::unpack(cur, v);
       uint32_t lo, hi;
       uint32_t sb = quantize_block(v, s_enc, zero_tensor, lo, hi);
       reinterpret_cast<uint2 *>(codes + r * (cols >> 1))[cb] = make_uint2(lo, hi);
@@ -130,18 +170,18 @@ __device__ __forceinline__ void quantize_act_body(
           float xh = (ev[i] * sbf) * s_dec;
           float rr = xh - v[i];
           rmax = fmaxf(rmax, fabsf(rr));
-          acc[i] += fixed_point_term(rr * rr, F);   // each term < 2^37
+          accd[i] += fixed_point_term_f64(rr * rr, F);   // each term < 2^37
         }
       }
+      if (RAC) cur = nxt;
     }
   }
   if (RAC) {
     // reduce the per-thread sums over ty, then one atomic per channel
     // (channel 16 tx + i of row ty at 17 i + tx: consecutive tx are
     // adjacent when written, and consecutive channels 17 apart when read)
-    __shared__ uint64_t part[16][16 * 17];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) part[ty][17 * i + tx] = acc[i];
+    for (int i = 0; i < 16; ++i) part[ty][17 * i + tx] = (uint64_t)accd[i];
     __syncthreads();
     uint64_t s = 0;
     const int rd = 17 * (threadIdx.x & 15) + (threadIdx.x >> 4);
@@ -151,8 +191,21 @@ __device__ __forceinline__ void quantize_act_body(
     if (ch < cols && s != 0ull) atomicAdd((unsigned long long *)&scores[ch], (unsigned long long)s);
     float m = block_max(rmax, red);
     if (threadIdx.x == 0 && m > 0.0f)
-      atomicMax(reinterpret_cast<unsigned int *>(ramax), __float_as_uint(m));
+      atomic_max_pos(ramax, m);
   }
+}
+
+// quantize_act_rows with LDS arrays of its own
+template <typename T, bool RAC>
+__device__ __forceinline__ void quantize_act_body(
+    int bx, int by, int gy, const void *__restrict__ x, int64_t rows, int64_t cols,
+    const float *__restrict__ amax_part, int n_part, uint8_t *__restrict__ codes,
+    uint8_t *__restrict__ scales, float *__restrict__ gscale, uint64_t *__restrict__ scores,
+    float *__restrict__ ramax) {
+  __shared__ float red[16];
+  __shared__ uint64_t part[RAC ? 16 : 1][kQuantPartCols];
+  quantize_act_rows<T, RAC>(bx, by, gy, x, rows, cols, amax_part, n_part, codes, scales, gscale,
+                            scores, ramax, part, red);
 }
 
 constexpr int kAmaxPartials = 1024;     // per-call partial maxima (workspace)
@@ -173,6 +226,9 @@ inline void quant_grid(int64_t rows, int64_t cols, bool rac, int &gx, int &gy) {
   int64_t lim = cap / gx;
   if (lim < 1) lim = 1;
   if (g > lim) g = lim;
+  // at most kScoreMaxRows rows per thread (the exact double score sums)
+  const int64_t need = (rows + 16 * kScoreMaxRows - 1) / (16 * kScoreMaxRows);
+  if (g < need) g = need;
   gy = (int)g;
 }
 

@@ -90,7 +90,7 @@ __global__ __launch_bounds__(256) void rac_scores_kernel(
   if (ch < K && s != 0ull) atomicAdd((unsigned long long *)&scores[ch], (unsigned long long)s);
   float m = block_max(rmax, red);
   if (threadIdx.x == 0 && m > 0.0f)
-    atomicMax(reinterpret_cast<unsigned int *>(ramax), __float_as_uint(m));
+    atomic_max_pos(ramax, m);
 }
 
 // One workgroup of 1024 threads.  Radix select over 8-bit digits of the u64
@@ -357,7 +357,7 @@ __global__ __launch_bounds__(256) void rac_scores_pe_kernel(
   if (ch < K) scores_pe[(int64_t)e * K + ch] = sum;
   const float m = block_max(rmax, red);
   if (threadIdx.x == 0 && m > 0.0f)
-    atomicMax(reinterpret_cast<unsigned int *>(ramax), __float_as_uint(m));
+    atomic_max_pos(ramax, m);
 }
 
 // one workgroup per expert: the selection of rac_select_channels on score_e

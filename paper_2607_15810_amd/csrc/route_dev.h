@@ -313,12 +313,15 @@ __device__ __forceinline__ void route_topk_body(int bid, const float *__restrict
 // Per block of 256 tokens: expert bitmasks in LDS give every (token, slot)
 // its rank among the block's tokens routed to the same expert, and the
 // block's per-expert counts.
-__device__ __forceinline__ void route_rank_body(int bid, int64_t T, int E, int k,
+// (mask: kMaxE x 8 words and before: kMaxE x 8 bytes of LDS, from the caller)
+constexpr int kRankLdsBytes = kMaxE * (kTokBlock / 32) * 5;
+__device__ __forceinline__ void route_rank_rows(int bid, int64_t T, int E, int k,
                                                 const int32_t *__restrict__ ids,
                                                 int32_t *__restrict__ counts,
-                                                int32_t *__restrict__ ranks) {
-  __shared__ uint32_t mask[kMaxE][kTokBlock / 32];
-  __shared__ uint8_t before[kMaxE][kTokBlock / 32];   // tokens of e in earlier words
+                                                int32_t *__restrict__ ranks,
+                                                uint32_t (*mask)[kTokBlock / 32],
+                                                uint8_t (*before)[kTokBlock / 32]) {
+  // before[e][w]: tokens of e in earlier words
   const int64_t t0 = (int64_t)bid * kTokBlock;
   for (int i = threadIdx.x; i < E * (kTokBlock / 32); i += blockDim.x) (&mask[0][0])[i] = 0u;
   __syncthreads();
@@ -357,6 +360,16 @@ __device__ __forceinline__ void route_rank_body(int bid, int64_t T, int E, int k
       ranks[t * k + s] = (int)before[e][wd] + __popc(mask[e][wd] & low);
     }
   }
+}
+
+// route_rank_rows with LDS arrays of its own
+__device__ __forceinline__ void route_rank_body(int bid, int64_t T, int E, int k,
+                                                const int32_t *__restrict__ ids,
+                                                int32_t *__restrict__ counts,
+                                                int32_t *__restrict__ ranks) {
+  __shared__ uint32_t mask[kMaxE][kTokBlock / 32];
+  __shared__ uint8_t before[kMaxE][kTokBlock / 32];
+  route_rank_rows(bid, T, E, k, ids, counts, ranks, mask, before);
 }
 
 __device__ __forceinline__ void route_scatter_body(
