@@ -183,6 +183,18 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// The channel-score term trunc(sq * 2^F) (what the float64 product and
+// truncation give), for a finite sq >= 0 whose term is below 2^37, computed in
+// floating point: sq * 2^F is exact in float wherever it is >= 1 (a
+// power-of-two scaling of a normal value into the normal range), anything
+// below 1 truncates to 0 either way, and the integer result is exact in
+// double, where sums of up to kScoreMaxRows such terms stay exact.  The clamp
+// only keeps a non-finite input's term bounded.
+constexpr int64_t kScoreMaxRows = 1 << 16;
+__device__ __forceinline__ double fixed_point_term_f64(float sq, int F) {
+  return (double)fminf(truncf(ldexpf(sq, F)), 137438953472.0f);   // 2^37
+}
+
 // max(*addr, m) for finite m >= 0 into a float >= 0 that many workgroups
 // update at the end of a kernel: the device-coherent value is read first and
 // the atomic is issued only when m exceeds it.  The stored value only grows

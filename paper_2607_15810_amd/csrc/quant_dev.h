@@ -87,19 +87,6 @@ __device__ __forceinline__ void amax_partial_body(int bid, int nblk, const void 
   if (threadIdx.x == 0) part[bid] = m;
 }
 
-// The channel-score term trunc(sq * 2^F) (what the float64 product and
-// truncation give), for a finite sq >= 0 whose term is below 2^37, computed in
-// floating point: sq * 2^F is exact in float wherever it is >= 1 (a
-// power-of-two scaling of a normal value into the normal range), anything
-// below 1 truncates to 0 either way, and the integer result is exact in
-// double, where sums of up to 2^16 such terms stay exact (the quantiser's grid
-// gives no thread more rows than that).  The clamp only keeps a non-finite
-// input's term bounded.
-constexpr int64_t kScoreMaxRows = 1 << 16;
-__device__ __forceinline__ double fixed_point_term_f64(float sq, int F) {
-  return (double)fminf(truncf(ldexpf(sq, F)), 137438953472.0f);   // 2^37
-}
-
 // Q_A over [rows][cols] on a (gx, gy) grid of workgroups; this is
 // workgroup (bx, by).  Thread (tx, ty) of a 16x16 workgroup owns column block
 // (bx*16 + tx) and rows ty, ty+16*gy, ...  With RAC the same pass forms

@@ -62,9 +62,16 @@ __global__ __launch_bounds__(256) void rac_scores_kernel(
   const float s_dec = gscale[1];
   const int64_t nbc = K >> 4;
   const int64_t cb = (int64_t)blockIdx.x * 16 + tx;
+  // exact integer sums in double, moved into the u64 sums every
+  // kScoreMaxRows rows of the thread
   uint64_t acc[16];
+  double accd[16];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc[i] = 0ull;
+  for (int i = 0; i < 16; ++i) {
+    acc[i] = 0ull;
+    accd[i] = 0.0;
+  }
+  int nrow = 0;
   float rmax = 0.0f;
   if (cb < nbc) {
     for (int64_t t = (int64_t)blockIdx.y * 16 + ty; t < T; t += (int64_t)gridDim.y * 16) {
@@ -75,13 +82,20 @@ __global__ __launch_bounds__(256) void rac_scores_kernel(
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         rmax = fmaxf(rmax, fabsf(r[i]));
-        float sq = r[i] * r[i];
-        acc[i] += (uint64_t)ldexp((double)sq, F);
+        accd[i] += fixed_point_term_f64(r[i] * r[i], F);
+      }
+      if (++nrow == kScoreMaxRows) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          acc[i] += (uint64_t)accd[i];
+          accd[i] = 0.0;
+        }
+        nrow = 0;
       }
     }
   }
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc_s[ty][tx * 16 + i] = acc[i];
+  for (int i = 0; i < 16; ++i) acc_s[ty][tx * 16 + i] = acc[i] + (uint64_t)accd[i];
   __syncthreads();
   uint64_t s = 0;
 #pragma unroll
@@ -327,9 +341,16 @@ __global__ __launch_bounds__(256) void rac_scores_pe_kernel(
   const float s_dec = gscale[1];
   const int64_t nbc = K >> 4;
   const int64_t cb = (int64_t)blockIdx.x * 16 + tx;
+  // exact integer sums in double, moved into the u64 sums every
+  // kScoreMaxRows rows of the thread
   uint64_t acc[16];
+  double accd[16];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc[i] = 0ull;
+  for (int i = 0; i < 16; ++i) {
+    acc[i] = 0ull;
+    accd[i] = 0.0;
+  }
+  int nrow = 0;
   float rmax = 0.0f;
   if (cb < nbc) {
     const int r1 = offsets[e + 1];
@@ -342,13 +363,20 @@ __global__ __launch_bounds__(256) void rac_scores_pe_kernel(
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         rmax = fmaxf(rmax, fabsf(r[i]));
-        const float sq = r[i] * r[i];
-        acc[i] += (uint64_t)ldexp((double)sq, F);
+        accd[i] += fixed_point_term_f64(r[i] * r[i], F);
+      }
+      if (++nrow == kScoreMaxRows) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          acc[i] += (uint64_t)accd[i];
+          accd[i] = 0.0;
+        }
+        nrow = 0;
       }
     }
   }
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc_s[ty][tx * 16 + i] = acc[i];
+  for (int i = 0; i < 16; ++i) acc_s[ty][tx * 16 + i] = acc[i] + (uint64_t)accd[i];
   __syncthreads();
   uint64_t sum = 0;
 #pragma unroll
