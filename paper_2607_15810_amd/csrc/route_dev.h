@@ -381,11 +381,21 @@ __device__ __forceinline__ void route_scatter_body(
   __shared__ int32_t total[kMaxE];
   const int b = bid;
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    // eight token blocks' counts in flight at a time
     int tot = 0, pre = 0;
-    for (int bb = 0; bb < nblk; ++bb) {
-      int c = counts[(int64_t)bb * E + e];
-      tot += c;
-      if (bb < b) pre += c;
+    for (int b0 = 0; b0 < nblk; b0 += 8) {
+      int c[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int bj = b0 + j < nblk ? b0 + j : nblk - 1;   // in bounds, unpredicated
+        const int v = counts[(int64_t)bj * E + e];
+        c[j] = b0 + j < nblk ? v : 0;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        tot += c[j];
+        if (b0 + j < b) pre += c[j];
+      }
     }
     total[e] = tot;
     base[e] = pre;
