@@ -321,11 +321,18 @@ __global__ __launch_bounds__(256) void layer_scatter_kernel(
                           inv_row);
 }
 
+// the masked residual over all channels (sel not NULL: workgroup 0 also lists
+// S from the bitmap, for K <= 8192)
 __global__ __launch_bounds__(256) void layer_resq_kernel(
     const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
     const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
     const float *__restrict__ ramax, const uint32_t *__restrict__ bitmap,
-    uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales, float *__restrict__ rgs) {
+    uint8_t *__restrict__ rcodes, uint8_t *__restrict__ rscales, float *__restrict__ rgs,
+    int32_t *__restrict__ sel) {
+  if (sel && blockIdx.x == 0) {
+    __shared__ int sh[1024 + 32];
+    qdc::rac_list_selected(bitmap, (int)K, sel, sh);
+  }
   qdc::rac_resq_body(blockIdx.x, gridDim.x, x, xcodes, xscales, xgs, T, K, ramax, bitmap, rcodes,
                      rscales, rgs);
 }
@@ -570,6 +577,10 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
   // for the compact residual (H <= 4096) the selection by rank alone, with S
   // listed from the bitmap by the compact-residual kernel
   const bool rank_only = want_sel && H <= qdc::kRankSelMaxK;
+  // every other RAC case with H <= 4096 (the dense residual pass of the tile
+  // kernel): the selection by rank as well, then the masked residual, whose
+  // first workgroup lists S from the bitmap
+  const bool rank_dense = rac && !want_sel && !rank_sel && H <= qdc::kRankSelMaxK;
   void *rq_sel = want_sel ? P(QD_VIEW_RQ_SEL) : nullptr;
   hipStream_t s = qdh::S(stream);
   // routing scratch, amax partials of X and the channel bitmap (the same
@@ -622,7 +633,7 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
   mark(QD_STAGE_SELECT);
   if (rac) {
     const dim3 g3((unsigned)(nr + 1));
-    if (rank_sel || rank_only)
+    if (rank_sel || rank_only || rank_dense)
       hipLaunchKernelGGL(layer_pre3r_kernel, dim3((unsigned)(nr + H / 16)),
                          dim3(qdc::kRankSelThreads), 0, s, T,
                          E, k, nr, ids, counts, ranks, offs, row_token, inv_row, scores, (int)H,
@@ -657,7 +668,8 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
       if (g < 1) g = 1;
       hipLaunchKernelGGL(layer_resq_kernel, dim3((unsigned)g), dim3(256), 0, s,
                          static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
-                         ramax, bitmap, rq.codes, rq.scales, rq.gscale);
+                         ramax, bitmap, rq.codes, rq.scales, rq.gscale,
+                         rank_dense ? sel : nullptr);
     }
   } else {
     hipLaunchKernelGGL(layer_scatter_kernel, dim3((unsigned)nr), dim3(256), 0, s, T, E, k, nr,
