@@ -728,14 +728,16 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
     if (st) return st;
     // as at the W13 site: for I <= 4096 the selection by rank (one
     // workgroup per 16-channel block; no routing workgroups here), with the
-    // masked residual for the decode GEMM in bitmap mode, or with S listed
-    // by the compact-residual kernel for the tile GEMM
+    // masked residual for the decode GEMM in bitmap mode, with S listed by
+    // the compact-residual kernel for the tile GEMM, or (the dense residual
+    // pass) with S listed by the masked-residual launch
     const bool want2 = qdi::gemm_wants_rq_sel(R, E, H, I, Ks2, QD_EPI_NONE);
     bm2 = !want2 && I <= qdc::kRankSelMaxK &&
           qdi::gemm_takes_bitmap(R, E, H, I, Ks2, QD_EPI_NONE);
     const bool ro2 = want2 && I <= qdc::kRankSelMaxK;
+    const bool rd2 = !want2 && !bm2 && I <= qdc::kRankSelMaxK;
     if (want2) hr_sel = P(QD_VIEW_HR_SEL);
-    if (bm2 || ro2) {
+    if (bm2 || ro2 || rd2) {
       hipLaunchKernelGGL(layer_pre3r_kernel, dim3((unsigned)(I / 16)),
                          dim3(qdc::kRankSelThreads), 0, s, R, E, k, 0, ids, counts, ranks, offs,
                          row_token, inv_row, hscores, (int)I, Ks2, bitmap2, h, hq.codes,
@@ -749,6 +751,13 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
         hipLaunchKernelGGL(layer_compact_kernel, dim3((unsigned)g), dim3(256), 0, s, h, hq.codes,
                            hq.scales, hq.gscale, R, I, hramax, sel2, Ks2, width,
                            static_cast<uint16_t *>(hr_sel), hr.gscale, bitmap2);
+      } else if (rd2) {
+        int64_t g = (R * (I / 16) + 255) / 256;
+        if (g > 4096) g = 4096;
+        if (g < 1) g = 1;
+        hipLaunchKernelGGL(layer_resq_kernel, dim3((unsigned)g), dim3(256), 0, s, h, hq.codes,
+                           hq.scales, hq.gscale, R, I, hramax, bitmap2, hr.codes, hr.scales,
+                           hr.gscale, sel2);
       }
       st = qdh::check_launch();
       if (st) return st;
