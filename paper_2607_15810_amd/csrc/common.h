@@ -274,6 +274,12 @@ bool gemm_wants_rq_sel(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks
 // (the decode kernel, K <= 4096).
 bool gemm_takes_bitmap(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
                        int32_t epilogue);
+// The number of amax partials the grouped GEMM's kernel on these sizes
+// writes (its grid; moe_w4a4_grouped_gemm_amax_count is an upper bound over
+// the kernels that could run); sfrag: the weights carry fragment-ordered
+// scales; bitmap: the residual comes in bitmap mode.
+int64_t gemm_amax_written(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
+                          int32_t epilogue, bool sfrag, bool bitmap);
 // moe_w4a4_grouped_gemm in bitmap mode: bitmap [K / 32] marks the selected
 // channels S in place of a list; the decode kernel writes S in ascending
 // order to sel_out.  QD_ERR_UNSUPPORTED where gemm_takes_bitmap is false.

@@ -1968,6 +1968,22 @@ bool qdi::gemm_wants_rq_sel(int64_t rows, int32_t E, int64_t N, int64_t K, int32
   return tp.ok && !tp.dense;
 }
 
+int64_t qdi::gemm_amax_written(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
+                               int32_t epilogue, bool sfrag, bool bitmap) {
+  if (rows <= 0 || E < 1 || N <= 0 || K <= 0 || Ks < 0) return 0;
+  // the kernel choice of the grouped GEMM (launch_epi) and its grid
+  const bool rac = Ks > 0;
+  const SkPlan pl = skinny_plan(rows, E, N, K, Ks, epilogue, bitmap);
+  if (pl.ok) return pl.grid;
+  if (!rac) {
+    const WdPlan wp = wide_plan(rows, E, N, K, false, Ks, sfrag);
+    if (wp.ok) return wp.grid;
+  }
+  const TlPlan tp = tile_plan(rows, E, N, K, rac, Ks);
+  if (tp.ok) return tp.grid;
+  return grid_x(rows, E, true) * grid_y(N, epilogue);
+}
+
 bool qdi::gemm_takes_bitmap(int64_t rows, int32_t E, int64_t N, int64_t K, int32_t Ks,
                             int32_t epilogue) {
   if (Ks <= 0 || rows <= 0 || E < 1 || N <= 0 || K <= 0) return false;

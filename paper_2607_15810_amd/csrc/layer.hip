@@ -714,7 +714,8 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
   bool bm2 = false;                 // the W2 GEMM takes S as a bitmap
   if (!rac2) {
     st = nvfp4_quantize_act(h, QD_DTYPE_BF16, R, I, hamax,
-                            moe_w4a4_grouped_gemm_amax_count(R, 2 * I, H, E, Ks, QD_EPI_SWIGLU),
+                            qdi::gemm_amax_written(R, E, 2 * I, H, Ks, QD_EPI_SWIGLU,
+                                                   w13->scales_frag != nullptr, rank_sel),
                             &hq, nullptr, nullptr, b + L.q2_ws,
                             nvfp4_quantize_act_workspace(R, I), stream);
     if (st) return st;

@@ -123,6 +123,10 @@ extern "C" size_t nvfp4_quantize_act_workspace(int64_t rows, int64_t cols) {
   return (size_t)kAmaxPartials * sizeof(float) + 256;
 }
 
+// Up to this many amax partials the quantiser's workgroups read them directly
+// (eight loads in flight per thread); more are reduced by a launch of their own.
+constexpr int64_t kDirectPartials = 8192;
+
 extern "C" qd_status nvfp4_quantize_act(const void *x, int x_dtype, int64_t rows, int64_t cols,
                                         const float *amax_partials, int64_t n_partials,
                                         const qd_nvfp4 *out, uint64_t *rac_scores,
@@ -160,7 +164,7 @@ extern "C" qd_status nvfp4_quantize_act(const void *x, int x_dtype, int64_t rows
                          nullptr, 0, nullptr);
     ap = part;
     np = g;
-  } else if (n_partials > kAmaxPartials) {
+  } else if (n_partials > kDirectPartials) {
     qdi::launch_reduce_max(amax_partials, n_partials, part, s);
     ap = part;
     np = 1;
