@@ -437,6 +437,32 @@ def test_quantize_edge_values():
     assert_nvfp4_equal(qt, OQ.quantize(tiny.cpu().numpy()), "tiny tensor")
 
 
+@pytest.mark.parametrize("e", [-70, -30, 0, 40])
+def test_channel_scores_extreme_scales(e):
+    """The fixed-point channel scores (Eq. (channel-score), reading R2) at
+    tensor scales 2^e: at 2^-70 the squared residuals are float32 subnormals
+    whose terms trunc(r^2 * 2^F) are still large (F = 36 - 2 * exponent of
+    the tensor amax), at 2^40 F is negative.  Both the fused score pass of the
+    quantiser and the standalone one, bit for bit against the oracle."""
+    rng = np.random.default_rng(100 + e)
+    x = np_bf16(torch.from_numpy(rng.standard_normal((300, 512)).astype(np.float32) *
+                                 np.float32(2.0 ** e)).to(torch.bfloat16))
+    act = OR.rac_activation(x, 8)
+    if e == -70:
+        sq = (act["r"] * act["r"]).astype(np.float32)
+        assert np.any((sq > 0) & (sq < np.float32(2.0 ** -126)))   # subnormal squares
+    xt = bf16_tensor(x)
+    xq, scores, ramax = ops.quantize_act(xt, rac=True)
+    assert_nvfp4_equal(xq, act["xq"], "xq")
+    assert np.array_equal(scores.cpu().numpy().view(np.uint64), act["scores"])
+    assert ramax.item() == np.max(np.abs(act["r"]))
+    sel, rq, sc2, ra2 = ops.select_channels(xt, xq, 8)
+    assert np.array_equal(sc2.cpu().numpy().view(np.uint64), act["scores"])
+    assert ra2.item() == ramax.item()
+    assert np.array_equal(sel.cpu().numpy(), act["sel"])
+    assert_nvfp4_equal(rq, act["rq"], "rq")
+
+
 def test_determinism():
     inp = synth.small_moe("det", 96, 256, 8, 2, 64, 12, seed=7)
     w13 = ops.quantize_weight(inp.w13.to(DEV))
