@@ -18,7 +18,8 @@ from oracle import layer as OL, quant as OQ, rac as OR, route as ORt
 from paper_2607_15810_amd import ops, synth
 from paper_2607_15810_amd import quads as Q
 
-from helpers import assert_bank_equal, assert_nvfp4_equal, check_close_bf16, np_bf16, oracle_bank
+from helpers import (assert_bank_equal, assert_nvfp4_equal, bf16_tensor, check_close_bf16, np_bf16,
+                     oracle_bank)
 
 pytestmark = pytest.mark.gpu
 
@@ -107,6 +108,25 @@ def test_per_expert_stages_and_layer(case):
     yg = np_bf16(y).astype(np.float64)
     rel = np.linalg.norm(yg - ref["yb"]) / np.linalg.norm(ref["yb"])
     assert rel <= 1e-3, f"layer rel-L2 {rel:.3e}"
+
+
+@pytest.mark.parametrize("e", [-70, 40])
+def test_per_expert_scores_extreme_scales(e):
+    """The per-expert scores at tensor scales 2^e (subnormal squared
+    residuals at 2^-70, a negative fixed-point shift at 2^40), bit for bit."""
+    rng = np.random.default_rng(200 + e)
+    T, H, E, k, Ks = 300, 512, 8, 2, 8
+    x = bf16_tensor(rng.standard_normal((T, H)).astype(np.float32) * np.float32(2.0 ** e))
+    logits = torch.from_numpy(rng.standard_normal((T, E)).astype(np.float32)).to(DEV)
+    ids, wts, offs, row_token, inv_row = ops.route_permute(logits, k)
+    perm = ORt.permute(ORt.topk(logits.cpu().numpy(), k), E)
+    assert np.array_equal(row_token.cpu().numpy(), perm["row_token"])
+    xq, _, _ = ops.quantize_act(x)
+    act = OR.rac_activation_per_expert(np_bf16(x), Ks, perm["row_token"], perm["offsets"])
+    sel_pe, rq, rq_rows, scores, ramax = ops.select_channels_per_expert(x, xq, Ks, row_token, offs)
+    assert np.array_equal(scores.cpu().numpy().view(np.uint64), act["scores_pe"])
+    assert ramax.item() == np.max(np.abs(act["r"]))
+    assert np.array_equal(sel_pe.cpu().numpy(), act["sel_pe"])
 
 
 def test_per_expert_layer_matches_global_when_one_expert():
