@@ -188,11 +188,15 @@ __device__ __forceinline__ float wave_max(float v) {
 // floating point: sq * 2^F is exact in float wherever it is >= 1 (a
 // power-of-two scaling of a normal value into the normal range), anything
 // below 1 truncates to 0 either way, and the integer result is exact in
-// double, where sums of up to kScoreMaxRows such terms stay exact.  The clamp
-// only keeps a non-finite input's term bounded.
+// double, where sums of up to kScoreMaxRows such terms stay exact.
+// score_sum_u64 converts such a sum; its clamp only keeps the sum of a
+// non-finite input's terms in range.
 constexpr int64_t kScoreMaxRows = 1 << 16;
 __device__ __forceinline__ double fixed_point_term_f64(float sq, int F) {
-  return (double)fminf(truncf(ldexpf(sq, F)), 137438953472.0f);   // 2^37
+  return (double)truncf(ldexpf(sq, F));
+}
+__device__ __forceinline__ uint64_t score_sum_u64(double d) {
+  return (uint64_t)fmin(d, 9007199254740992.0);   // 2^53
 }
 
 // max(*addr, m) for finite m >= 0 into a float >= 0 that many workgroups

@@ -168,7 +168,7 @@ __device__ __forceinline__ void quantize_act_rows(
     // (channel 16 tx + i of row ty at 17 i + tx: consecutive tx are
     // adjacent when written, and consecutive channels 17 apart when read)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) part[ty][17 * i + tx] = (uint64_t)accd[i];
+    for (int i = 0; i < 16; ++i) part[ty][17 * i + tx] = score_sum_u64(accd[i]);
     __syncthreads();
     uint64_t s = 0;
     const int rd = 17 * (threadIdx.x & 15) + (threadIdx.x >> 4);

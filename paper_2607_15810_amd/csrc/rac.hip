@@ -87,7 +87,7 @@ __global__ __launch_bounds__(256) void rac_scores_kernel(
       if (++nrow == kScoreMaxRows) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          acc[i] += (uint64_t)accd[i];
+          acc[i] += score_sum_u64(accd[i]);
           accd[i] = 0.0;
         }
         nrow = 0;
@@ -95,7 +95,7 @@ __global__ __launch_bounds__(256) void rac_scores_kernel(
     }
   }
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc_s[ty][tx * 16 + i] = acc[i] + (uint64_t)accd[i];
+  for (int i = 0; i < 16; ++i) acc_s[ty][tx * 16 + i] = acc[i] + score_sum_u64(accd[i]);
   __syncthreads();
   uint64_t s = 0;
 #pragma unroll
@@ -368,7 +368,7 @@ __global__ __launch_bounds__(256) void rac_scores_pe_kernel(
       if (++nrow == kScoreMaxRows) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          acc[i] += (uint64_t)accd[i];
+          acc[i] += score_sum_u64(accd[i]);
           accd[i] = 0.0;
         }
         nrow = 0;
@@ -376,7 +376,7 @@ __global__ __launch_bounds__(256) void rac_scores_pe_kernel(
     }
   }
 #pragma unroll
-  for (int i = 0; i < 16; ++i) acc_s[ty][tx * 16 + i] = acc[i] + (uint64_t)accd[i];
+  for (int i = 0; i < 16; ++i) acc_s[ty][tx * 16 + i] = acc[i] + score_sum_u64(accd[i]);
   __syncthreads();
   uint64_t sum = 0;
 #pragma unroll
