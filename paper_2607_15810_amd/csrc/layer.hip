@@ -341,8 +341,9 @@ __global__ __launch_bounds__(256) void layer_resq_kernel(
 // prefill W13 kernel consumes), with the residual's tensor scale
 // (bitmap not NULL: S comes as the selection bitmap; every workgroup lists
 // it into LDS, and workgroup 0 also into sel for the GEMM)
-__global__ __launch_bounds__(256) void layer_compact_kernel(
-    const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
+// (workgroup bid of nblk)
+__device__ __forceinline__ void compact_part(
+    int bid, int nblk, const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
     const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
     const float *__restrict__ ramax, int32_t *__restrict__ sel, int Ks, int width,
     uint16_t *__restrict__ out, float *__restrict__ rgs, const uint32_t *__restrict__ bitmap) {
@@ -352,12 +353,20 @@ __global__ __launch_bounds__(256) void layer_compact_kernel(
   if (bitmap) {
     qdc::rac_list_selected(bitmap, (int)K, lsel, sh);
     __syncthreads();
-    if (blockIdx.x == 0)
+    if (bid == 0)
       for (int i = threadIdx.x; i < Ks; i += blockDim.x) sel[i] = lsel[i];
     sp = lsel;
   }
-  qdc::rac_compact_body(blockIdx.x, gridDim.x, x, xcodes, xscales, xgs, T, K, ramax, sp, Ks,
-                        width, out, rgs);
+  qdc::rac_compact_body(bid, nblk, x, xcodes, xscales, xgs, T, K, ramax, sp, Ks, width, out, rgs);
+}
+
+__global__ __launch_bounds__(256) void layer_compact_kernel(
+    const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
+    const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
+    const float *__restrict__ ramax, int32_t *__restrict__ sel, int Ks, int width,
+    uint16_t *__restrict__ out, float *__restrict__ rgs, const uint32_t *__restrict__ bitmap) {
+  compact_part(blockIdx.x, gridDim.x, x, xcodes, xscales, xgs, T, K, ramax, sel, Ks, width, out,
+               rgs, bitmap);
 }
 
 // routing scatter (nr workgroups) | RAC channel selection by rank and the
@@ -388,13 +397,13 @@ __global__ __launch_bounds__(qdc::kRankSelThreads) void layer_pre3r_kernel(
 // thread x its 16-byte piece x % 2 of grouped row x / 2; the rows after are
 // scale group y - K / 64, thread x grouped row x.  Consecutive threads write
 // consecutive 16-byte pieces.
-__global__ __launch_bounds__(256) void layer_stage_kernel(const int32_t *__restrict__ row_token,
-                                                          const uint8_t *__restrict__ codes,
-                                                          const uint8_t *__restrict__ scales,
-                                                          int64_t R, int64_t K,
-                                                          uint8_t *__restrict__ out) {
-  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t y = blockIdx.y, nst = K / 64;
+__device__ __forceinline__ void stage_part(int64_t bx, int64_t y,
+                                           const int32_t *__restrict__ row_token,
+                                           const uint8_t *__restrict__ codes,
+                                           const uint8_t *__restrict__ scales, int64_t R,
+                                           int64_t K, uint8_t *__restrict__ out) {
+  const int64_t x = bx * 256 + threadIdx.x;
+  const int64_t nst = K / 64;
   uint4 *o = reinterpret_cast<uint4 *>(out);
   if (y < nst) {
     if (x >= 2 * R) return;
@@ -406,6 +415,33 @@ __global__ __launch_bounds__(256) void layer_stage_kernel(const int32_t *__restr
     const int64_t g = y - nst;
     const int64_t t = row_token[x];
     o[R * (K / 32) + g * R + x] = *reinterpret_cast<const uint4 *>(scales + t * (K / 16) + 16 * g);
+  }
+}
+
+__global__ __launch_bounds__(256) void layer_stage_kernel(const int32_t *__restrict__ row_token,
+                                                          const uint8_t *__restrict__ codes,
+                                                          const uint8_t *__restrict__ scales,
+                                                          int64_t R, int64_t K,
+                                                          uint8_t *__restrict__ out) {
+  stage_part(blockIdx.x, blockIdx.y, row_token, codes, scales, R, K, out);
+}
+
+// the compact residual (gc workgroups) | the staged W13 operand (gxs x gys
+// workgroups of layer_stage_kernel's grid, x fastest) in one launch: the two
+// are independent and run side by side
+__global__ __launch_bounds__(256) void layer_compact_stage_kernel(
+    const uint16_t *__restrict__ x, const uint8_t *__restrict__ xcodes,
+    const uint8_t *__restrict__ xscales, const float *__restrict__ xgs, int64_t T, int64_t K,
+    const float *__restrict__ ramax, int32_t *__restrict__ sel, int Ks, int width,
+    uint16_t *__restrict__ out, float *__restrict__ rgs, const uint32_t *__restrict__ bitmap,
+    int gc, const int32_t *__restrict__ row_token, int64_t R, int64_t gxs,
+    uint8_t *__restrict__ stg) {
+  const int b = blockIdx.x;
+  if (b < gc) {
+    compact_part(b, gc, x, xcodes, xscales, xgs, T, K, ramax, sel, Ks, width, out, rgs, bitmap);
+  } else {
+    const int64_t q = b - gc;
+    stage_part(q % gxs, q / gxs, row_token, xcodes, xscales, R, K, stg);
   }
 }
 
@@ -597,6 +633,16 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
   int gx, gy;
   qdq::quant_grid(T, H, rac, gx, gy);
 
+  // the staged W13 operand (timed with the steps before the GEMM, so that
+  // the W13 stage is the GEMM launch alone); with the compact residual it is
+  // written by the same launch
+  const int64_t stg_bytes = rank_sel ? 0 : qdi::gemm_stage_bytes(R, E, 2 * I, H, Ks, QD_EPI_SWIGLU);
+  const bool staged = stg_bytes > 0 && stg_bytes <= L.stg_bytes;
+  uint8_t *stg = reinterpret_cast<uint8_t *>(b + L.stg);
+  const int64_t gxs = (2 * R + 255) / 256, gys = H / 64 + H / 256;
+  if (staged && (gxs > 0x7fffffffLL || gys > 65535 || gxs * gys > 0x7fff0000LL))
+    return QD_ERR_UNSUPPORTED;
+  bool stg_done = false;
   mark(QD_STAGE_ROUTE);
   int np = ga;      // amax partials of X
   if (blk) {
@@ -657,10 +703,19 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
       int64_t g = (total + 255) / 256;
       if (g > 8192) g = 8192;
       if (g < 1) g = 1;
-      hipLaunchKernelGGL(layer_compact_kernel, dim3((unsigned)g), dim3(256), 0, s,
-                         static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T, H,
-                         ramax, sel, Ks, width, static_cast<uint16_t *>(rq_sel), rq.gscale,
-                         rank_only ? bitmap : nullptr);
+      if (staged) {
+        hipLaunchKernelGGL(layer_compact_stage_kernel, dim3((unsigned)(g + gxs * gys)), dim3(256),
+                           0, s, static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale,
+                           T, H, ramax, sel, Ks, width, static_cast<uint16_t *>(rq_sel),
+                           rq.gscale, rank_only ? bitmap : nullptr, (int)g, row_token, R, gxs,
+                           stg);
+        stg_done = true;
+      } else {
+        hipLaunchKernelGGL(layer_compact_kernel, dim3((unsigned)g), dim3(256), 0, s,
+                           static_cast<const uint16_t *>(x), xq.codes, xq.scales, xq.gscale, T,
+                           H, ramax, sel, Ks, width, static_cast<uint16_t *>(rq_sel), rq.gscale,
+                           rank_only ? bitmap : nullptr);
+      }
     } else if (!rank_sel) {
       const int64_t total = T * (H / 16);
       int64_t g = (total + 255) / 256;
@@ -679,14 +734,7 @@ qd_status layer_impl(const void *x, const float *logits, int64_t T, int64_t H, i
   if (st) return st;
   uint16_t *h = (uint16_t *)P(QD_VIEW_H);
   float *hamax = (float *)P(QD_VIEW_H_AMAX);
-  // the staged W13 operand (timed with the steps before the GEMM, so that
-  // the W13 stage is the GEMM launch alone)
-  const int64_t stg_bytes = rank_sel ? 0 : qdi::gemm_stage_bytes(R, E, 2 * I, H, Ks, QD_EPI_SWIGLU);
-  const bool staged = stg_bytes > 0 && stg_bytes <= L.stg_bytes;
-  uint8_t *stg = reinterpret_cast<uint8_t *>(b + L.stg);
-  if (staged) {
-    const int64_t gxs = (2 * R + 255) / 256, gys = H / 64 + H / 256;
-    if (gxs > 0x7fffffffLL || gys > 65535) return QD_ERR_UNSUPPORTED;
+  if (staged && !stg_done) {
     hipLaunchKernelGGL(layer_stage_kernel, dim3((unsigned)gxs, (unsigned)gys), dim3(256), 0, s,
                        row_token, xq.codes, xq.scales, R, H, stg);
   }
