@@ -211,18 +211,19 @@ __device__ __forceinline__ void atomic_max_pos(float *addr, float m) {
 }
 
 // This thread's max over the n partial maxima (>= 0) at p, taken in steps of
-// blockDim.x: eight independent loads in flight per thread, so one round trip
-// to memory covers up to eight values per thread (the partials are read once
-// at the start of a kernel, where that latency is the kernel's critical path).
+// blockDim.x: sixteen independent loads in flight per thread, so one round
+// trip to memory covers up to sixteen values per thread (the partials are read
+// once at the start of a kernel, where that latency is the kernel's critical
+// path).
 __device__ __forceinline__ float partials_max(const float *__restrict__ p, int64_t n) {
   float m = 0.0f;
   const int64_t st = blockDim.x;
-  for (int64_t i = threadIdx.x; i < n; i += 8 * st) {
-    float v[8];
+  for (int64_t i = threadIdx.x; i < n; i += 16 * st) {
+    float v[16];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = i + j * st < n ? p[i + j * st] : 0.0f;
+    for (int j = 0; j < 16; ++j) v[j] = i + j * st < n ? p[i + j * st] : 0.0f;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) m = fmaxf(m, v[j]);
+    for (int j = 0; j < 16; ++j) m = fmaxf(m, v[j]);
   }
   return m;
 }
